@@ -1,0 +1,164 @@
+"""fp64 CPU oracle for the MoRE router (test infrastructure).
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's CPU-baseline
+leg are the only callers.  The library under `paper_2609_36301_amd` never imports this
+package, and this package never imports the library.
+
+The arithmetic lives in `oracle.c` (plain C, double precision); this module compiles it
+with gcc and wraps it with ctypes.  Every function here is argument marshalling only.
+
+Functions and the passage they follow:
+  route_lowrank   softmax(TopK(x R1 R2)), the MoRE router ("Preliminaries", MoRE layer)
+  route_fullrank  softmax(TopK(x W)), the standard router ("Preliminaries")
+  histogram       per-expert selection counts (Appendix "Training", statistic f)
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c into liboracle.so (gcc, -O2, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall",
+               "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def load_library(path: str):
+    """Open a compiled oracle library at `path` and declare its entry points."""
+    lib = ctypes.CDLL(path)
+    P = ctypes.c_void_p
+    i64, i32 = ctypes.c_int64, ctypes.c_int32
+    lib.oracle_route_lowrank.argtypes = [P, P, P, i64, i32, i32, i32, i32, P, i64, P, P, P, P, i32]
+    lib.oracle_route_lowrank.restype = ctypes.c_int
+    for name in ("oracle_route_fullrank_f64", "oracle_route_fullrank_bf16"):
+        fn = getattr(lib, name)
+        fn.argtypes = [P, P, i64, i32, i32, i32, P, i64, P, P, P, P, i32]
+        fn.restype = ctypes.c_int
+    lib.oracle_histogram.argtypes = [P, i64, i32, i32, P]
+    lib.oracle_histogram.restype = ctypes.c_int
+    return lib
+
+
+def _load(lib=None):
+    global _lib
+    if lib is not None:
+        return lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build(force=True)
+    _lib = load_library(_LIB_PATH)
+    return _lib
+
+
+_ERRORS = {1: "invalid argument", 2: "non-finite input", 3: "out of memory"}
+
+
+def _check(status: int):
+    if status != 0:
+        raise ValueError("oracle: " + _ERRORS.get(status, "error %d" % status))
+
+
+@dataclasses.dataclass
+class OracleResult:
+    idx: np.ndarray  # int32 [n][k], experts in (logit desc, index asc) order
+    gate: np.ndarray  # float64 [n][k]
+    topval: np.ndarray  # float64 [n][k], the selected logits
+    next: np.ndarray  # float64 [n], the best unselected logit (-inf when k == M)
+
+    @property
+    def kth(self) -> np.ndarray:
+        return self.topval[:, -1]
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _rows_arg(rows, T):
+    if rows is None:
+        return None, 0, T
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    return rows, rows.size, rows.size
+
+
+def _threads(threads):
+    if threads is None:
+        try:
+            return len(os.sched_getaffinity(0))
+        except AttributeError:  # pragma: no cover
+            return os.cpu_count() or 1
+    return int(threads)
+
+
+def _u16(a, shape_len=2):
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint16 or a.ndim != shape_len:
+        raise TypeError("expected a %d-D uint16 array of bfloat16 bits" % shape_len)
+    return a
+
+
+def route_lowrank(x, R1, R2, k: int, rows=None, threads=None, lib=None) -> OracleResult:
+    """x: bf16 bits [T][h]; R1: [h][r]; R2: [r][M] (row-major, mathematical orientation)."""
+    x, R1, R2 = _u16(x), _u16(R1), _u16(R2)
+    T, h = x.shape
+    h2, r = R1.shape
+    r2, M = R2.shape
+    if h2 != h or r2 != r:
+        raise ValueError("shape mismatch")
+    rows_a, nrows, n = _rows_arg(rows, T)
+    out = OracleResult(np.zeros((n, k), np.int32), np.zeros((n, k)), np.zeros((n, k)), np.zeros(n))
+    lib = _load(lib)
+    _check(lib.oracle_route_lowrank(_ptr(x), _ptr(R1), _ptr(R2), T, h, r, M, k,
+                                    None if rows_a is None else _ptr(rows_a), nrows,
+                                    _ptr(out.idx), _ptr(out.gate), _ptr(out.topval),
+                                    _ptr(out.next), _threads(threads)))
+    return out
+
+
+def route_fullrank(x, W, k: int, rows=None, threads=None, lib=None) -> OracleResult:
+    """x: bf16 bits [T][h]; W: [h][M] as float64 values or as bf16 bits (uint16)."""
+    x = _u16(x)
+    W = np.ascontiguousarray(W)
+    T, h = x.shape
+    h2, M = W.shape
+    if h2 != h:
+        raise ValueError("shape mismatch")
+    rows_a, nrows, n = _rows_arg(rows, T)
+    out = OracleResult(np.zeros((n, k), np.int32), np.zeros((n, k)), np.zeros((n, k)), np.zeros(n))
+    lib = _load(lib)
+    if W.dtype == np.uint16:
+        fn = lib.oracle_route_fullrank_bf16
+    elif W.dtype == np.float64:
+        fn = lib.oracle_route_fullrank_f64
+    else:
+        raise TypeError("W must be float64 values or uint16 bfloat16 bits")
+    _check(fn(_ptr(x), _ptr(W), T, h, M, k, None if rows_a is None else _ptr(rows_a), nrows,
+              _ptr(out.idx), _ptr(out.gate), _ptr(out.topval), _ptr(out.next), _threads(threads)))
+    return out
+
+
+def histogram(idx, M: int, lib=None) -> np.ndarray:
+    """counts[e] = number of entries of idx ([n][k] int32) equal to e."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    if idx.ndim != 2:
+        raise ValueError("idx must be [n][k]")
+    counts = np.zeros(M, np.int64)
+    _check(_load(lib).oracle_histogram(_ptr(idx), idx.shape[0], idx.shape[1], M, _ptr(counts)))
+    return counts

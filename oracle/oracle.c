@@ -1,0 +1,262 @@
+/*
+ * Router oracle: a plain, slow, fp64 evaluation of the MoRE router output.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the checker the HIP library is compared
+ * against.  Only the test suite, the smoke check and the benchmark's CPU-baseline
+ * leg may load it.  It shares no code, header, table or helper with the library.
+ *
+ * What it computes is the definition itself (Section "Preliminaries", MoRE layer):
+ *     g(x; R1, R2) = softmax(TopK(x R1 R2))
+ * written here in the library's orientation, x [T][h], R1 [h][r], R2 [r][M]
+ * (the paper writes the same product as R1_paper R2_paper x, with
+ * R1_paper = R2^T and R2_paper = R1^T; Appendix "Pseudocode", eq. for the logits).
+ * Steps, per token t:
+ *   1. decode the bfloat16 inputs exactly to double;
+ *   2. z_t = sum_j x[t][j] * R1[j][:]                        (fp64)
+ *   3. l_t[e] = sum_i z_t[i] * R2[i][e] for every expert e     (fp64; z is never narrowed)
+ *   4. S_t = the first k experts in the total order "logit descending, then expert
+ *      index ascending" (a full sort of all M candidates with qsort);
+ *   5. gate_t[j] = exp(l_(j) - l_(1)) / sum_{i<k} exp(l_(i) - l_(1))   (softmax over the k
+ *      selected logits, standard router definition in "Preliminaries");
+ *   6. also report the selected logits and l_(k+1), the best unselected logit, so the
+ *      caller can tell near-ties at the selection boundary.
+ * The full-rank entry points run steps 4-6 on logits x W with a given W [h][M]
+ * (standard router, "Preliminaries").  The histogram is the per-expert count of
+ * selections (bincount of the chosen indices, Appendix "Training", load-balancing
+ * statistic f).
+ *
+ * Non-finite inputs are rejected (return value ORACLE_ERR_NONFINITE).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define ORACLE_OK 0
+#define ORACLE_ERR_ARG 1
+#define ORACLE_ERR_NONFINITE 2
+#define ORACLE_ERR_NOMEM 3
+
+static double bf16_bits_to_double(uint16_t b) {
+    uint32_t u = ((uint32_t)b) << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* Decode n bf16 values; returns 0 if any is NaN or infinite. */
+static int decode_all(const uint16_t* src, int64_t n, double* dst) {
+    int finite = 1;
+    for (int64_t i = 0; i < n; ++i) {
+        dst[i] = bf16_bits_to_double(src[i]);
+        if (!isfinite(dst[i])) finite = 0;
+    }
+    return finite;
+}
+
+typedef struct {
+    double value;
+    int32_t expert;
+} candidate;
+
+/* Total order used for selection: larger logit first; equal logits -> smaller index first. */
+static int candidate_order(const void* pa, const void* pb) {
+    const candidate* a = (const candidate*)pa;
+    const candidate* b = (const candidate*)pb;
+    if (a->value > b->value) return -1;
+    if (a->value < b->value) return 1;
+    if (a->expert < b->expert) return -1;
+    if (a->expert > b->expert) return 1;
+    return 0;
+}
+
+/* Steps 4-6 for one token, given all M logits. */
+static void select_and_gate(const double* logit, int32_t M, int32_t k, candidate* work,
+                            int32_t* idx, double* gate, double* topval, double* next) {
+    for (int32_t e = 0; e < M; ++e) {
+        work[e].value = logit[e];
+        work[e].expert = e;
+    }
+    qsort(work, (size_t)M, sizeof(candidate), candidate_order);
+    double top = work[0].value;
+    double denom = 0.0;
+    for (int32_t j = 0; j < k; ++j) {
+        idx[j] = work[j].expert;
+        topval[j] = work[j].value;
+        gate[j] = exp(work[j].value - top);
+        denom += gate[j];
+    }
+    for (int32_t j = 0; j < k; ++j) gate[j] /= denom;
+    *next = (k < M) ? work[k].value : -INFINITY;
+}
+
+static int check_shape(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                       const int64_t* rows, int64_t nrows) {
+    if (T < 0 || h <= 0 || r <= 0 || M <= 0 || k < 1 || k > M) return 0;
+    if (rows) {
+        if (nrows < 0) return 0;
+        for (int64_t i = 0; i < nrows; ++i)
+            if (rows[i] < 0 || rows[i] >= T) return 0;
+    }
+    return 1;
+}
+
+/*
+ * Low-rank router.  x: bf16 [T][h]; R1: bf16 [h][r]; R2: bf16 [r][M]  (all row-major).
+ * rows: the tokens to evaluate (nrows of them), or NULL for all T tokens in order.
+ * Outputs, one row per evaluated token: idx int32 [n][k], gate/topval double [n][k],
+ * next double [n] (the (k+1)-th logit, -inf when k == M).
+ */
+int oracle_route_lowrank(const uint16_t* x, const uint16_t* R1, const uint16_t* R2,
+                         int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                         const int64_t* rows, int64_t nrows,
+                         int32_t* idx, double* gate, double* topval, double* next,
+                         int32_t nthreads) {
+    if (!x || !R1 || !R2 || !idx || !gate || !topval || !next) return ORACLE_ERR_ARG;
+    if (!check_shape(T, h, r, M, k, rows, nrows)) return ORACLE_ERR_ARG;
+    int64_t n = rows ? nrows : T;
+    double* r1 = (double*)malloc(sizeof(double) * (size_t)h * (size_t)r);
+    double* r2 = (double*)malloc(sizeof(double) * (size_t)r * (size_t)M);
+    if (!r1 || !r2) {
+        free(r1);
+        free(r2);
+        return ORACLE_ERR_NOMEM;
+    }
+    int ok = decode_all(R1, (int64_t)h * r, r1) & decode_all(R2, (int64_t)r * M, r2);
+    int status = ok ? ORACLE_OK : ORACLE_ERR_NONFINITE;
+    if (status == ORACLE_OK) {
+#ifdef _OPENMP
+        if (nthreads > 0) omp_set_num_threads(nthreads);
+#endif
+#pragma omp parallel
+        {
+            double* xrow = (double*)malloc(sizeof(double) * (size_t)h);
+            double* z = (double*)malloc(sizeof(double) * (size_t)r);
+            double* logit = (double*)malloc(sizeof(double) * (size_t)M);
+            candidate* work = (candidate*)malloc(sizeof(candidate) * (size_t)M);
+            int local_ok = xrow && z && logit && work;
+#pragma omp for schedule(dynamic, 4)
+            for (int64_t t = 0; t < n; ++t) {
+                if (!local_ok) continue;
+                int64_t tok = rows ? rows[t] : t;
+                if (!decode_all(x + tok * (int64_t)h, h, xrow)) {
+#pragma omp atomic write
+                    status = ORACLE_ERR_NONFINITE;
+                    continue;
+                }
+                /* step 2: z = x R1 */
+                for (int32_t i = 0; i < r; ++i) z[i] = 0.0;
+                for (int32_t j = 0; j < h; ++j) {
+                    const double* r1row = r1 + (int64_t)j * r;
+                    for (int32_t i = 0; i < r; ++i) z[i] += xrow[j] * r1row[i];
+                }
+                /* step 3: logits = z R2 */
+                for (int32_t e = 0; e < M; ++e) logit[e] = 0.0;
+                for (int32_t i = 0; i < r; ++i) {
+                    const double* r2row = r2 + (int64_t)i * M;
+                    for (int32_t e = 0; e < M; ++e) logit[e] += z[i] * r2row[e];
+                }
+                /* steps 4-6 */
+                select_and_gate(logit, M, k, work, idx + t * k, gate + t * k, topval + t * k,
+                                next + t);
+            }
+            if (!local_ok) {
+#pragma omp atomic write
+                status = ORACLE_ERR_NOMEM;
+            }
+            free(xrow);
+            free(z);
+            free(logit);
+            free(work);
+        }
+    }
+    free(r1);
+    free(r2);
+    return status;
+}
+
+/* Shared body of the two full-rank entry points; W is already decoded to double [h][M]. */
+static int fullrank_body(const uint16_t* x, const double* W, int64_t T, int32_t h, int32_t M,
+                         int32_t k, const int64_t* rows, int64_t nrows, int32_t* idx,
+                         double* gate, double* topval, double* next, int32_t nthreads) {
+    int64_t n = rows ? nrows : T;
+    int status = ORACLE_OK;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#endif
+#pragma omp parallel
+    {
+        double* xrow = (double*)malloc(sizeof(double) * (size_t)h);
+        double* logit = (double*)malloc(sizeof(double) * (size_t)M);
+        candidate* work = (candidate*)malloc(sizeof(candidate) * (size_t)M);
+        int local_ok = xrow && logit && work;
+#pragma omp for schedule(dynamic, 4)
+        for (int64_t t = 0; t < n; ++t) {
+            if (!local_ok) continue;
+            int64_t tok = rows ? rows[t] : t;
+            if (!decode_all(x + tok * (int64_t)h, h, xrow)) {
+#pragma omp atomic write
+                status = ORACLE_ERR_NONFINITE;
+                continue;
+            }
+            for (int32_t e = 0; e < M; ++e) logit[e] = 0.0;
+            for (int32_t j = 0; j < h; ++j) {
+                const double* wrow = W + (int64_t)j * M;
+                for (int32_t e = 0; e < M; ++e) logit[e] += xrow[j] * wrow[e];
+            }
+            select_and_gate(logit, M, k, work, idx + t * k, gate + t * k, topval + t * k, next + t);
+        }
+        if (!local_ok) {
+#pragma omp atomic write
+            status = ORACLE_ERR_NOMEM;
+        }
+        free(xrow);
+        free(logit);
+        free(work);
+    }
+    return status;
+}
+
+/* Full-rank router with W given in double, [h][M] row-major. */
+int oracle_route_fullrank_f64(const uint16_t* x, const double* W, int64_t T, int32_t h,
+                              int32_t M, int32_t k, const int64_t* rows, int64_t nrows,
+                              int32_t* idx, double* gate, double* topval, double* next,
+                              int32_t nthreads) {
+    if (!x || !W || !idx || !gate || !topval || !next) return ORACLE_ERR_ARG;
+    if (!check_shape(T, h, 1, M, k, rows, nrows)) return ORACLE_ERR_ARG;
+    for (int64_t i = 0; i < (int64_t)h * M; ++i)
+        if (!isfinite(W[i])) return ORACLE_ERR_NONFINITE;
+    return fullrank_body(x, W, T, h, M, k, rows, nrows, idx, gate, topval, next, nthreads);
+}
+
+/* Full-rank router with W given as bf16 bit patterns, [h][M] row-major. */
+int oracle_route_fullrank_bf16(const uint16_t* x, const uint16_t* W, int64_t T, int32_t h,
+                               int32_t M, int32_t k, const int64_t* rows, int64_t nrows,
+                               int32_t* idx, double* gate, double* topval, double* next,
+                               int32_t nthreads) {
+    if (!x || !W || !idx || !gate || !topval || !next) return ORACLE_ERR_ARG;
+    if (!check_shape(T, h, 1, M, k, rows, nrows)) return ORACLE_ERR_ARG;
+    double* w = (double*)malloc(sizeof(double) * (size_t)h * (size_t)M);
+    if (!w) return ORACLE_ERR_NOMEM;
+    int status = decode_all(W, (int64_t)h * M, w)
+                     ? fullrank_body(x, w, T, h, M, k, rows, nrows, idx, gate, topval, next,
+                                     nthreads)
+                     : ORACLE_ERR_NONFINITE;
+    free(w);
+    return status;
+}
+
+/* counts[e] = number of (token, slot) pairs with idx == e.  Out-of-range ids -> error. */
+int oracle_histogram(const int32_t* idx, int64_t n, int32_t k, int32_t M, int64_t* counts) {
+    if (!idx || !counts || n < 0 || k < 1 || M < 1) return ORACLE_ERR_ARG;
+    for (int32_t e = 0; e < M; ++e) counts[e] = 0;
+    for (int64_t i = 0; i < n * (int64_t)k; ++i) {
+        if (idx[i] < 0 || idx[i] >= M) return ORACLE_ERR_ARG;
+        counts[idx[i]] += 1;
+    }
+    return ORACLE_OK;
+}

@@ -1,0 +1,78 @@
+"""Planted mistakes in the oracle must each fail at least one pin.
+
+Every mutant is a copy of oracle/oracle.c with one plausible mistake (a dropped term, a
+wrong sign, a transposed operand, a flipped tie rule, a missing normalisation, an
+off-by-one), compiled with gcc into a temporary library.  The real oracle is untouched.
+"""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import oracle_pins
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
+
+MUTANTS = {
+    "z_drops_last_hidden_term": (
+        "for (int32_t j = 0; j < h; ++j) {\n                    const double* r1row",
+        "for (int32_t j = 0; j < h - 1; ++j) {\n                    const double* r1row"),
+    "logit_drops_last_rank_term": (
+        "for (int32_t i = 0; i < r; ++i) {\n                    const double* r2row",
+        "for (int32_t i = 0; i < r - 1; ++i) {\n                    const double* r2row"),
+    "R2_read_transposed": (
+        "logit[e] += z[i] * r2row[e];",
+        "logit[e] += z[i] * r2[(int64_t)e * r + i];"),
+    "R1_read_transposed": (
+        "z[i] += xrow[j] * r1row[i];",
+        "z[i] += xrow[j] * r1[((int64_t)i * h + j) % ((int64_t)h * r)];"),
+    "selects_smallest": (
+        "if (a->value > b->value) return -1;\n    if (a->value < b->value) return 1;",
+        "if (a->value > b->value) return 1;\n    if (a->value < b->value) return -1;"),
+    "ties_prefer_larger_index": (
+        "if (a->expert < b->expert) return -1;\n    if (a->expert > b->expert) return 1;",
+        "if (a->expert < b->expert) return 1;\n    if (a->expert > b->expert) return -1;"),
+    "softmax_sign_flipped": (
+        "gate[j] = exp(work[j].value - top);",
+        "gate[j] = exp(top - work[j].value);"),
+    "softmax_not_normalised": (
+        "for (int32_t j = 0; j < k; ++j) gate[j] /= denom;",
+        "for (int32_t j = 0; j < k; ++j) gate[j] /= (denom + 0.0 * gate[j]) * 1.0 + 0.01;"),
+    "next_is_kth_itself": (
+        "*next = (k < M) ? work[k].value : -INFINITY;",
+        "*next = (k < M) ? work[k - 1].value : -INFINITY;"),
+    "selection_off_by_one": (
+        "idx[j] = work[j].expert;\n        topval[j] = work[j].value;",
+        "idx[j] = work[j + (j + 1 < M)].expert;\n        topval[j] = work[j + (j + 1 < M)].value;"),
+    "fullrank_drops_last_hidden_term": (
+        "for (int32_t j = 0; j < h; ++j) {\n                const double* wrow",
+        "for (int32_t j = 0; j < h - 1; ++j) {\n                const double* wrow"),
+    "histogram_off_by_one": (
+        "counts[idx[i]] += 1;",
+        "counts[(idx[i] + 1) % M] += 1;"),
+}
+
+
+def _build_mutant(name, tmp_path):
+    old, new = MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, "mutation anchor for %s not found exactly once" % name
+    path = tmp_path / (name + ".c")
+    path.write_text(src.replace(old, new))
+    lib_path = tmp_path / ("lib" + name + ".so")
+    subprocess.run(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-o", str(lib_path),
+                    str(path), "-lm"], check=True)
+    return oracle.load_library(str(lib_path))
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    lib = _build_mutant(name, tmp_path)
+    failed = []
+    for check in oracle_pins.ALL_CHECKS:
+        try:
+            check(lib=lib)
+        except (AssertionError, ValueError):
+            failed.append(check.__name__)
+    assert failed, "planted mistake %r passed every pin" % name
