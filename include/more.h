@@ -1,0 +1,143 @@
+/*
+ * more.h -- C ABI of the MoRE low-rank router library for AMD Instinct MI355X (gfx950).
+ *
+ * The library computes the MoRE router output (Section "Preliminaries", MoRE layer):
+ *
+ *     g(x; R1, R2) = softmax(TopK(x R1 R2))
+ *
+ * for T tokens at once, x [T x h], R1 [h x r], R2 [r x M].  In the paper's own notation the
+ * same logits are x R2_paper^T R1_paper^T with the down-projection R2_paper (r x h) and the
+ * expert matrix R1_paper (M x r, row e = expert vector u_e); so R1 = R2_paper^T and
+ * R2 = R1_paper^T (Appendix "Pseudocode", logits equation).  TopK keeps the k largest logits
+ * of the M experts; the softmax runs over those k logits only.  The T x M logit matrix is
+ * never written to memory (Appendix "Pseudocode", inference algorithm).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Element types: bfloat16 inputs are passed as uint16_t bit patterns.  Accumulation is
+ *    fp32.  Outputs: int32 expert ids, fp32 gates and logits.
+ *  - Storage: x is row-major [T][h] (token rows).  Both router factors are passed
+ *    TRANSPOSED, i.e. in the paper's row-major orientation:
+ *        R1t = R1^T stored row-major [r][h]   (= R2_paper, one row per rank direction)
+ *        R2t = R2^T stored row-major [M][r]   (= R1_paper, one row per expert vector)
+ *    so every contraction reads contiguous rows along its reduction axis.
+ *  - Pointers are device pointers on the current HIP device unless marked "host".  Every
+ *    device pointer must be 16-byte aligned.  Inputs are read only; outputs must not alias
+ *    inputs or one another.  The caller owns and allocates every buffer, including the
+ *    workspace; the router calls never allocate, free or synchronise.
+ *  - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued on it and the
+ *    call returns after launching.  Launch failures return MORE_ERR_HIP; faults during
+ *    execution surface at the caller's next synchronisation.
+ *  - Arguments are validated on the host before anything is launched; an error status means
+ *    nothing was enqueued.  T == 0 returns MORE_OK without launching.
+ *  - Selection order: experts are ranked by logit, larger first; equal logits are ranked by
+ *    expert id, smaller first.  idx[t][0..k-1] lists the selected experts in that order.
+ *    (The paper's buffer leaves both the slot order and tie handling open; this total
+ *    order makes every plan and every run bitwise reproducible.)
+ *  - Limits: 1 <= k <= min(M, MORE_K_MAX); r in {16, 32, 64, 128}; h a positive multiple
+ *    of 16; M >= 1 (any value; the last expert tile is masked to -inf, as the paper's
+ *    inference algorithm does for out-of-range experts); T <= 2^31 - 1.
+ *  - Numerics: z = x R1 is accumulated in fp32 and carried into the expert contraction as
+ *    an unevaluated pair of bfloat16 values (hi + lo, about 16 significant bits), not
+ *    narrowed to one bfloat16 as in the paper's kernel; the logits are fp32.
+ */
+#ifndef MORE_H
+#define MORE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum more_status {
+    MORE_OK = 0,
+    MORE_ERR_INVALID_ARG = 1, /* NULL/misaligned pointer, negative or zero size, k out of range */
+    MORE_ERR_UNSUPPORTED = 2, /* valid arguments outside the limits listed above               */
+    MORE_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than the matching size query        */
+    MORE_ERR_HIP = 4          /* the HIP runtime or hipBLASLt reported an error                */
+} more_status;
+
+#define MORE_K_MAX 32
+
+/*
+ * Low-rank router (Section "Preliminaries", MoRE layer; Appendix "Pseudocode", inference
+ * algorithm).
+ *   x       bf16 [T][h]            tokens
+ *   R1t     bf16 [r][h]            R1 transposed (the paper's down-projection R2_paper)
+ *   R2t     bf16 [M][r]            R2 transposed (the paper's expert matrix R1_paper)
+ *   idx     int32 [T][k]  out      selected experts, in selection order
+ *   gate    fp32  [T][k]  out      softmax over the k selected logits, same order
+ *   topval  fp32  [T][k]  out      the selected logits, or NULL
+ *   counts  int32 [M]     out      per-expert number of selections over all T tokens
+ *                                  (overwritten), or NULL to skip
+ *   workspace / workspace_bytes    scratch of at least more_route_lowrank_workspace_size()
+ *                                  bytes (NULL/0 allowed when that size is 0)
+ */
+more_status more_route_lowrank(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
+                               int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                               int32_t* idx, float* gate, float* topval, int32_t* counts,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes more_route_lowrank needs for this shape (written to *bytes, host). */
+more_status more_route_lowrank_workspace_size(int64_t T, int32_t h, int32_t r, int32_t M,
+                                              int32_t k, size_t* bytes);
+
+/*
+ * Same as more_route_lowrank with the expert axis split into `m_chunks` slices processed by
+ * separate workgroups and merged afterwards (0 = the library's choice, 1 = no split, else a
+ * multiple of 8 up to 1024).  Every choice returns bitwise identical results; this entry
+ * point exists for tuning and for tests of that property.  Its workspace size comes from
+ * more_route_lowrank_workspace_size_ex with the same m_chunks.
+ */
+more_status more_route_lowrank_ex(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
+                                  int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                  int32_t m_chunks, int32_t* idx, float* gate, float* topval,
+                                  int32_t* counts, void* workspace, size_t workspace_bytes,
+                                  void* stream);
+more_status more_route_lowrank_workspace_size_ex(int64_t T, int32_t h, int32_t r, int32_t M,
+                                                 int32_t k, int32_t m_chunks, size_t* bytes);
+
+/* The m_chunks value the library picks for this shape (written to *m_chunks, host). */
+more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                    int32_t* m_chunks);
+
+/*
+ * Full-rank (standard) router, the baseline (Section "Preliminaries": softmax(TopK(R x)) with
+ * R in R^{M x h}).  The logits x W^T are formed with a hipBLASLt GEMM into the workspace
+ * (fp32 when logit_bits == 32, bf16 when logit_bits == 16) and a row top-k kernel then
+ * selects and normalises, as the paper's unfused standard router does.
+ *   Wt      bf16 [M][h]            the router matrix, one row per expert (the paper's R)
+ *   other arguments as in more_route_lowrank (no histogram).
+ * The library keeps one hipBLASLt handle per device, created on first use and never freed;
+ * calls may run concurrently from several threads.
+ */
+more_status more_route_fullrank(const uint16_t* x, const uint16_t* Wt, int64_t T, int32_t h,
+                                int32_t M, int32_t k, int32_t logit_bits, int32_t* idx,
+                                float* gate, float* topval, void* workspace,
+                                size_t workspace_bytes, void* stream);
+more_status more_route_fullrank_workspace_size(int64_t T, int32_t h, int32_t M, int32_t k,
+                                               int32_t logit_bits, size_t* bytes);
+
+/*
+ * Per-expert histogram of a selection (the bincount behind the load-balancing statistic,
+ * Appendix "Training"): counts[e] = #{(t, j) : idx[t][j] == e}.
+ *   idx     int32 [T][k]   selections; every entry must lie in [0, M)
+ *   counts  int32 [M] out  overwritten
+ * Entries outside [0, M) are not counted (no error is raised for them).
+ */
+more_status more_expert_histogram(const int32_t* idx, int64_t T, int32_t k, int32_t M,
+                                  int32_t* counts, void* stream);
+
+/* Static, never NULL. */
+const char* more_status_string(more_status s);
+
+/* Library version string, e.g. "0.1.0 gfx950". Static, never NULL. */
+const char* more_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MORE_H */

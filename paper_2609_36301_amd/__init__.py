@@ -1,0 +1,18 @@
+"""MoRE low-rank mixture-of-experts router for AMD Instinct MI355X (gfx950).
+
+The compute lives in libmore.so (HIP kernels behind the C ABI declared in include/more.h).
+This package holds the library, its build script (`python -m paper_2609_36301_amd.build`),
+a ctypes binding with torch tensors (`router`), and the seeded input generator (`inputs`).
+
+    from paper_2609_36301_amd import route_lowrank
+    out = route_lowrank(x, R1t, R2t, k)      # out.idx [T][k] int32, out.gate [T][k] fp32
+"""
+__all__ = ["route_lowrank", "route_fullrank", "expert_histogram", "LowrankRouter",
+           "lowrank_workspace_size", "lowrank_plan", "fullrank_workspace_size", "Routing"]
+
+
+def __getattr__(name):
+    if name in __all__:
+        from . import router
+        return getattr(router, name)
+    raise AttributeError(name)

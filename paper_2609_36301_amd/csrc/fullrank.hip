@@ -1,0 +1,194 @@
+// Full-rank (standard) router baseline: softmax(TopK(x W)) with the logits materialised.
+// ("Preliminaries", standard router; the paper's unfused router is a GEMM followed by
+// top-k and softmax as separate kernels.)
+//
+//   1. hipBLASLt GEMM  L[T][M] = x[T][h] * Wt[M][h]^T, fp32 accumulate, fp32 or bf16 output,
+//      into the caller's workspace;
+//   2. rows_topk: one wave per token row; each lane scans its strided share of the row
+//      keeping a sorted register list, then a butterfly of list merges across the wave;
+//      lane 0 applies the softmax and stores the row.
+#include <hip/hip_runtime.h>
+#include <hipblaslt/hipblaslt.h>
+#include <stdint.h>
+
+#include <map>
+#include <mutex>
+#include <tuple>
+
+#include "device_common.h"
+#include "lowrank.h"
+
+namespace more {
+
+template <int K, bool BF16>
+__global__ __launch_bounds__(256) void rows_topk_kernel(const void* __restrict__ logits, int32_t T,
+                                                        int32_t M, int32_t k,
+                                                        int32_t* __restrict__ idx,
+                                                        float* __restrict__ gate,
+                                                        float* __restrict__ topval) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= T) return;  // wave-uniform
+    float v[K];
+    int32_t ix[K];
+    list_init<K>(v, ix);
+    if (BF16) {
+        const uint16_t* L = static_cast<const uint16_t*>(logits) + row * M;
+#pragma unroll 4
+        for (int32_t e = lane; e < M; e += 64) {
+            const float x = bf16_bits_to_f32(L[e]);
+            if (x > v[K - 1]) list_insert_newer<K>(v, ix, x, e);
+        }
+    } else {
+        const float* L = static_cast<const float*>(logits) + row * M;
+#pragma unroll 4
+        for (int32_t e = lane; e < M; e += 64) {
+            const float x = L[e];
+            if (x > v[K - 1]) list_insert_newer<K>(v, ix, x, e);
+        }
+    }
+    for (int s = 1; s < 64; s <<= 1) list_merge_xor<K>(v, ix, s);
+    if (lane == 0) store_selection<K>(v, ix, k, row, idx, gate, topval);
+}
+
+// ---------------------------------------------------------------- hipBLASLt state
+namespace {
+
+struct GemmKey {
+    int device;
+    int64_t T;
+    int32_t h, M, bits;
+    bool operator<(const GemmKey& o) const {
+        return std::tie(device, T, h, M, bits) < std::tie(o.device, o.T, o.h, o.M, o.bits);
+    }
+};
+
+struct GemmEntry {
+    hipblasLtMatmulDesc_t desc = nullptr;
+    hipblasLtMatrixLayout_t la = nullptr, lb = nullptr, lc = nullptr;
+    hipblasLtMatmulHeuristicResult_t heur{};
+    bool ok = false;
+};
+
+std::mutex g_mu;
+std::map<int, hipblasLtHandle_t> g_handles;
+std::map<GemmKey, GemmEntry> g_gemms;
+
+constexpr size_t kGemmWorkspace = (size_t)64 << 20;
+
+// Returns nullptr and sets *status on failure.  Caller holds g_mu.
+GemmEntry* gemm_entry(int device, int64_t T, int32_t h, int32_t M, int32_t bits, int* status) {
+    GemmKey key{device, T, h, M, bits};
+    auto it = g_gemms.find(key);
+    if (it != g_gemms.end()) return it->second.ok ? &it->second : nullptr;
+    hipblasLtHandle_t handle;
+    auto hit = g_handles.find(device);
+    if (hit == g_handles.end()) {
+        hipblasStatus_t s = hipblasLtCreate(&handle);
+        if (s != HIPBLAS_STATUS_SUCCESS) {
+            *status = (int)s;
+            return nullptr;
+        }
+        g_handles[device] = handle;
+    } else {
+        handle = hit->second;
+    }
+    GemmEntry e;
+    hipblasStatus_t s = hipblasLtMatmulDescCreate(&e.desc, HIPBLAS_COMPUTE_32F, HIP_R_32F);
+    hipblasOperation_t opA = HIPBLAS_OP_T, opB = HIPBLAS_OP_N;
+    if (s == HIPBLAS_STATUS_SUCCESS)
+        s = hipblasLtMatmulDescSetAttribute(e.desc, HIPBLASLT_MATMUL_DESC_TRANSA, &opA, sizeof(opA));
+    if (s == HIPBLAS_STATUS_SUCCESS)
+        s = hipblasLtMatmulDescSetAttribute(e.desc, HIPBLASLT_MATMUL_DESC_TRANSB, &opB, sizeof(opB));
+    // Column-major view: A = Wt as (h x M), B = x as (h x T), D = L as (M x T).
+    if (s == HIPBLAS_STATUS_SUCCESS) s = hipblasLtMatrixLayoutCreate(&e.la, HIP_R_16BF, h, M, h);
+    if (s == HIPBLAS_STATUS_SUCCESS) s = hipblasLtMatrixLayoutCreate(&e.lb, HIP_R_16BF, h, T, h);
+    if (s == HIPBLAS_STATUS_SUCCESS)
+        s = hipblasLtMatrixLayoutCreate(&e.lc, bits == 16 ? HIP_R_16BF : HIP_R_32F, M, T, M);
+    hipblasLtMatmulPreference_t pref = nullptr;
+    if (s == HIPBLAS_STATUS_SUCCESS) s = hipblasLtMatmulPreferenceCreate(&pref);
+    uint64_t wsb = kGemmWorkspace;
+    if (s == HIPBLAS_STATUS_SUCCESS)
+        s = hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES,
+                                                  &wsb, sizeof(wsb));
+    int returned = 0;
+    if (s == HIPBLAS_STATUS_SUCCESS)
+        s = hipblasLtMatmulAlgoGetHeuristic(handle, e.desc, e.la, e.lb, e.lc, e.lc, pref, 1,
+                                            &e.heur, &returned);
+    if (pref) hipblasLtMatmulPreferenceDestroy(pref);
+    e.ok = (s == HIPBLAS_STATUS_SUCCESS && returned > 0);
+    if (!e.ok) *status = (s == HIPBLAS_STATUS_SUCCESS) ? (int)HIPBLAS_STATUS_NOT_SUPPORTED : (int)s;
+    auto ins = g_gemms.emplace(key, e).first;
+    return e.ok ? &ins->second : nullptr;
+}
+
+}  // namespace
+
+static int pow2_at_least_fr(int k) {
+    int K = 1;
+    while (K < k) K <<= 1;
+    return K;
+}
+
+bool fullrank_make_plan(int64_t T, int32_t h, int32_t M, int32_t k, int32_t logit_bits,
+                        FullrankPlan* p) {
+    (void)h;
+    FullrankPlan q{};
+    q.K = pow2_at_least_fr(k);
+    q.logit_bits = logit_bits;
+    const size_t lbytes = (size_t)T * (size_t)M * (logit_bits == 16 ? 2 : 4);
+    q.off_logits = 0;
+    q.off_gemm_ws = (lbytes + 255) & ~(size_t)255;
+    q.gemm_ws_bytes = kGemmWorkspace;
+    q.workspace_bytes = q.off_gemm_ws + q.gemm_ws_bytes;
+    *p = q;
+    return true;
+}
+
+template <int K>
+static void launch_rows(const FullrankPlan& p, const void* L, int64_t T, int32_t M, int32_t k,
+                        int32_t* idx, float* gate, float* topval, hipStream_t st) {
+    dim3 grid((unsigned)((T + 3) / 4));
+    if (p.logit_bits == 16)
+        hipLaunchKernelGGL((rows_topk_kernel<K, true>), grid, dim3(256), 0, st, L, (int32_t)T, M, k,
+                           idx, gate, topval);
+    else
+        hipLaunchKernelGGL((rows_topk_kernel<K, false>), grid, dim3(256), 0, st, L, (int32_t)T, M,
+                           k, idx, gate, topval);
+}
+
+hipError_t fullrank_launch(const FullrankPlan& p, const uint16_t* x, const uint16_t* Wt, int64_t T,
+                           int32_t h, int32_t M, int32_t k, int32_t* idx, float* gate,
+                           float* topval, void* workspace, hipStream_t st, int* blas_status) {
+    *blas_status = 0;
+    int device = 0;
+    hipError_t he = hipGetDevice(&device);
+    if (he != hipSuccess) return he;
+    char* ws = static_cast<char*>(workspace);
+    void* L = ws + p.off_logits;
+    {
+        std::lock_guard<std::mutex> lock(g_mu);
+        GemmEntry* e = gemm_entry(device, T, h, M, p.logit_bits, blas_status);
+        if (!e) return hipErrorUnknown;
+        const float alpha = 1.0f, beta = 0.0f;
+        hipblasStatus_t s = hipblasLtMatmul(g_handles[device], e->desc, &alpha, Wt, e->la, x, e->lb,
+                                            &beta, L, e->lc, L, e->lc, &e->heur.algo,
+                                            ws + p.off_gemm_ws, p.gemm_ws_bytes, st);
+        if (s != HIPBLAS_STATUS_SUCCESS) {
+            *blas_status = (int)s;
+            return hipErrorUnknown;
+        }
+    }
+    switch (p.K) {
+        case 1: launch_rows<1>(p, L, T, M, k, idx, gate, topval, st); break;
+        case 2: launch_rows<2>(p, L, T, M, k, idx, gate, topval, st); break;
+        case 4: launch_rows<4>(p, L, T, M, k, idx, gate, topval, st); break;
+        case 8: launch_rows<8>(p, L, T, M, k, idx, gate, topval, st); break;
+        case 16: launch_rows<16>(p, L, T, M, k, idx, gate, topval, st); break;
+        case 32: launch_rows<32>(p, L, T, M, k, idx, gate, topval, st); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace more

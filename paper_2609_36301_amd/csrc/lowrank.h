@@ -1,0 +1,50 @@
+// Internal interface between the C ABI layer and the low-rank router kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace more {
+
+// How one low-rank routing call is split into launches and where its scratch lives.
+struct LowrankPlan {
+    int32_t RC;               // rank chunks of 16 (r = 16 RC)
+    int32_t RT;               // 32-row tiles of the rank axis in the z pass
+    int32_t K;                // top-K list length (power of two >= k)
+    int32_t TPW;              // 32-token groups per route workgroup
+    int32_t ntb;              // token blocks of 32*TPW tokens
+    int32_t chunks;           // expert-axis chunks (1 = final output written directly)
+    int32_t hsplit;           // workgroups sharing the h axis of one token group in the z pass
+    int32_t steps_per_split;  // 16-wide h steps per z-pass workgroup
+    size_t off_zparts, off_z, off_part_v, off_part_i;
+    size_t workspace_bytes;
+};
+
+// Returns false when m_chunks is not 0, 1 or a multiple of 8 up to 1024.
+bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, int32_t m_chunks,
+                       LowrankPlan* plan);
+
+hipError_t lowrank_launch(const LowrankPlan& plan, const uint16_t* x, const uint16_t* R1t,
+                          const uint16_t* R2t, int64_t T, int32_t h, int32_t r, int32_t M,
+                          int32_t k, int32_t* idx, float* gate, float* topval, void* workspace,
+                          hipStream_t stream);
+
+hipError_t histogram_launch(const int32_t* idx, int64_t n, int32_t M, int32_t* counts,
+                            hipStream_t stream);
+
+struct FullrankPlan {
+    int32_t K;
+    int32_t logit_bits;
+    size_t off_logits, off_gemm_ws, gemm_ws_bytes;
+    size_t workspace_bytes;
+};
+
+bool fullrank_make_plan(int64_t T, int32_t h, int32_t M, int32_t k, int32_t logit_bits,
+                        FullrankPlan* plan);
+
+hipError_t fullrank_launch(const FullrankPlan& plan, const uint16_t* x, const uint16_t* Wt,
+                           int64_t T, int32_t h, int32_t M, int32_t k, int32_t* idx, float* gate,
+                           float* topval, void* workspace, hipStream_t stream, int* blas_status);
+
+}  // namespace more

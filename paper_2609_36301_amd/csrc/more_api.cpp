@@ -1,0 +1,168 @@
+// C ABI of the router library: argument validation, planning and launch.
+// Every check runs on the host before anything is enqueued, so an error status means the
+// stream was not touched.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/more.h"
+#include "lowrank.h"
+
+namespace {
+
+constexpr int64_t kMaxT = 0x7FFFFFFF;
+constexpr int32_t kMaxM = 1 << 30;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool rank_supported(int32_t r) { return r == 16 || r == 32 || r == 64 || r == 128; }
+
+more_status check_common(int64_t T, int32_t h, int32_t M, int32_t k) {
+    if (T < 0 || h <= 0 || M <= 0 || k < 1 || k > M) return MORE_ERR_INVALID_ARG;
+    if (T > kMaxT || M > kMaxM || h % 16 != 0 || k > MORE_K_MAX) return MORE_ERR_UNSUPPORTED;
+    return MORE_OK;
+}
+
+more_status check_lowrank(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                          int32_t m_chunks) {
+    if (r <= 0) return MORE_ERR_INVALID_ARG;
+    more_status s = check_common(T, h, M, k);
+    if (s != MORE_OK) return s;
+    if (!rank_supported(r)) return MORE_ERR_UNSUPPORTED;
+    if (m_chunks < 0 || (m_chunks > 1 && (m_chunks % 8 != 0 || m_chunks > 1024)))
+        return MORE_ERR_INVALID_ARG;
+    return MORE_OK;
+}
+
+more_status from_hip(hipError_t e) { return e == hipSuccess ? MORE_OK : MORE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+const char* more_status_string(more_status s) {
+    switch (s) {
+        case MORE_OK: return "MORE_OK";
+        case MORE_ERR_INVALID_ARG: return "MORE_ERR_INVALID_ARG: invalid argument";
+        case MORE_ERR_UNSUPPORTED: return "MORE_ERR_UNSUPPORTED: shape outside supported limits";
+        case MORE_ERR_WORKSPACE: return "MORE_ERR_WORKSPACE: workspace missing or too small";
+        case MORE_ERR_HIP: return "MORE_ERR_HIP: HIP runtime or hipBLASLt error";
+    }
+    return "MORE_ERR_UNKNOWN: unknown status";
+}
+
+const char* more_version(void) { return "0.1.0 gfx950"; }
+
+more_status more_route_lowrank_workspace_size_ex(int64_t T, int32_t h, int32_t r, int32_t M,
+                                                 int32_t k, int32_t m_chunks, size_t* bytes) {
+    if (!bytes) return MORE_ERR_INVALID_ARG;
+    more_status s = check_lowrank(T, h, r, M, k, m_chunks);
+    if (s != MORE_OK) return s;
+    if (T == 0) {
+        *bytes = 0;
+        return MORE_OK;
+    }
+    more::LowrankPlan p;
+    if (!more::lowrank_make_plan(T, h, r, M, k, m_chunks, &p)) return MORE_ERR_INVALID_ARG;
+    *bytes = p.workspace_bytes;
+    return MORE_OK;
+}
+
+more_status more_route_lowrank_workspace_size(int64_t T, int32_t h, int32_t r, int32_t M,
+                                              int32_t k, size_t* bytes) {
+    return more_route_lowrank_workspace_size_ex(T, h, r, M, k, 0, bytes);
+}
+
+more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                    int32_t* m_chunks) {
+    if (!m_chunks) return MORE_ERR_INVALID_ARG;
+    more_status s = check_lowrank(T, h, r, M, k, 0);
+    if (s != MORE_OK) return s;
+    more::LowrankPlan p;
+    if (!more::lowrank_make_plan(T > 0 ? T : 1, h, r, M, k, 0, &p)) return MORE_ERR_INVALID_ARG;
+    *m_chunks = p.chunks;
+    return MORE_OK;
+}
+
+more_status more_route_lowrank_ex(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
+                                  int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                  int32_t m_chunks, int32_t* idx, float* gate, float* topval,
+                                  int32_t* counts, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+    if (!x || !R1t || !R2t || !idx || !gate) return MORE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(R1t, 16) || !aligned(R2t, 16) || !aligned(idx, 4) ||
+        !aligned(gate, 4) || !aligned(topval, 4) || !aligned(counts, 4) || !aligned(workspace, 16))
+        return MORE_ERR_INVALID_ARG;
+    more_status s = check_lowrank(T, h, r, M, k, m_chunks);
+    if (s != MORE_OK) return s;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (T == 0) {
+        if (counts) return from_hip(more::histogram_launch(idx, 0, M, counts, st));
+        return MORE_OK;
+    }
+    more::LowrankPlan p;
+    if (!more::lowrank_make_plan(T, h, r, M, k, m_chunks, &p)) return MORE_ERR_INVALID_ARG;
+    if (p.workspace_bytes > 0 && (!workspace || workspace_bytes < p.workspace_bytes))
+        return MORE_ERR_WORKSPACE;
+    hipError_t e = more::lowrank_launch(p, x, R1t, R2t, T, h, r, M, k, idx, gate, topval,
+                                        workspace, st);
+    if (e != hipSuccess) return MORE_ERR_HIP;
+    if (counts) return from_hip(more::histogram_launch(idx, T * (int64_t)k, M, counts, st));
+    return MORE_OK;
+}
+
+more_status more_route_lowrank(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
+                               int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                               int32_t* idx, float* gate, float* topval, int32_t* counts,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+    return more_route_lowrank_ex(x, R1t, R2t, T, h, r, M, k, 0, idx, gate, topval, counts,
+                                 workspace, workspace_bytes, stream);
+}
+
+more_status more_route_fullrank_workspace_size(int64_t T, int32_t h, int32_t M, int32_t k,
+                                               int32_t logit_bits, size_t* bytes) {
+    if (!bytes) return MORE_ERR_INVALID_ARG;
+    more_status s = check_common(T, h, M, k);
+    if (s != MORE_OK) return s;
+    if (logit_bits != 16 && logit_bits != 32) return MORE_ERR_INVALID_ARG;
+    if (T == 0) {
+        *bytes = 0;
+        return MORE_OK;
+    }
+    more::FullrankPlan p;
+    more::fullrank_make_plan(T, h, M, k, logit_bits, &p);
+    *bytes = p.workspace_bytes;
+    return MORE_OK;
+}
+
+more_status more_route_fullrank(const uint16_t* x, const uint16_t* Wt, int64_t T, int32_t h,
+                                int32_t M, int32_t k, int32_t logit_bits, int32_t* idx,
+                                float* gate, float* topval, void* workspace,
+                                size_t workspace_bytes, void* stream) {
+    if (!x || !Wt || !idx || !gate) return MORE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(Wt, 16) || !aligned(idx, 4) || !aligned(gate, 4) ||
+        !aligned(topval, 4) || !aligned(workspace, 256))
+        return MORE_ERR_INVALID_ARG;
+    more_status s = check_common(T, h, M, k);
+    if (s != MORE_OK) return s;
+    if (logit_bits != 16 && logit_bits != 32) return MORE_ERR_INVALID_ARG;
+    if (T == 0) return MORE_OK;
+    more::FullrankPlan p;
+    more::fullrank_make_plan(T, h, M, k, logit_bits, &p);
+    if (!workspace || workspace_bytes < p.workspace_bytes) return MORE_ERR_WORKSPACE;
+    int blas = 0;
+    hipError_t e = more::fullrank_launch(p, x, Wt, T, h, M, k, idx, gate, topval, workspace,
+                                         static_cast<hipStream_t>(stream), &blas);
+    return from_hip(e);
+}
+
+more_status more_expert_histogram(const int32_t* idx, int64_t T, int32_t k, int32_t M,
+                                  int32_t* counts, void* stream) {
+    if (!counts || (!idx && T > 0)) return MORE_ERR_INVALID_ARG;
+    if (!aligned(idx, 4) || !aligned(counts, 4)) return MORE_ERR_INVALID_ARG;
+    if (T < 0 || k < 1 || M < 1) return MORE_ERR_INVALID_ARG;
+    if (T > kMaxT || M > kMaxM) return MORE_ERR_UNSUPPORTED;
+    return from_hip(more::histogram_launch(idx, T * (int64_t)k, M, counts,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,162 @@
+"""Python binding of the router library: torch tensors in, torch tensors out.
+
+Every function here only checks tensor metadata, allocates outputs and workspace with
+torch on the tensors' device, and passes raw device pointers and the current HIP stream to
+libmore.so.  All arithmetic runs in the library's HIP kernels.
+
+Layouts (see include/more.h): x [T][h] bf16; R1t = R1^T [r][h] bf16 (the paper's
+down-projection); R2t = R2^T [M][r] bf16 (the paper's expert vectors, one row per expert);
+Wt [M][h] bf16 (the full-rank router matrix, one row per expert).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+from typing import Optional
+
+import torch
+
+from . import _lib
+
+
+@dataclasses.dataclass
+class Routing:
+    idx: torch.Tensor  # int32 [T][k], experts in selection order
+    gate: torch.Tensor  # float32 [T][k], softmax over the selected logits
+    topval: Optional[torch.Tensor] = None  # float32 [T][k], the selected logits
+    counts: Optional[torch.Tensor] = None  # int32 [M], selections per expert
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _check_bf16(name: str, t: torch.Tensor, ndim: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != torch.bfloat16:
+        raise TypeError("%s must be bfloat16, got %s" % (name, t.dtype))
+    if t.dim() != ndim or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous %d-D tensor" % (name, ndim))
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on a GPU device" % name)
+
+
+def lowrank_workspace_size(T: int, h: int, r: int, M: int, k: int, m_chunks: int = 0) -> int:
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.load().more_route_lowrank_workspace_size_ex(T, h, r, M, k, m_chunks,
+                                                                ctypes.byref(n)),
+               "more_route_lowrank_workspace_size_ex")
+    return n.value
+
+
+def lowrank_plan(T: int, h: int, r: int, M: int, k: int) -> int:
+    """Number of expert-axis chunks the library picks for this shape."""
+    c = ctypes.c_int32(0)
+    _lib.check(_lib.load().more_route_lowrank_plan(T, h, r, M, k, ctypes.byref(c)),
+               "more_route_lowrank_plan")
+    return c.value
+
+
+def fullrank_workspace_size(T: int, h: int, M: int, k: int, logit_bits: int = 32) -> int:
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.load().more_route_fullrank_workspace_size(T, h, M, k, logit_bits,
+                                                              ctypes.byref(n)),
+               "more_route_fullrank_workspace_size")
+    return n.value
+
+
+class LowrankRouter:
+    """Pre-allocated outputs and workspace for repeated calls with one shape.
+
+    `__call__` only launches; results land in the tensors held by `out`.
+    """
+
+    def __init__(self, T: int, h: int, r: int, M: int, k: int, *, device=None,
+                 topval: bool = False, histogram: bool = False, m_chunks: int = 0):
+        self.shape = (T, h, r, M, k)
+        self.m_chunks = m_chunks
+        self.device = torch.device(device or "cuda")
+        dev = self.device
+        self.out = Routing(
+            idx=torch.empty((T, k), dtype=torch.int32, device=dev),
+            gate=torch.empty((T, k), dtype=torch.float32, device=dev),
+            topval=torch.empty((T, k), dtype=torch.float32, device=dev) if topval else None,
+            counts=torch.empty((M,), dtype=torch.int32, device=dev) if histogram else None,
+        )
+        nbytes = lowrank_workspace_size(T, h, r, M, k, m_chunks)
+        self.workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+        self.workspace_bytes = nbytes
+
+    def __call__(self, x: torch.Tensor, R1t: torch.Tensor, R2t: torch.Tensor) -> Routing:
+        T, h, r, M, k = self.shape
+        _check_bf16("x", x, 2)
+        _check_bf16("R1t", R1t, 2)
+        _check_bf16("R2t", R2t, 2)
+        if tuple(x.shape) != (T, h) or tuple(R1t.shape) != (r, h) or tuple(R2t.shape) != (M, r):
+            raise ValueError("shapes %s %s %s do not match the router's (T=%d, h=%d, r=%d, M=%d)"
+                             % (tuple(x.shape), tuple(R1t.shape), tuple(R2t.shape), T, h, r, M))
+        o = self.out
+        st = _lib.load().more_route_lowrank_ex(
+            _ptr(x), _ptr(R1t), _ptr(R2t), T, h, r, M, k, self.m_chunks, _ptr(o.idx),
+            _ptr(o.gate), _ptr(o.topval), _ptr(o.counts),
+            _ptr(self.workspace) if self.workspace_bytes else None, self.workspace_bytes,
+            _stream(x.device))
+        _lib.check(st, "more_route_lowrank_ex")
+        return o
+
+
+def route_lowrank(x: torch.Tensor, R1t: torch.Tensor, R2t: torch.Tensor, k: int, *,
+                  topval: bool = False, histogram: bool = False, m_chunks: int = 0) -> Routing:
+    """softmax(TopK(x R1 R2)) for every row of x; R1t = R1^T [r][h], R2t = R2^T [M][r]."""
+    _check_bf16("x", x, 2)
+    _check_bf16("R1t", R1t, 2)
+    _check_bf16("R2t", R2t, 2)
+    T, h = x.shape
+    r, h2 = R1t.shape
+    M, r2 = R2t.shape
+    if h2 != h or r2 != r:
+        raise ValueError("inconsistent shapes x %s R1t %s R2t %s"
+                         % (tuple(x.shape), tuple(R1t.shape), tuple(R2t.shape)))
+    router = LowrankRouter(T, h, r, M, k, device=x.device, topval=topval, histogram=histogram,
+                           m_chunks=m_chunks)
+    return router(x, R1t, R2t)
+
+
+def route_fullrank(x: torch.Tensor, Wt: torch.Tensor, k: int, *, topval: bool = False,
+                   logit_bits: int = 32) -> Routing:
+    """softmax(TopK(x W)) with Wt = W^T [M][h] (the standard router; logits materialised)."""
+    _check_bf16("x", x, 2)
+    _check_bf16("Wt", Wt, 2)
+    T, h = x.shape
+    M, h2 = Wt.shape
+    if h2 != h:
+        raise ValueError("inconsistent shapes x %s Wt %s" % (tuple(x.shape), tuple(Wt.shape)))
+    dev = x.device
+    out = Routing(idx=torch.empty((T, k), dtype=torch.int32, device=dev),
+                  gate=torch.empty((T, k), dtype=torch.float32, device=dev),
+                  topval=torch.empty((T, k), dtype=torch.float32, device=dev) if topval else None)
+    nbytes = fullrank_workspace_size(T, h, M, k, logit_bits)
+    ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    st = _lib.load().more_route_fullrank(_ptr(x), _ptr(Wt), T, h, M, k, logit_bits, _ptr(out.idx),
+                                         _ptr(out.gate), _ptr(out.topval), _ptr(ws), nbytes,
+                                         _stream(dev))
+    _lib.check(st, "more_route_fullrank")
+    return out
+
+
+def expert_histogram(idx: torch.Tensor, M: int) -> torch.Tensor:
+    """counts[e] = number of entries of idx (int32 [T][k]) equal to e."""
+    if idx.dtype != torch.int32 or idx.dim() != 2 or not idx.is_contiguous():
+        raise ValueError("idx must be a contiguous int32 [T][k] tensor")
+    if idx.device.type != "cuda":
+        raise ValueError("idx must be on a GPU device")
+    T, k = idx.shape
+    counts = torch.empty((M,), dtype=torch.int32, device=idx.device)
+    st = _lib.load().more_expert_histogram(_ptr(idx), T, k, M, _ptr(counts), _stream(idx.device))
+    _lib.check(st, "more_expert_histogram")
+    return counts

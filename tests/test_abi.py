@@ -1,0 +1,170 @@
+"""The C ABI on the host: symbols, validation and size queries (no GPU needed).
+
+Every call here either fails validation or is a pure host query, so nothing is launched.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36301_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "more.h")
+
+FAKE = ctypes.c_void_p(0x10000)  # aligned, never dereferenced (validation fails first)
+ODD = ctypes.c_void_p(0x10002)  # misaligned
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2609_36301_amd import build
+        build.build(verbose=False)
+    return _lib.load()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:more_status|const char\*)\s+(more_\w+)\(", text, re.M)))
+
+
+def test_header_declares_the_api():
+    names = declared_symbols()
+    for n in ("more_route_lowrank", "more_route_fullrank", "more_expert_histogram",
+              "more_route_lowrank_workspace_size", "more_status_string"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in declared_symbols():
+        assert hasattr(lib, name), name
+        assert name in _lib.SIGNATURES, "binding lacks " + name
+
+
+def test_status_strings(lib):
+    for s in range(5):
+        assert lib.more_status_string(s)
+    assert lib.more_status_string(99).startswith(b"MORE_ERR_UNKNOWN")
+    assert b"gfx950" in lib.more_version()
+
+
+def lowrank(lib, T=64, h=64, r=16, M=64, k=4, x=FAKE, R1t=FAKE, R2t=FAKE, idx=FAKE, gate=FAKE,
+            topval=None, counts=None, ws=None, wsb=0, m_chunks=0):
+    return lib.more_route_lowrank_ex(x, R1t, R2t, T, h, r, M, k, m_chunks, idx, gate, topval,
+                                     counts, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), _lib.ERR_INVALID_ARG),
+    (dict(R1t=None), _lib.ERR_INVALID_ARG),
+    (dict(R2t=None), _lib.ERR_INVALID_ARG),
+    (dict(idx=None), _lib.ERR_INVALID_ARG),
+    (dict(gate=None), _lib.ERR_INVALID_ARG),
+    (dict(x=ODD), _lib.ERR_INVALID_ARG),
+    (dict(R2t=ODD), _lib.ERR_INVALID_ARG),
+    (dict(idx=ctypes.c_void_p(0x10001)), _lib.ERR_INVALID_ARG),
+    (dict(T=-1), _lib.ERR_INVALID_ARG),
+    (dict(h=0), _lib.ERR_INVALID_ARG),
+    (dict(r=0), _lib.ERR_INVALID_ARG),
+    (dict(M=0), _lib.ERR_INVALID_ARG),
+    (dict(k=0), _lib.ERR_INVALID_ARG),
+    (dict(k=65, M=64), _lib.ERR_INVALID_ARG),
+    (dict(k=33, M=64), _lib.ERR_UNSUPPORTED),
+    (dict(r=48), _lib.ERR_UNSUPPORTED),
+    (dict(r=256), _lib.ERR_UNSUPPORTED),
+    (dict(h=72), _lib.ERR_UNSUPPORTED),
+    (dict(T=2**31), _lib.ERR_UNSUPPORTED),
+    (dict(m_chunks=3), _lib.ERR_INVALID_ARG),
+    (dict(m_chunks=2048), _lib.ERR_INVALID_ARG),
+    (dict(m_chunks=-1), _lib.ERR_INVALID_ARG),
+])
+def test_lowrank_validation(lib, kw, status):
+    assert lowrank(lib, **kw) == status
+
+
+def test_lowrank_empty_batch_is_a_no_op(lib):
+    assert lowrank(lib, T=0) == _lib.OK
+
+
+def test_lowrank_workspace_checked_before_launch(lib):
+    n = ctypes.c_size_t(0)
+    assert lib.more_route_lowrank_workspace_size_ex(1000, 512, 32, 4096, 8, 8,
+                                                    ctypes.byref(n)) == _lib.OK
+    assert n.value > 0
+    assert lowrank(lib, T=1000, h=512, r=32, M=4096, k=8, m_chunks=8) == _lib.ERR_WORKSPACE
+    assert lowrank(lib, T=1000, h=512, r=32, M=4096, k=8, m_chunks=8, ws=FAKE,
+                   wsb=n.value - 1) == _lib.ERR_WORKSPACE
+
+
+def test_workspace_size_queries(lib):
+    n = ctypes.c_size_t(123)
+    assert lib.more_route_lowrank_workspace_size(0, 512, 32, 4096, 8, ctypes.byref(n)) == _lib.OK
+    assert n.value == 0
+    assert lib.more_route_lowrank_workspace_size(16, 512, 32, 4096, 8, None) == _lib.ERR_INVALID_ARG
+    assert lib.more_route_lowrank_workspace_size(16, 512, 40, 4096, 8,
+                                                 ctypes.byref(n)) == _lib.ERR_UNSUPPORTED
+    # one big z buffer plus, for split plans, the chunk lists: grows with T
+    a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    lib.more_route_lowrank_workspace_size_ex(1024, 512, 32, 4096, 8, 8, ctypes.byref(a))
+    lib.more_route_lowrank_workspace_size_ex(2048, 512, 32, 4096, 8, 8, ctypes.byref(b))
+    assert b.value > a.value
+    f = ctypes.c_size_t(0)
+    assert lib.more_route_fullrank_workspace_size(100, 64, 1000, 4, 32, ctypes.byref(f)) == _lib.OK
+    assert f.value >= 100 * 1000 * 4
+    f16 = ctypes.c_size_t(0)
+    assert lib.more_route_fullrank_workspace_size(100, 64, 1000, 4, 16, ctypes.byref(f16)) == 0
+    assert f16.value < f.value
+    assert lib.more_route_fullrank_workspace_size(100, 64, 1000, 4, 8,
+                                                  ctypes.byref(f)) == _lib.ERR_INVALID_ARG
+
+
+def test_plans_for_the_paper_shapes(lib):
+    c = ctypes.c_int32(0)
+    plans = {}
+    for name, (T, h, r, M, k) in {"teaser": (16384, 512, 32, 4096, 8),
+                                  "mid": (32768, 2048, 64, 16384, 8),
+                                  "fine": (16384, 4096, 64, 65536, 8),
+                                  "decode": (128, 4096, 64, 262144, 16)}.items():
+        assert lib.more_route_lowrank_plan(T, h, r, M, k, ctypes.byref(c)) == _lib.OK
+        plans[name] = c.value
+    assert plans["teaser"] == 1 and plans["mid"] == 1
+    assert plans["fine"] % 8 == 0 and plans["fine"] >= 8
+    assert plans["decode"] % 8 == 0 and plans["decode"] >= 64
+
+
+def test_fullrank_validation(lib):
+    def call(**kw):
+        a = dict(x=FAKE, W=FAKE, T=10, h=64, M=100, k=4, bits=32, idx=FAKE, gate=FAKE, ws=None,
+                 wsb=0)
+        a.update(kw)
+        return lib.more_route_fullrank(a["x"], a["W"], a["T"], a["h"], a["M"], a["k"], a["bits"],
+                                       a["idx"], a["gate"], None, a["ws"], a["wsb"], None)
+    assert call(x=None) == _lib.ERR_INVALID_ARG
+    assert call(W=ODD) == _lib.ERR_INVALID_ARG
+    assert call(k=101) == _lib.ERR_INVALID_ARG
+    assert call(k=40) == _lib.ERR_UNSUPPORTED
+    assert call(bits=8) == _lib.ERR_INVALID_ARG
+    assert call() == _lib.ERR_WORKSPACE
+    assert call(T=0) == _lib.OK
+
+
+def test_histogram_validation(lib):
+    assert lib.more_expert_histogram(FAKE, 10, 4, 100, None, None) == _lib.ERR_INVALID_ARG
+    assert lib.more_expert_histogram(None, 10, 4, 100, FAKE, None) == _lib.ERR_INVALID_ARG
+    assert lib.more_expert_histogram(FAKE, -1, 4, 100, FAKE, None) == _lib.ERR_INVALID_ARG
+    assert lib.more_expert_histogram(FAKE, 10, 0, 100, FAKE, None) == _lib.ERR_INVALID_ARG
+    assert lib.more_expert_histogram(FAKE, 10, 4, 0, FAKE, None) == _lib.ERR_INVALID_ARG
+    assert lib.more_expert_histogram(ODD, 10, 4, 100, FAKE, None) == _lib.ERR_INVALID_ARG
+
+
+def test_binding_rejects_bad_tensors():
+    import torch
+    from paper_2609_36301_amd import router
+    x = torch.zeros((4, 16), dtype=torch.bfloat16)
+    with pytest.raises(ValueError):  # CPU tensors are refused before any library call
+        router.route_lowrank(x, torch.zeros((16, 16), dtype=torch.bfloat16),
+                             torch.zeros((8, 16), dtype=torch.bfloat16), 2)
+    with pytest.raises(TypeError):
+        router.route_lowrank(x.float(), x, x, 2)

@@ -1,0 +1,75 @@
+"""GPU parity of the full-rank baseline router and of the expert histogram (marked `gpu`)."""
+import numpy as np
+import pytest
+
+import oracle
+import parity
+from gpu_util import announce, require_gpu, to_dev
+from paper_2609_36301_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits, make_inputs
+
+pytestmark = pytest.mark.gpu
+
+
+def _w_bf16(inp):
+    """W = R1 R2 formed in fp64 on the host, rounded to bf16 ([h][M])."""
+    W = bf16_bits_to_f32(inp.R1).astype(np.float64) @ bf16_bits_to_f32(inp.R2).astype(np.float64)
+    return f32_to_bf16_bits(W.astype(np.float32))
+
+
+def _fullrank(inp, Wb, k, bits, tag):
+    torch = require_gpu()
+    from paper_2609_36301_amd import router
+    T, h = inp.x.shape
+    M = Wb.shape[1]
+    announce("%s route_fullrank T=%d h=%d M=%d k=%d logit_bits=%d" % (tag, T, h, M, k, bits))
+    out = router.route_fullrank(to_dev(inp.x), to_dev(np.ascontiguousarray(Wb.T)), k,
+                                topval=True, logit_bits=bits)
+    torch.cuda.synchronize()
+    return out.idx.cpu().numpy(), out.gate.cpu().numpy(), out.topval.cpu().numpy()
+
+
+@pytest.mark.parametrize("shape", [(16384, 512, 32, 4096, 8), (333, 128, 16, 1000, 5),
+                                   (64, 64, 16, 33, 32), (1, 32, 16, 7, 1)],
+                         ids=lambda s: "T%d_h%d_M%d_k%d" % (s[0], s[1], s[3], s[4]))
+def test_fullrank_fp32_logits_parity(shape):
+    T, h, r, M, k = shape
+    inp = make_inputs(T, h, r, M, seed=5)
+    Wb = _w_bf16(inp)
+    idx, gate, topval = _fullrank(inp, Wb, k, 32, "fullrank")
+    rows = np.arange(T) if T <= 4096 else np.sort(
+        np.random.default_rng(0).choice(T, 3000, replace=False))
+    orc = oracle.route_fullrank(inp.x, Wb, k, rows=rows)
+    rep = parity.compare(orc, idx[rows], gate[rows], k, M)
+    print("[parity] fullrank %s %s" % (shape, rep), flush=True)
+    assert rep.ok(), str(rep)
+
+
+def test_fullrank_bf16_logits_valid():
+    T, h, r, M, k = 2000, 512, 32, 4096, 8
+    inp = make_inputs(T, h, r, M, seed=6)
+    Wb = _w_bf16(inp)
+    idx, gate, _ = _fullrank(inp, Wb, k, 16, "fullrank-bf16")
+    parity.check_valid(idx, gate, M)
+    orc = oracle.route_fullrank(inp.x, Wb, k)
+    same = np.all(np.sort(orc.idx, 1) == np.sort(idx, 1), axis=1)
+    # bf16 logits carry 8 significant bits: most sets still agree
+    assert same.mean() > 0.8, same.mean()
+
+
+@pytest.mark.parametrize("M,T,k,skew", [(64, 1000, 4, False), (16384, 32768, 8, False),
+                                        (65536, 16384, 8, True), (262144, 128, 16, False),
+                                        (100, 0, 3, False)])
+def test_histogram(M, T, k, skew):
+    torch = require_gpu()
+    from paper_2609_36301_amd import router
+    rng = np.random.default_rng(M + T)
+    if skew:  # 40% of all selections on one expert
+        idx = rng.integers(0, M, size=(T, k)).astype(np.int32)
+        idx[:, 0] = np.where(rng.random(T) < 0.4 * k, 7, idx[:, 0])
+    else:
+        idx = rng.integers(0, M, size=(T, k)).astype(np.int32)
+    announce("expert_histogram T=%d k=%d M=%d" % (T, k, M))
+    counts = router.expert_histogram(to_dev(idx), M)
+    torch.cuda.synchronize()
+    c = counts.cpu().numpy()
+    assert np.array_equal(c, oracle.histogram(idx, M).astype(np.int32))
