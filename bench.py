@@ -1,0 +1,214 @@
+"""Benchmark of the fused low-rank MoE router on one MI355X.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one full low-rank routing call (softmax(TopK(x R1 R2)) for T tokens, plus the
+per-expert histogram for the workloads that carry one) over one batch of synthetic inputs.
+Inputs are resident in HBM before timing starts; consecutive steps rotate over enough
+distinct input batches (> 256 MB in total) that each step reads its batch from HBM rather
+than from the last-level cache.  K steps are timed with HIP events on the stream the
+library launches on, bracketed by device synchronisation.
+
+Printed: one JSON line with routed tokens/s, the roofline position of the routing call,
+the full-rank router measured on the same inputs, and the fp64 CPU oracle timed on a
+bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "routed tokens/sec (fused low-rank router) + % of roofline; speedup vs full-rank"
+PEAK_HBM_GBS = 8000.0  # MI355X HBM3E, GB/s
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+MALL_BYTES = 256 << 20
+
+
+def algorithmic(w):
+    """Bytes and flops one routing call must move / execute (no T x M traffic)."""
+    nbytes = 2 * w.T * w.h + 2 * w.h * w.r + 2 * w.r * w.M + 8 * w.T * w.k
+    if w.histogram:
+        nbytes += 4 * w.M
+    flops = 2 * w.T * w.r * (w.h + w.M)
+    return nbytes, flops
+
+
+def roofline(w, seconds):
+    nbytes, flops = algorithmic(w)
+    t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
+    t_mfma = flops / (PEAK_BF16_TFLOPS * 1e12)
+    if t_hbm >= t_mfma:
+        achieved = nbytes / seconds / 1e9
+        return {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+    achieved = flops / seconds / 1e12
+    return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+
+
+def timed(fn, steps, warmup, stream):
+    """Seconds per call of fn(i), eager launches (for calls much longer than launch cost)."""
+    import torch
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for i in range(steps):
+        fn(i)
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / 1e3 / steps
+
+
+def timed_graph(fn, steps, warmup):
+    """Seconds per step, with the `steps` timed steps captured in one HIP graph.
+
+    Host launch cost per routing call (ctypes + checks) exceeds the kernels' run time, so
+    eager launches would time the host.  The graph holds exactly the library's launches for
+    `steps` consecutive steps; after `warmup` eager steps it is replayed once untimed, then
+    once inside the timed region.
+    """
+    import torch
+    for i in range(warmup):
+        fn(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(steps):
+            fn(i)
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    g.replay()
+    end.record(stream)
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / 1e3 / steps
+
+
+def cpu_baseline(w, inp, budget_s=12.0):
+    """fp64 oracle on a bounded token sample of the same workload (all host cores)."""
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    n = min(w.T, 64)
+    t0 = time.perf_counter()
+    oracle.route_lowrank(inp.x[:n], inp.R1, inp.R2, w.k, threads=cores)
+    per_tok = (time.perf_counter() - t0) / n
+    n = int(min(w.T, max(n, budget_s / max(per_tok, 1e-9))))
+    t0 = time.perf_counter()
+    oracle.route_lowrank(inp.x[:n], inp.R1, inp.R2, w.k, threads=cores)
+    dt = time.perf_counter() - t0
+    return {"value": round(n / dt, 1), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": "first %d of %d tokens of the same workload, fp64, %.1f s wall" % (n, w.T, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="teaser_prefill")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fullrank", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: the router runs data-parallel over tokens, so "
+              "each GPU routes its own token shard with no communication; --gpus %d is not "
+              "supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_36301_amd import router
+    from paper_2609_36301_amd.inputs import WORKLOADS, make_workload_inputs, transposed_factors
+
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    inp = make_workload_inputs(w)
+    R1t, R2t = transposed_factors(inp)
+
+    def to_dev(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).view(torch.bfloat16).to(dev)
+
+    x0, r1, r2 = to_dev(inp.x), to_dev(R1t), to_dev(R2t)
+    per_batch = 2 * (x0.numel() + r1.numel() + r2.numel())
+    nbuf = max(2, min(64, math.ceil(1.5 * MALL_BYTES / per_batch)))
+    # distinct batches: rows of x and expert rows of R2t rolled by a different offset each
+    bufs = []
+    for b in range(nbuf):
+        bufs.append((torch.roll(x0, shifts=b * 97, dims=0).contiguous(),
+                     torch.roll(r1, shifts=b, dims=1).contiguous(),
+                     torch.roll(r2, shifts=b * 13, dims=0).contiguous()))
+    torch.cuda.synchronize()
+
+    lr = router.LowrankRouter(w.T, w.h, w.r, w.M, w.k, device=dev, histogram=w.histogram)
+    stream = torch.cuda.current_stream(dev)
+
+    def step(i):
+        xb, r1b, r2b = bufs[i % nbuf]
+        lr(xb, r1b, r2b)
+
+    sec = timed_graph(step, args.steps, args.warmup)
+    plan_chunks = router.lowrank_plan(w.T, w.h, w.r, w.M, w.k)
+
+    result = {
+        "metric": METRIC,
+        "value": round(w.T / sec, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(sec * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "T": w.T, "h": w.h, "r": w.r, "M": w.M, "k": w.k,
+                   "histogram": w.histogram, "expert_chunks": plan_chunks,
+                   "rotating_batches": nbuf, "launch": "hip graph of the timed steps"},
+        "roofline": roofline(w, sec),
+    }
+
+    if not args.no_fullrank:
+        # full-rank router on the same token batches with W = R1 R2 rounded to bf16; logits
+        # materialised in fp32 and in bf16; the speedup uses the faster of the two.
+        from paper_2609_36301_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
+        W = bf16_bits_to_f32(inp.R1).astype(np.float64) @ bf16_bits_to_f32(inp.R2).astype(
+            np.float64)
+        Wt = to_dev(np.ascontiguousarray(f32_to_bf16_bits(W.astype(np.float32)).T))
+        fr = {}
+        for bits, key in ((32, "fp32_logits_ms"), (16, "bf16_logits_ms")):
+            frr = router.FullrankRouter(w.T, w.h, w.M, w.k, device=dev, logit_bits=bits)
+            fr[key] = round(timed(lambda i: frr(bufs[i % nbuf][0], Wt),
+                                  max(5, args.steps // 10), 3, stream) * 1e3, 5)
+            del frr
+            torch.cuda.empty_cache()
+        best = min(fr["fp32_logits_ms"], fr["bf16_logits_ms"])
+        fr["speedup_lowrank_vs_fullrank"] = round(best / (sec * 1e3), 3)
+        fr["speedup_target"] = round(w.M / (2 * w.r) * w.h / (w.h + w.M), 3)
+        result["fullrank"] = fr
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, inp)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -54,21 +54,16 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) {
     return __builtin_bit_cast(float, b << 16);
 }
 
-// Split eight fp32 values into bf16 hi = bf16(z) and lo = bf16(z - hi).  z - hi is exact
-// in fp32, so hi + lo carries about 16 significant bits of z.
+// Split eight fp32 values into bf16 hi = bf16(z) and lo = bf16(z - hi), both rounded to
+// nearest even (v_cvt_pk_bf16_f32).  z - hi is exact in fp32, so hi + lo carries about 16
+// significant bits of z.
 __device__ __forceinline__ void split_hi_lo(const float (&z)[8], bf16x8& hi, bf16x8& lo) {
-    u32x4 h, l;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        uint32_t h0 = f32_to_bf16_bits(z[2 * q]);
-        uint32_t h1 = f32_to_bf16_bits(z[2 * q + 1]);
-        uint32_t l0 = f32_to_bf16_bits(z[2 * q] - bf16_bits_to_f32(h0));
-        uint32_t l1 = f32_to_bf16_bits(z[2 * q + 1] - bf16_bits_to_f32(h1));
-        h[q] = h0 | (h1 << 16);
-        l[q] = l0 | (l1 << 16);
+    for (int q = 0; q < 8; ++q) {
+        const __bf16 h = (__bf16)z[q];
+        hi[q] = h;
+        lo[q] = (__bf16)(z[q] - (float)h);
     }
-    hi = __builtin_bit_cast(bf16x8, h);
-    lo = __builtin_bit_cast(bf16x8, l);
 }
 
 // ---------------------------------------------------------------- top-K lists
@@ -98,6 +93,21 @@ __device__ __forceinline__ void list_insert_newer(float (&v)[K], int32_t (&ix)[K
 #pragma unroll
     for (int j = 0; j < K; ++j) {
         bool b = nv > v[j];
+        float tv = v[j];
+        int32_t ti = ix[j];
+        v[j] = b ? nv : tv;
+        ix[j] = b ? ni : ti;
+        nv = b ? tv : nv;
+        ni = b ? ti : ni;
+    }
+}
+
+// Insert any candidate (general position in the selection order); the last pair falls off.
+template <int K>
+__device__ __forceinline__ void list_insert(float (&v)[K], int32_t (&ix)[K], float nv, int32_t ni) {
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+        bool b = better(nv, ni, v[j], ix[j]);
         float tv = v[j];
         int32_t ti = ix[j];
         v[j] = b ? nv : tv;

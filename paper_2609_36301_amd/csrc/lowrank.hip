@@ -57,16 +57,26 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
     for (int pt = 0; pt < RT; ++pt) acc[pt] = zero_f32x16();
 
     const uint16_t* xrow = x + (tok_ok ? tok : 0) * (int64_t)h + 8 * half;
-#pragma unroll 4
-    for (int s = ws0; s < ws1; ++s) {
-        bf16x8 b = tok_ok ? load_bf16x8(xrow + 16 * s) : zero_bf16x8();
+    // Operands of 8 consecutive h steps are loaded before their MFMAs so that each wave keeps
+    // 8 x 16 bytes of x per lane in flight; steps past the wave's range contribute zeros.
+    for (int s = ws0; s < ws1; s += 8) {
+        bf16x8 b[8], a[8][RT];
 #pragma unroll
-        for (int pt = 0; pt < RT; ++pt) {
-            const int row = 32 * pt + prow;
-            bf16x8 a = row < r ? load_bf16x8(R1t + (int64_t)row * h + 16 * s + 8 * half)
+        for (int u = 0; u < 8; ++u) {
+            const bool ok = s + u < ws1;
+            b[u] = (ok && tok_ok) ? load_bf16x8(xrow + 16 * (s + u)) : zero_bf16x8();
+#pragma unroll
+            for (int pt = 0; pt < RT; ++pt) {
+                const int row = 32 * pt + prow;
+                a[u][pt] = (ok && row < r)
+                               ? load_bf16x8(R1t + (int64_t)row * h + 16 * (s + u) + 8 * half)
                                : zero_bf16x8();
-            acc[pt] = mfma_32x32x16(a, b, acc[pt]);
+            }
         }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+            for (int pt = 0; pt < RT; ++pt) acc[pt] = mfma_32x32x16(a[u][pt], b[u], acc[pt]);
     }
 
     __shared__ f32x16 red[3][RT][64];
@@ -119,16 +129,268 @@ __global__ __launch_bounds__(256) void zreduce_kernel(const float* __restrict__ 
 // ------------------------------------------------------------------------------ route
 constexpr int kRouteWaves = 8;
 
+// Shared-memory layout of one route workgroup (NT tokens, lists of K).
+template <int K, int TPW>
+struct RouteSmem {
+    static constexpr int NT = 32 * TPW;                // tokens of the workgroup
+    static constexpr int LPT = 2 * kRouteWaves;        // lanes that see a token's experts
+    static constexpr int BL = (2 * K + LPT - 1) / LPT; // screening buckets per lane
+    static constexpr int NB = LPT * BL;                // screening buckets per token (>= 2K)
+    static constexpr int S = K <= 8 ? 4 : 8;           // private candidate slots per lane
+    static constexpr int OCAP = 2 * K + 16;            // shared overflow slots per token
+    // Per-token rows have an odd length in 32-bit words so that the 32-64 tokens handled
+    // side by side in a wave fall on different LDS banks.
+    static constexpr int NBP = NB + 1;
+    static constexpr int SLP = LPT * S + 1;
+    static constexpr int OCP = OCAP + 1;
+    struct Fast {
+        float bucket[NT][NBP];
+        float theta[NT];
+        int32_t lane_count[NT][LPT + 1];
+        int32_t ovf_count[NT];
+        int32_t fallback;
+        float slot_v[NT][SLP];
+        int32_t slot_i[NT][SLP];
+        float ovf_v[NT][OCP];
+        int32_t ovf_i[NT][OCP];
+    };
+    struct Exact {
+        float sv[kRouteWaves / 2][TPW][32][K];
+        int32_t si[kRouteWaves / 2][TPW][32][K];
+    };
+    static constexpr size_t bytes = sizeof(Fast) > sizeof(Exact) ? sizeof(Fast) : sizeof(Exact);
+};
+
+template <int RC, int K, int TPW>
+struct RouteLane {
+    bf16x8 zhi[TPW][RC], zlo[TPW][RC];
+};
+
+// z for the lane's token(s) (rows tb*TPW*32 + g*32 + n of the z workspace), split into
+// hi/lo bf16 B operands; tokens past T get zeros.
+template <int RC, int K, int TPW>
+__device__ __forceinline__ void load_z_operands(const float* __restrict__ z, int32_t T, int tb,
+                                                int n, int half, RouteLane<RC, K, TPW>& zl) {
+    constexpr int R = 16 * RC;
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) {
+        const int64_t tok = ((int64_t)tb * TPW + g) * 32 + n;
+#pragma unroll
+        for (int c = 0; c < RC; ++c) {
+            float v[8];
+            if (tok < T) {
+                const f32x4* p = reinterpret_cast<const f32x4*>(z + tok * R + 16 * c + 8 * half);
+                const f32x4 a0 = p[0], a1 = p[1];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    v[q] = a0[q];
+                    v[4 + q] = a1[q];
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 8; ++q) v[q] = 0.0f;
+            }
+            split_hi_lo(v, zl.zhi[g][c], zl.zlo[g][c]);
+        }
+    }
+}
+
+// A operand of expert tile t: expert row t*32 + n, K half `half` of each 16-wide rank chunk.
+template <int RC>
+__device__ __forceinline__ void load_expert_rows(const uint16_t* __restrict__ R2t, int32_t M,
+                                                 int64_t t, int n, int half, bf16x8 (&a)[RC]) {
+    constexpr int R = 16 * RC;
+    const int64_t e = t * 32 + n;
+    if (e < M) {
+        const uint16_t* p = R2t + e * R + 8 * half;
+#pragma unroll
+        for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(p + 16 * c);
+    } else {
+#pragma unroll
+        for (int c = 0; c < RC; ++c) a[c] = zero_bf16x8();
+    }
+}
+
+__device__ __forceinline__ void mask_past_end(f32x16& acc, int32_t e0, int32_t M, int half) {
+    if (e0 + 32 > M) {
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+            if (e0 + acc_row(j, half) >= M) acc[j] = -__builtin_huge_valf();
+    }
+}
+
+__device__ __forceinline__ float max16(const f32x16& a) {
+    float m = fmaxf(fmaxf(a[0], a[1]), a[2]);
+    m = fmaxf(fmaxf(m, a[3]), a[4]);
+    m = fmaxf(fmaxf(m, a[5]), a[6]);
+    m = fmaxf(fmaxf(m, a[7]), a[8]);
+    m = fmaxf(fmaxf(m, a[9]), a[10]);
+    m = fmaxf(fmaxf(m, a[11]), a[12]);
+    m = fmaxf(fmaxf(m, a[13]), a[14]);
+    return fmaxf(m, a[15]);
+}
+
+// Tile loop helper: calls body(a, e0, partial) for the wave's tiles [wb, we); only the
+// tile that crosses M (at most one, the last) is visited with partial = true, so full tiles
+// carry no bounds checks.  The A operands of the next D tiles are kept in flight in a
+// register ring while the current tile is processed.
+template <int RC>
+struct TileDepth {
+    static constexpr int D = RC <= 2 ? 4 : 2;
+};
+
+template <int RC, typename Body>
+__device__ __forceinline__ void for_each_tile(const uint16_t* __restrict__ R2t, int32_t M,
+                                              int64_t wb, int64_t we, int n, int half,
+                                              Body&& body) {
+    constexpr int D = TileDepth<RC>::D;
+    const int64_t full_end = we < (int64_t)(M / 32) ? we : (int64_t)(M / 32);
+    if (wb < full_end) {
+        bf16x8 ring[D][RC];
+#pragma unroll
+        for (int d = 0; d < D; ++d)
+            if (wb + d < full_end) load_expert_rows<RC>(R2t, M, wb + d, n, half, ring[d]);
+        for (int64_t t = wb; t < full_end; t += D) {
+#pragma unroll
+            for (int d = 0; d < D; ++d) {
+                if (t + d < full_end) {
+                    body(ring[d], (int32_t)((t + d) * 32), false);
+                    if (t + d + D < full_end)
+                        load_expert_rows<RC>(R2t, M, t + d + D, n, half, ring[d]);
+                }
+            }
+        }
+    }
+    if (full_end < we && full_end >= wb) {  // the partial last tile
+        bf16x8 a[RC];
+        load_expert_rows<RC>(R2t, M, full_end, n, half, a);
+        body(a, (int32_t)(full_end * 32), true);
+    }
+}
+
+// Exact path: every lane keeps a sorted register list of its token over its own experts,
+// inserting every logit that beats the list's last entry; lists are then merged across the
+// two K halves and across the waves.  Used when the screened path cannot certify a token.
+template <int RC, int K, int TPW, bool FINAL>
+__device__ __noinline__ void route_exact(const float* __restrict__ z,
+                            const uint16_t* __restrict__ R2t,
+                            int32_t T, int32_t M, int32_t k, int tb, int chunk, int64_t wb,
+                            int64_t we, int w, char* smem, int32_t* __restrict__ idx,
+                            float* __restrict__ gate, float* __restrict__ topval,
+                            float* __restrict__ part_v, int32_t* __restrict__ part_i) {
+    using S = RouteSmem<K, TPW>;
+    auto& sm = *reinterpret_cast<typename S::Exact*>(smem);
+    const int lane = threadIdx.x & 63;
+    const int n = lane & 31;
+    const int half = lane >> 5;
+    RouteLane<RC, K, TPW> zl;
+    load_z_operands<RC, K, TPW>(z, T, tb, n, half, zl);
+    float lv[TPW][K];
+    int32_t li[TPW][K];
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) list_init<K>(lv[g], li[g]);
+    for_each_tile<RC>(R2t, M, wb, we, n, half, [&](const bf16x8 (&a)[RC], int32_t e0, bool partial) {
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            f32x16 acc = zero_f32x16();
+#pragma unroll
+            for (int c = 0; c < RC; ++c) {
+                acc = mfma_32x32x16(a[c], zl.zhi[g][c], acc);
+                acc = mfma_32x32x16(a[c], zl.zlo[g][c], acc);
+            }
+            if (partial) mask_past_end(acc, e0, M, half);
+            if (max16(acc) > lv[g][K - 1]) {
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    if (acc[j] > lv[g][K - 1])
+                        list_insert_newer<K>(lv[g], li[g], acc[j], e0 + acc_row(j, half));
+                }
+            }
+        }
+    });
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) list_merge_xor<K>(lv[g], li[g], 32);
+#pragma unroll
+    for (int s = kRouteWaves / 2; s >= 1; s >>= 1) {
+        if (w >= s && w < 2 * s && half == 0) {
+#pragma unroll
+            for (int g = 0; g < TPW; ++g) {
+#pragma unroll
+                for (int j = 0; j < K; ++j) {
+                    sm.sv[w - s][g][n][j] = lv[g][j];
+                    sm.si[w - s][g][n][j] = li[g][j];
+                }
+            }
+        }
+        __syncthreads();
+        if (w < s) {
+#pragma unroll
+            for (int g = 0; g < TPW; ++g) {
+                float pv[K];
+                int32_t pi[K];
+#pragma unroll
+                for (int j = 0; j < K; ++j) {
+                    pv[j] = sm.sv[w][g][n][j];
+                    pi[j] = sm.si[w][g][n][j];
+                }
+                list_merge<K>(lv[g], li[g], pv, pi);
+            }
+        }
+        __syncthreads();
+    }
+    if (w == 0 && half == 0) {
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            const int64_t tok = ((int64_t)tb * TPW + g) * 32 + n;
+            if (tok >= T) continue;
+            if (FINAL) {
+                store_selection<K>(lv[g], li[g], k, tok, idx, gate, topval);
+            } else {
+                const int64_t base = ((int64_t)chunk * T + tok) * K;
+#pragma unroll
+                for (int j = 0; j < K; ++j) {
+                    part_v[base + j] = lv[g][j];
+                    part_i[base + j] = li[g][j];
+                }
+            }
+        }
+    }
+}
+
+// Route one block of 32*TPW tokens over one chunk of the expert axis.
+//
+// Screened path, in three steps:
+//  1. screening sweep with z_hi only (one MFMA per rank chunk): each lane keeps the maximum
+//     of its experts' screened logits in BL buckets (tiles assigned round robin).  The K-th
+//     largest of a token's NB >= 2K bucket maxima comes from K distinct experts, so it is a
+//     lower bound on the token's K-th largest screened logit; lowered by a 2^-6 relative
+//     margin it becomes the candidate threshold theta;
+//  2. exact sweep with z_hi + z_lo: every logit above theta is appended to the lane's
+//     private candidate slots in LDS (a shared per-token overflow area takes the rest);
+//  3. each token's candidates are ranked under the selection order; ranks < K are the
+//     result.
+// Certificate: if a token has at least k candidates, every logit >= its k-th largest is above
+// theta and therefore a candidate, so the result is exact.  Otherwise (or if the overflow
+// area fills) the whole workgroup recomputes its tokens on the exact path.
 template <int RC, int K, int TPW, bool FINAL>
 __global__ __launch_bounds__(kRouteWaves * 64) void route_kernel(
     const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
     int32_t k, int32_t chunks, int32_t ntb, int32_t* __restrict__ idx, float* __restrict__ gate,
     float* __restrict__ topval, float* __restrict__ part_v, int32_t* __restrict__ part_i) {
+    using S = RouteSmem<K, TPW>;
     constexpr int R = 16 * RC;
-    const int lane = threadIdx.x & 63;
-    const int w = threadIdx.x >> 6;
+    constexpr int NT = S::NT, NB = S::NB, BL = S::BL, SL = S::S, OCAP = S::OCAP, LPT = S::LPT;
+    constexpr int NTHREADS = kRouteWaves * 64;
+    constexpr int TPT = NTHREADS / NT;  // threads per token when ranking bucket maxima
+    __shared__ __attribute__((aligned(16))) char smem[S::bytes];
+    auto& sm = *reinterpret_cast<typename S::Fast*>(smem);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31;
     const int half = lane >> 5;
+    const int ls = w * 2 + half;  // this lane's index among the lanes of its token
 
     // Workgroup -> (token block, expert chunk).  With chunks a multiple of 8, the chunk's
     // low three bits equal the XCD the workgroup is dispatched to (workgroups are dealt to
@@ -143,138 +405,159 @@ __global__ __launch_bounds__(kRouteWaves * 64) void route_kernel(
         tb = local % ntb;
         chunk = (blockIdx.x & 7) + 8 * (local / ntb);
     }
+    if (tid < NT) sm.ovf_count[tid] = 0;
+    if (tid == 0) sm.fallback = 0;
 
     // z for the lane's token(s), split into hi/lo bf16 B operands.
-    bf16x8 zhi[TPW][RC], zlo[TPW][RC];
-#pragma unroll
-    for (int g = 0; g < TPW; ++g) {
-        const int64_t tok = ((int64_t)tb * TPW + g) * 32 + n;
-#pragma unroll
-        for (int c = 0; c < RC; ++c) {
-            float v[8];
-            if (tok < T) {
-                const f32x4* p = reinterpret_cast<const f32x4*>(z + tok * R + 16 * c + 8 * half);
-                f32x4 a0 = p[0], a1 = p[1];
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    v[q] = a0[q];
-                    v[4 + q] = a1[q];
-                }
-            } else {
-#pragma unroll
-                for (int q = 0; q < 8; ++q) v[q] = 0.0f;
-            }
-            split_hi_lo(v, zhi[g][c], zlo[g][c]);
-        }
-    }
+    RouteLane<RC, K, TPW> zl;
+    load_z_operands<RC, K, TPW>(z, T, tb, n, half, zl);
 
-    // This wave's range of 32-expert tiles.
+    // This wave's range of 32-expert tiles inside the chunk (wave-uniform).
     const int64_t Mt = (M + 31) / 32;
     const int64_t cb = Mt * chunk / chunks;
     const int64_t ce = Mt * (chunk + 1) / chunks;
     const int64_t wb = cb + (ce - cb) * w / kRouteWaves;
     const int64_t we = cb + (ce - cb) * (w + 1) / kRouteWaves;
 
-    float lv[TPW][K];
-    int32_t li[TPW][K];
+    // ---- step 1: screening maxima
+    float bm[TPW][BL];
 #pragma unroll
-    for (int g = 0; g < TPW; ++g) list_init<K>(lv[g], li[g]);
-
-    // A operand of tile t: expert row t*32 + n, K half `half` of each 16-wide rank chunk.
-    auto load_a = [&](int64_t t, bf16x8 (&a)[RC]) {
-        const int64_t e = t * 32 + n;
-        if (e < M) {
-            const uint16_t* p = R2t + e * R + 8 * half;
+    for (int g = 0; g < TPW; ++g)
 #pragma unroll
-            for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(p + 16 * c);
-        } else {
-#pragma unroll
-            for (int c = 0; c < RC; ++c) a[c] = zero_bf16x8();
-        }
-    };
-
-    bf16x8 a_cur[RC], a_nxt[RC];
-    if (wb < we) load_a(wb, a_cur);
-    for (int64_t t = wb; t < we; ++t) {
-        if (t + 1 < we) load_a(t + 1, a_nxt);
-        const int32_t e0 = (int32_t)(t * 32);
+        for (int b = 0; b < BL; ++b) bm[g][b] = -__builtin_huge_valf();
+    for_each_tile<RC>(R2t, M, wb, we, n, half, [&](const bf16x8 (&a)[RC], int32_t e0, bool partial) {
+        const int bsel = BL == 1 ? 0 : (int)(((e0 >> 5) - wb) % BL);
+        f32x16 acc[TPW];
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
-            f32x16 acc = zero_f32x16();
+            acc[g] = zero_f32x16();
+#pragma unroll
+            for (int c = 0; c < RC; ++c) acc[g] = mfma_32x32x16(a[c], zl.zhi[g][c], acc[g]);
+        }
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            if (partial) mask_past_end(acc[g], e0, M, half);
+            const float mx = max16(acc[g]);
+#pragma unroll
+            for (int b = 0; b < BL; ++b)
+                if (b == bsel) bm[g][b] = fmaxf(bm[g][b], mx);
+        }
+    });
+#pragma unroll
+    for (int g = 0; g < TPW; ++g)
+#pragma unroll
+        for (int b = 0; b < BL; ++b) sm.bucket[g * 32 + n][ls * BL + b] = bm[g][b];
+    __syncthreads();
+
+    // theta per token: the bucket maximum of rank K-1 (ties ranked by position), lowered.
+    {
+        const int tt = tid / TPT, sub = tid % TPT;
+        for (int q = sub; q < NB; q += TPT) {
+            const float v = sm.bucket[tt][q];
+            int rank = 0;
+            for (int i = 0; i < NB; ++i) {
+                const float u = sm.bucket[tt][i];
+                rank += (u > v || (u == v && i < q)) ? 1 : 0;
+            }
+            if (rank == K - 1) sm.theta[tt] = v - fabsf(v) * 0x1p-6f;
+        }
+    }
+    __syncthreads();
+
+    // ---- step 2: exact sweep, candidates above theta into the lane's slots
+    float th[TPW];
+    int32_t cnt[TPW];
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) {
+        th[g] = sm.theta[g * 32 + n];
+        cnt[g] = 0;
+    }
+    for_each_tile<RC>(R2t, M, wb, we, n, half, [&](const bf16x8 (&a)[RC], int32_t e0, bool partial) {
+        f32x16 acc[TPW];
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            acc[g] = zero_f32x16();
 #pragma unroll
             for (int c = 0; c < RC; ++c) {
-                acc = mfma_32x32x16(a_cur[c], zhi[g][c], acc);
-                acc = mfma_32x32x16(a_cur[c], zlo[g][c], acc);
-            }
-            if (e0 + 32 > M) {  // last tile: experts past M do not exist
-#pragma unroll
-                for (int j = 0; j < 16; ++j)
-                    if (e0 + acc_row(j, half) >= M) acc[j] = -__builtin_huge_valf();
-            }
-            float mx = acc[0];
-#pragma unroll
-            for (int j = 1; j < 16; ++j) mx = fmaxf(mx, acc[j]);
-            if (mx > lv[g][K - 1]) {
-#pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    if (acc[j] > lv[g][K - 1])
-                        list_insert_newer<K>(lv[g], li[g], acc[j], e0 + acc_row(j, half));
-                }
+                acc[g] = mfma_32x32x16(a[c], zl.zhi[g][c], acc[g]);
+                acc[g] = mfma_32x32x16(a[c], zl.zlo[g][c], acc[g]);
             }
         }
-#pragma unroll
-        for (int c = 0; c < RC; ++c) a_cur[c] = a_nxt[c];
-    }
-
-    // The two K halves of a lane pair saw disjoint expert rows of the same token.
-#pragma unroll
-    for (int g = 0; g < TPW; ++g) list_merge_xor<K>(lv[g], li[g], 32);
-
-    // Tree merge across the waves of the workgroup through LDS.
-    __shared__ float sv[kRouteWaves / 2][TPW][32][K];
-    __shared__ int32_t si[kRouteWaves / 2][TPW][32][K];
-#pragma unroll
-    for (int s = kRouteWaves / 2; s >= 1; s >>= 1) {
-        if (w >= s && w < 2 * s && half == 0) {
-#pragma unroll
-            for (int g = 0; g < TPW; ++g) {
-#pragma unroll
-                for (int j = 0; j < K; ++j) {
-                    sv[w - s][g][n][j] = lv[g][j];
-                    si[w - s][g][n][j] = li[g][j];
-                }
-            }
-        }
-        __syncthreads();
-        if (w < s) {
-#pragma unroll
-            for (int g = 0; g < TPW; ++g) {
-                float pv[K];
-                int32_t pi[K];
-#pragma unroll
-                for (int j = 0; j < K; ++j) {
-                    pv[j] = sv[w][g][n][j];
-                    pi[j] = si[w][g][n][j];
-                }
-                list_merge<K>(lv[g], li[g], pv, pi);
-            }
-        }
-        __syncthreads();
-    }
-
-    if (w == 0 && half == 0) {
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
-            const int64_t tok = ((int64_t)tb * TPW + g) * 32 + n;
-            if (tok >= T) continue;
+            if (partial) mask_past_end(acc[g], e0, M, half);
+            if (max16(acc[g]) > th[g]) {
+                const int tl = g * 32 + n;
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    if (acc[g][j] > th[g]) {
+                        const int32_t e = e0 + acc_row(j, half);
+                        if (cnt[g] < SL) {
+                            sm.slot_v[tl][ls * SL + cnt[g]] = acc[g][j];
+                            sm.slot_i[tl][ls * SL + cnt[g]] = e;
+                        } else {
+                            const int o = atomicAdd(&sm.ovf_count[tl], 1);
+                            if (o < OCAP) {
+                                sm.ovf_v[tl][o] = acc[g][j];
+                                sm.ovf_i[tl][o] = e;
+                            }
+                        }
+                        ++cnt[g];
+                    }
+                }
+            }
+        }
+    });
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) sm.lane_count[g * 32 + n][ls] = cnt[g] < SL ? cnt[g] : SL;
+    __syncthreads();
+
+    // ---- step 3: one thread per token keeps the best K of its candidates; certificate
+    float lv[K];
+    int32_t li[K];
+    if (tid < NT) {
+        list_init<K>(lv, li);
+        int P = 0;
+        for (int l = 0; l < LPT; ++l) {
+            const int c = sm.lane_count[tid][l];
+            P += c;
+            for (int q = 0; q < c; ++q) {
+                const float v = sm.slot_v[tid][l * SL + q];
+                const int32_t e = sm.slot_i[tid][l * SL + q];
+                if (better(v, e, lv[K - 1], li[K - 1])) list_insert<K>(lv, li, v, e);
+            }
+        }
+        const int ovf = sm.ovf_count[tid];
+        const int no = ovf < OCAP ? ovf : OCAP;
+        P += no;
+        for (int q = 0; q < no; ++q) {
+            const float v = sm.ovf_v[tid][q];
+            const int32_t e = sm.ovf_i[tid][q];
+            if (better(v, e, lv[K - 1], li[K - 1])) list_insert<K>(lv, li, v, e);
+        }
+        const bool all_in = sm.theta[tid] == -__builtin_huge_valf();  // nothing screened out
+        const bool tok_ok = (int64_t)tb * NT + tid < T;
+        if (tok_ok && (ovf > OCAP || (P < k && !all_in))) atomicOr(&sm.fallback, 1);
+    }
+    __syncthreads();
+
+    if (sm.fallback) {  // workgroup-uniform
+        __syncthreads();
+        route_exact<RC, K, TPW, FINAL>(z, R2t, T, M, k, tb, chunk, wb, we, w, smem, idx, gate,
+                                       topval, part_v, part_i);
+        return;
+    }
+    if (tid < NT) {
+        const int64_t tok = (int64_t)tb * NT + tid;
+        if (tok < T) {
             if (FINAL) {
-                store_selection<K>(lv[g], li[g], k, tok, idx, gate, topval);
+                store_selection<K>(lv, li, k, tok, idx, gate, topval);
             } else {
                 const int64_t base = ((int64_t)chunk * T + tok) * K;
 #pragma unroll
                 for (int j = 0; j < K; ++j) {
-                    part_v[base + j] = lv[g][j];
-                    part_i[base + j] = li[g][j];
+                    part_v[base + j] = lv[j];
+                    part_i[base + j] = li[j];
                 }
             }
         }
@@ -326,7 +609,7 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     q.RC = r / 16;
     q.RT = (q.RC + 1) / 2;
     q.K = pow2_at_least(k);
-    q.TPW = (q.RC <= 4 && q.K <= 16) ? 2 : 1;
+    q.TPW = (q.RC <= 4 && q.K <= 8) ? 2 : 1;
     q.ntb = (int32_t)((T + 32 * q.TPW - 1) / (32 * q.TPW));
     const int64_t Mt = ((int64_t)M + 31) / 32;
     if (m_chunks > 0) {
@@ -386,7 +669,7 @@ template <int RC, int K>
 static void launch_route(const LowrankPlan& p, const float* z, const uint16_t* R2t, int64_t T,
                          int32_t M, int32_t k, int32_t* idx, float* gate, float* topval,
                          float* pv, int32_t* pi, hipStream_t st) {
-    constexpr int TPW = (RC <= 4 && K <= 16) ? 2 : 1;
+    constexpr int TPW = (RC <= 4 && K <= 8) ? 2 : 1;
     dim3 grid((unsigned)((int64_t)p.ntb * p.chunks)), block(kRouteWaves * 64);
     if (p.chunks == 1)
         hipLaunchKernelGGL((route_kernel<RC, K, TPW, true>), grid, block, 0, st, z, R2t,

@@ -4,7 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/more.h"
+#include "more.h"
 #include "lowrank.h"
 
 namespace {

@@ -127,6 +127,38 @@ def route_lowrank(x: torch.Tensor, R1t: torch.Tensor, R2t: torch.Tensor, k: int,
     return router(x, R1t, R2t)
 
 
+class FullrankRouter:
+    """Pre-allocated outputs and workspace (logits + GEMM scratch) for the full-rank router."""
+
+    def __init__(self, T: int, h: int, M: int, k: int, *, device=None, topval: bool = False,
+                 logit_bits: int = 32):
+        self.shape = (T, h, M, k)
+        self.logit_bits = logit_bits
+        dev = torch.device(device or "cuda")
+        self.out = Routing(
+            idx=torch.empty((T, k), dtype=torch.int32, device=dev),
+            gate=torch.empty((T, k), dtype=torch.float32, device=dev),
+            topval=torch.empty((T, k), dtype=torch.float32, device=dev) if topval else None)
+        self.workspace_bytes = fullrank_workspace_size(T, h, M, k, logit_bits)
+        self.workspace = torch.empty((max(self.workspace_bytes, 1),), dtype=torch.uint8,
+                                     device=dev)
+
+    def __call__(self, x: torch.Tensor, Wt: torch.Tensor) -> Routing:
+        T, h, M, k = self.shape
+        _check_bf16("x", x, 2)
+        _check_bf16("Wt", Wt, 2)
+        if tuple(x.shape) != (T, h) or tuple(Wt.shape) != (M, h):
+            raise ValueError("shapes %s %s do not match (T=%d, h=%d, M=%d)"
+                             % (tuple(x.shape), tuple(Wt.shape), T, h, M))
+        o = self.out
+        st = _lib.load().more_route_fullrank(_ptr(x), _ptr(Wt), T, h, M, k, self.logit_bits,
+                                             _ptr(o.idx), _ptr(o.gate), _ptr(o.topval),
+                                             _ptr(self.workspace), self.workspace_bytes,
+                                             _stream(x.device))
+        _lib.check(st, "more_route_fullrank")
+        return o
+
+
 def route_fullrank(x: torch.Tensor, Wt: torch.Tensor, k: int, *, topval: bool = False,
                    logit_bits: int = 32) -> Routing:
     """softmax(TopK(x W)) with Wt = W^T [M][h] (the standard router; logits materialised)."""
@@ -136,17 +168,7 @@ def route_fullrank(x: torch.Tensor, Wt: torch.Tensor, k: int, *, topval: bool = 
     M, h2 = Wt.shape
     if h2 != h:
         raise ValueError("inconsistent shapes x %s Wt %s" % (tuple(x.shape), tuple(Wt.shape)))
-    dev = x.device
-    out = Routing(idx=torch.empty((T, k), dtype=torch.int32, device=dev),
-                  gate=torch.empty((T, k), dtype=torch.float32, device=dev),
-                  topval=torch.empty((T, k), dtype=torch.float32, device=dev) if topval else None)
-    nbytes = fullrank_workspace_size(T, h, M, k, logit_bits)
-    ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
-    st = _lib.load().more_route_fullrank(_ptr(x), _ptr(Wt), T, h, M, k, logit_bits, _ptr(out.idx),
-                                         _ptr(out.gate), _ptr(out.topval), _ptr(ws), nbytes,
-                                         _stream(dev))
-    _lib.check(st, "more_route_fullrank")
-    return out
+    return FullrankRouter(T, h, M, k, device=x.device, topval=topval, logit_bits=logit_bits)(x, Wt)
 
 
 def expert_histogram(idx: torch.Tensor, M: int) -> torch.Tensor:

@@ -181,3 +181,61 @@ def test_proposition1_top1_and_counts_on_gpu():
     idx8, _, _, counts = route_lowrank(inp, g["k"], histogram=True, tag="prop1 k=8")
     assert counts.sum() == n * g["k"]
     assert np.abs(counts - g["mean_count"]).max() <= g["bound"]
+
+
+def test_graph_capture_replays_match_eager():
+    """Three routing calls captured in one HIP graph; every replay equals the eager result."""
+    import torch
+    from gpu_util import require_gpu, to_dev, announce
+    from paper_2609_36301_amd import router
+    from paper_2609_36301_amd.inputs import transposed_factors
+    require_gpu()
+    shapes = [(700, 512, 32, 4096, 8, 0), (300, 256, 64, 20000, 16, 16)]
+    routers, args, eager = [], [], []
+    for T, h, r, M, k, chunks in shapes:
+        inp = make_inputs(T, h, r, M, seed=T)
+        R1t, R2t = transposed_factors(inp)
+        a = (to_dev(inp.x), to_dev(R1t), to_dev(R2t))
+        lr = router.LowrankRouter(T, h, r, M, k, histogram=True, topval=True, m_chunks=chunks)
+        announce("graph eager T=%d M=%d chunks=%d" % (T, M, chunks))
+        o = lr(*a)
+        torch.cuda.synchronize()
+        eager.append([t.clone() for t in (o.idx, o.gate, o.topval, o.counts)])
+        routers.append(lr)
+        args.append(a)
+    announce("graph capture")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for lr, a in zip(routers, args):
+            lr(*a)
+    for rep in range(3):
+        for lr in routers:  # scribble over outputs between replays
+            lr.out.idx.fill_(-1)
+            lr.out.gate.fill_(-1.0)
+            lr.out.counts.fill_(12345)
+        torch.cuda.synchronize()
+        announce("graph replay %d" % rep)
+        g.replay()
+        torch.cuda.synchronize()
+        for lr, ref in zip(routers, eager):
+            o = lr.out
+            for got, want in zip((o.idx, o.gate, o.topval, o.counts), ref):
+                assert torch.equal(got, want), "replay %d differs from eager" % rep
+        _ = torch.ones(1000, device="cuda").sum().item()  # eager work between replays
+
+
+@pytest.mark.parametrize("chunks", [0, 8])
+def test_uncertified_tokens_recomputed_exactly(chunks):
+    """Zero-vector tokens have all logits equal to 0: the screened candidate pool is empty,
+    the certificate fails and the workgroup recomputes on the exact path.  Expected result:
+    experts 0..k-1 (ties go to the lower id), gates 1/k; neighbours stay correct."""
+    T, h, r, M, k = 300, 256, 32, 2000, 8
+    inp = make_inputs(T, h, r, M, seed=3)
+    zero_rows = [5, 77, 200, 299]
+    inp.x[zero_rows] = 0
+    idx, gate, topval, _ = route_lowrank(inp, k, m_chunks=chunks, tag="degenerate")
+    for t in zero_rows:
+        assert np.array_equal(idx[t], np.arange(k, dtype=np.int32))
+        assert np.allclose(gate[t], 1.0 / k, atol=1e-7)
+        assert np.all(topval[t] == 0.0)
+    _check(inp, k, idx, gate, topval, label="degenerate")
