@@ -34,12 +34,15 @@
  *    expert id, smaller first.  idx[t][0..k-1] lists the selected experts in that order.
  *    (The paper's buffer leaves both the slot order and tie handling open; this total
  *    order makes every plan and every run bitwise reproducible.)
- *  - Limits: 1 <= k <= min(M, MORE_K_MAX); r in {16, 32, 64, 128}; h a positive multiple
- *    of 16; M >= 1 (any value; the last expert tile is masked to -inf, as the paper's
- *    inference algorithm does for out-of-range experts); T <= 2^31 - 1.
- *  - Numerics: z = x R1 is accumulated in fp32 and carried into the expert contraction as
- *    an unevaluated pair of bfloat16 values (hi + lo, about 16 significant bits), not
- *    narrowed to one bfloat16 as in the paper's kernel; the logits are fp32.
+ *  - Limits: 1 <= k <= min(M, MORE_K_MAX) for the full-rank router and
+ *    1 <= k <= min(M, MORE_LOWRANK_K_MAX) for the low-rank router; r in {16, 32, 64}; h a
+ *    positive multiple of 16; M >= 1 (any value; the last expert tile is masked to -inf, as
+ *    the paper's inference algorithm does for out-of-range experts); T <= 2^31 - 1.
+ *  - Numerics: z = x R1 is accumulated in fp32.  The expert sweeps run on the matrix cores
+ *    with z rounded to bfloat16 and a rigorous bound on the resulting logit error, which
+ *    selects a small candidate set that provably holds the top k; the candidates' logits
+ *    are then evaluated exactly in fp32 (fp32 z times the bfloat16 expert rows).  The paper's
+ *    kernel instead narrows z to one bfloat16 for the whole contraction.
  */
 #ifndef MORE_H
 #define MORE_H
@@ -60,6 +63,7 @@ typedef enum more_status {
 } more_status;
 
 #define MORE_K_MAX 32
+#define MORE_LOWRANK_K_MAX 16
 
 /*
  * Low-rank router (Section "Preliminaries", MoRE layer; Appendix "Pseudocode", inference
@@ -85,10 +89,11 @@ more_status more_route_lowrank_workspace_size(int64_t T, int32_t h, int32_t r, i
                                               int32_t k, size_t* bytes);
 
 /*
- * Same as more_route_lowrank with the expert axis split into `m_chunks` slices processed by
- * separate workgroups and merged afterwards (0 = the library's choice, 1 = no split, else a
- * multiple of 8 up to 1024).  Every choice returns bitwise identical results; this entry
- * point exists for tuning and for tests of that property.  Its workspace size comes from
+ * Same as more_route_lowrank with the expert axis split into (at least) `m_chunks` slices
+ * processed by separate workgroups and merged afterwards (0 = the library's choice, 1 = no
+ * split, else a multiple of 8 up to 1024; the library raises it when a slice would not fit in
+ * one workgroup's LDS).  Every choice returns bitwise identical results; this entry point
+ * exists for tuning and for tests of that property.  Its workspace size comes from
  * more_route_lowrank_workspace_size_ex with the same m_chunks.
  */
 more_status more_route_lowrank_ex(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,

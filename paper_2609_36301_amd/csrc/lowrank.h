@@ -12,12 +12,13 @@ struct LowrankPlan {
     int32_t RC;               // rank chunks of 16 (r = 16 RC)
     int32_t RT;               // 32-row tiles of the rank axis in the z pass
     int32_t K;                // top-K list length (power of two >= k)
-    int32_t ntb;              // token blocks of 256 tokens (route workgroups per chunk)
-    int32_t chunks;           // expert-axis chunks (at most 65536 experts each)
+    int32_t ntb;              // token blocks of 512 tokens
+    int32_t chunks;           // expert-axis chunks, each resident in one workgroup's LDS
+    int32_t splits;           // token-block ranges per chunk (route grid = chunks * splits)
     int32_t theta_group;      // threads per token in the threshold kernel
     int32_t cap;              // candidate slots per token
     int32_t hsplit;           // workgroups sharing the h axis of one token group in the z pass
-    int32_t steps_per_split;  // 16-wide h steps per z-pass workgroup
+    int32_t steps_per_split;  // 64-wide h chunks per z-pass workgroup
     size_t off_zparts, off_z, off_top, off_gnorm, off_tau, off_count, off_cand;
     size_t workspace_bytes;
 };

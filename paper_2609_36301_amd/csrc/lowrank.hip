@@ -2,7 +2,7 @@
 // T x M logits (Appendix "Pseudocode", inference algorithm; MoRE layer in "Preliminaries").
 //
 // Pipeline of one call:
-//   zpass    z = x R1 (fp32 accumulate) for 32-token groups; the h axis may be split over
+//   zpass    z = x R1 (fp32 accumulate) for 128-token blocks; the h axis may be split over
 //            several workgroups (hsplit > 1), each writing a partial z;
 //   zreduce  sums the partials in a fixed order (only when hsplit > 1);
 //   route    for a block of 32*NW tokens and a chunk of the expert axis: logits
@@ -32,90 +32,174 @@
 
 namespace more {
 
+// Calls f(std::integral_constant<int, i>) for i = 0 .. N-1 (compile-time positions).
+template <typename F, int... I>
+__device__ __forceinline__ void unroll_impl(F&& f, std::integer_sequence<int, I...>) {
+    (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void unroll(F&& f) {
+    unroll_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 // ------------------------------------------------------------------------------ zpass
-template <int RT>
+// One workgroup = 4 waves = 128 tokens, wave w owning tokens 32w..32w+31 of the block.  The h
+// axis is walked in chunks of 64 (4 MFMA k-steps); the chunk of R1 (all rank rows) is staged
+// in LDS and shared by the four waves, x is prefetched D chunks ahead in registers.  With
+// hsplit > 1 the chunks are split over hsplit workgroups and each split writes a partial z.
+constexpr int kZWaves = 4;
+constexpr int kZTokens = 32 * kZWaves;
+constexpr int kZChunk = 64;
+
+// Group norms: gnorm[g] = (largest Euclidean norm among expert rows 4g..4g+3 of R2t) rounded
+// up, for every group of the rows < `rows` (all tiles); rows past M count as zero.  Lane (row, 16-byte segment) layout: the
+// r/8 segments of a row sit in consecutive lanes and the 4 rows of a group next to each other.
+template <int SPR>
+__device__ __forceinline__ void group_norms(const uint16_t* __restrict__ R2t, int32_t M,
+                                            int64_t rows, int64_t gid, float* __restrict__ gnorm) {
+    constexpr int R = 8 * SPR;
+    const int64_t row = gid / SPR;
+    const int col = (int)(gid % SPR);
+    float ss = 0.0f;
+    if (row < M) {
+        const bf16x8 v = load_bf16x8(R2t + row * R + col * 8);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) ss = fmaf((float)v[q], (float)v[q], ss);
+    }
+#pragma unroll
+    for (int m = 1; m < SPR; m <<= 1) ss += __shfl_xor(ss, m, kWave);
+    ss = fmaxf(ss, __shfl_xor(ss, SPR, kWave));
+    ss = fmaxf(ss, __shfl_xor(ss, 2 * SPR, kWave));
+    if (col == 0 && (row & 3) == 0 && row < rows) gnorm[row / 4] = sqrtf(ss) * (1.0f + 0x1p-20f);
+}
+
+template <int RT, int D>
 __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__ x,
                                                     const uint16_t* __restrict__ R1t,
                                                     float* __restrict__ zout, int32_t T, int32_t h,
-                                                    int32_t r, int32_t steps_per_split) {
-    const int lane = threadIdx.x & 63;
-    const int w = threadIdx.x >> 6;
+                                                    int32_t r, int32_t chunks_per_split,
+                                                    const uint16_t* __restrict__ R2t, int32_t M,
+                                                    int32_t zblocks, int32_t hsplit,
+                                                    float* __restrict__ gnorm) {
+    // Workgroups [0, zblocks * hsplit) compute z (token block bx % zblocks, h split
+    // bx / zblocks); the rest compute group norms.
+    if ((int)blockIdx.x >= zblocks * hsplit) {  // workgroup-uniform: a group-norm workgroup
+        const int64_t gid = ((int64_t)blockIdx.x - (int64_t)zblocks * hsplit) * 256 + threadIdx.x;
+        const int64_t rows = ((int64_t)M + 31) / 32 * 32;
+        switch (r) {
+            case 16: group_norms<2>(R2t, M, rows, gid, gnorm); break;
+            case 32: group_norms<4>(R2t, M, rows, gid, gnorm); break;
+            case 64: group_norms<8>(R2t, M, rows, gid, gnorm); break;
+        }
+        return;
+    }
+    constexpr int RR = 32 * RT;         // rank rows held by the MFMA tiles (r rounded up)
+    constexpr int LROW = kZChunk + 8;   // padded LDS row of R1, bf16 elements
+    constexpr int RLOADS = RR * (kZChunk / 8) / 256;  // 16-byte R1 segments per thread
+    __shared__ __attribute__((aligned(16))) uint16_t r1s[2][RR * LROW];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
     const int n = lane & 31;
     const int half = lane >> 5;
-    const int64_t tok = (int64_t)blockIdx.x * 32 + n;
+    const int zb = (int)(blockIdx.x % (unsigned)zblocks);
+    const int split = (int)(blockIdx.x / (unsigned)zblocks);
+    const int64_t tok = ((int64_t)zb * kZWaves + w) * 32 + n;
     const bool tok_ok = tok < T;
-    const int S = h >> 4;
-    const int s0 = blockIdx.y * steps_per_split;
-    const int s1 = min(S, s0 + steps_per_split);
-    const int len = max(0, s1 - s0);
-    const int ws0 = s0 + (len * w) / 4;
-    const int ws1 = s0 + (len * (w + 1)) / 4;
+    const int S = h >> 4;               // 16-wide k-steps
+    const int NC = (S + 3) / 4;         // 64-wide chunks
+    const int cbeg = split * chunks_per_split;
+    const int nc = max(0, min(NC, cbeg + chunks_per_split) - cbeg);
 
     const int jm = n >> 3, qm = (n >> 2) & 1, im = n & 3;
     const int prow = 16 * (jm >> 1) + 8 * qm + 4 * (jm & 1) + im;
 
+    // All loads are issued unconditionally with clamped addresses (chunks past the range
+    // re-read the last step, rows past r re-read row r - 1), so that every lane issues the
+    // same loads and the compiler can keep D chunks in flight.  Clamped values never reach a
+    // stored result: their MFMAs are skipped, or they land in rank rows that are not stored.
+    const uint16_t* xrow = x + (tok_ok ? tok : 0) * (int64_t)h + 8 * half;
+    u32x4 xb[D][4];
+    auto xload = [&](auto slot, int c) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            int step = 4 * (cbeg + c) + j;
+            step = step < S ? step : S - 1;
+            xb[decltype(slot)::value][j] = *reinterpret_cast<const u32x4*>(xrow + 16 * step);
+        }
+    };
+    u32x4 rb[RLOADS];
+    auto rload = [&](int c) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < RLOADS; ++i) {
+            const int seg = tid + 256 * i;
+            const int row = seg >> 3, col = seg & 7;
+            const int rr = row < r ? row : r - 1;
+            int hc = (cbeg + c) * kZChunk + col * 8;
+            hc = hc < h ? hc : h - 8;
+            rb[i] = *reinterpret_cast<const u32x4*>(R1t + (int64_t)rr * h + hc);
+        }
+    };
+    auto rstash = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < RLOADS; ++i) {
+            const int seg = tid + 256 * i;
+            const int row = seg >> 3, col = seg & 7;
+            *reinterpret_cast<u32x4*>(&r1s[buf][row * LROW + col * 8]) = rb[i];
+        }
+    };
+
     f32x16 acc[RT];
 #pragma unroll
     for (int pt = 0; pt < RT; ++pt) acc[pt] = zero_f32x16();
-
-    const uint16_t* xrow = x + (tok_ok ? tok : 0) * (int64_t)h + 8 * half;
-    // Operands of 8 consecutive h steps are loaded before their MFMAs so that each wave keeps
-    // 8 x 16 bytes of x per lane in flight; steps past the wave's range contribute zeros.
-    for (int s = ws0; s < ws1; s += 8) {
-        bf16x8 b[8], a[8][RT];
+    if (nc > 0) {
+        unroll<D>([&](auto s) __attribute__((always_inline)) { xload(s, decltype(s)::value); });
+        rload(0);
+        rstash(0);
+        rload(1);
+        __syncthreads();
+        for (int cb = 0; cb < nc; cb += D) {
+            unroll<D>([&](auto p) __attribute__((always_inline)) {
+                const int c = cb + decltype(p)::value;
+                if (c < nc) {
+                    const int buf = c & 1;
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const bool ok = s + u < ws1;
-            b[u] = (ok && tok_ok) ? load_bf16x8(xrow + 16 * (s + u)) : zero_bf16x8();
+                    for (int j = 0; j < 4; ++j) {
+                        if (4 * (cbeg + c) + j < S) {
+                            const bf16x8 b = __builtin_bit_cast(bf16x8, xb[decltype(p)::value][j]);
 #pragma unroll
-            for (int pt = 0; pt < RT; ++pt) {
-                const int row = 32 * pt + prow;
-                a[u][pt] = (ok && row < r)
-                               ? load_bf16x8(R1t + (int64_t)row * h + 16 * (s + u) + 8 * half)
-                               : zero_bf16x8();
-            }
+                            for (int pt = 0; pt < RT; ++pt) {
+                                const bf16x8 a = load_bf16x8(
+                                    &r1s[buf][(32 * pt + prow) * LROW + 16 * j + 8 * half]);
+                                acc[pt] = mfma_32x32x16(a, b, acc[pt]);
+                            }
+                        }
+                    }
+                    xload(p, c + D);
+                    rstash(buf ^ 1);
+                    rload(c + 2);
+                    __syncthreads();
+                }
+            });
         }
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-#pragma unroll
-            for (int pt = 0; pt < RT; ++pt) acc[pt] = mfma_32x32x16(a[u][pt], b[u], acc[pt]);
     }
 
-    // Partial sums of waves 1..3, element-major so that a wave's 64 lanes touch 64 consecutive
-    // words for each accumulator element.
-    __shared__ float red[3][RT][16][64];
-    if (w > 0) {
-#pragma unroll
-        for (int pt = 0; pt < RT; ++pt)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) red[w - 1][pt][j][lane] = acc[pt][j];
-    }
-    __syncthreads();
-    if (w == 0) {
+    if (tok_ok) {
+        float* zrow = zout + ((int64_t)split * T + tok) * r + 8 * half;
 #pragma unroll
         for (int pt = 0; pt < RT; ++pt) {
 #pragma unroll
-            for (int q = 0; q < 3; ++q)
+            for (int c2 = 0; c2 < 2; ++c2) {
+                const int c = 2 * pt + c2;
+                if (16 * c < r) {
+                    f32x4 lo4, hi4;
 #pragma unroll
-                for (int j = 0; j < 16; ++j) acc[pt][j] += red[q][pt][j][lane];
-        }
-        if (tok_ok) {
-            float* zrow = zout + ((int64_t)blockIdx.y * T + tok) * r + 8 * half;
-#pragma unroll
-            for (int pt = 0; pt < RT; ++pt) {
-#pragma unroll
-                for (int c2 = 0; c2 < 2; ++c2) {
-                    const int c = 2 * pt + c2;
-                    if (16 * c < r) {
-                        f32x4 lo4, hi4;
-#pragma unroll
-                        for (int p = 0; p < 4; ++p) {
-                            lo4[p] = acc[pt][8 * c2 + p];
-                            hi4[p] = acc[pt][8 * c2 + 4 + p];
-                        }
-                        *reinterpret_cast<f32x4*>(zrow + 16 * c) = lo4;
-                        *reinterpret_cast<f32x4*>(zrow + 16 * c + 4) = hi4;
+                    for (int q = 0; q < 4; ++q) {
+                        lo4[q] = acc[pt][8 * c2 + q];
+                        hi4[q] = acc[pt][8 * c2 + 4 + q];
                     }
+                    *reinterpret_cast<f32x4*>(zrow + 16 * c) = lo4;
+                    *reinterpret_cast<f32x4*>(zrow + 16 * c + 4) = hi4;
                 }
             }
         }
@@ -135,9 +219,11 @@ __global__ __launch_bounds__(256) void zreduce_kernel(const float* __restrict__ 
 }
 
 // ------------------------------------------------------------------------------ route
-// Route workgroups: 8 waves, wave w owning the 32 tokens tb*256 + 32w + (0..31), sweeping the
-// expert tiles of one chunk.  The chunk's expert rows stream through LDS in blocks of BT tiles
-// shared by all eight waves, so each R2 byte leaves L2 once per 256 tokens.
+// Screen and collect workgroups are expert-resident: a workgroup loads one chunk of the
+// expert axis (up to 128 KiB of R2t rows, with their group norms) into LDS once, then its 8
+// waves sweep that chunk for token blocks of 512 tokens (wave w takes the kTPW groups of 32
+// tokens 64w .. 64w+63 of the block), with no barrier inside the token loop.  Each A operand
+// read from LDS feeds kTPW MFMAs.
 //
 // Screening precision.  The sweeps compute s_e = z_hi . u_e on the matrix cores, with z_hi =
 // bf16(z) and fp32 accumulation, instead of the logit l_e = z . u_e.  With z_lo = z - z_hi,
@@ -146,51 +232,25 @@ __global__ __launch_bounds__(256) void zreduce_kernel(const float* __restrict__ 
 // and ||u_e|| <= N_g, the largest row norm of the 4-expert group g holding e.  So s_e - c N_g
 // is a lower and s_e + c N_g an upper bound of l_e.
 constexpr int kRouteWaves = 8;
+constexpr int kTPW = 2;
 constexpr int kRouteThreads = 64 * kRouteWaves;
-constexpr int kRouteTokens = 32 * kRouteWaves;
-constexpr int kLaneSlots = 16;         // candidate slots per lane in the collect kernel
-constexpr int kMaxChunkExperts = 65536;  // slots hold 16-bit offsets inside the chunk
+constexpr int kRouteTokens = 32 * kTPW * kRouteWaves;
+constexpr int kLaneSlots = 8;                 // candidate slots per lane and token group
+constexpr int kChunkBytes = 128 * 1024;       // LDS for the resident expert rows
 
 template <int RC, int K>
 struct RouteCfg {
     static constexpr int R = 16 * RC;
-    static constexpr int U = K / 4 > 1 ? K / 4 : 1;  // bucket period, in tiles
-    static constexpr int L = 4 * U;                  // bucket maxima per lane (>= K)
-    static constexpr int BT0 = RC <= 2 ? 8 : 4;
-    static constexpr int BT = U > BT0 ? U : BT0;     // tiles per LDS block (a multiple of U)
-    static constexpr int ROW = R + 8;                // padded LDS row, bf16 elements
-    static constexpr int BLOCK = BT * 32 * ROW;      // bf16 elements per block buffer
-    static constexpr int SPR = R / 8;                // 16-byte segments per expert row
-    static constexpr int SEGS = BT * 32 * SPR;
-    static constexpr int LOADS = (SEGS + kRouteThreads - 1) / kRouteThreads;
-    static constexpr int GROUPS = BT * 8;            // 4-expert groups per block
-    // Blocks in flight: a block is fetched DEPTH blocks ahead of its use into registers and
-    // stored to one of DEPTH + 1 LDS buffers one block ahead.
-    static constexpr int DEPTH = 3 * BLOCK * 2 <= 120 * 1024 ? 2 : 1;
-    static constexpr int NBUF = DEPTH + 1;
-    static_assert(GROUPS <= kRouteThreads, "one group norm per thread");
+    static constexpr int SPR = R / 8;                     // 16-byte segments per expert row
+    static constexpr int U = K / 4 > 1 ? K / 4 : 1;       // bucket period, in tiles
+    static constexpr int L = 4 * U;                       // bucket maxima per lane (>= K)
+    static constexpr int EMAX = kChunkBytes / (2 * R);    // experts per chunk (multiple of 32)
+    // Rows are stored unpadded; segment s of row e sits at position s ^ swz(e), which spreads
+    // the 16-byte reads of 16 consecutive rows over all 64 banks.
+    static constexpr int RPL = 16 / SPR;                  // rows per 256-byte bank line
+    __device__ static constexpr int swz(int e) { return (e / RPL) % SPR; }
 };
 
-template <typename F, int... I>
-__device__ __forceinline__ void unroll_impl(F&& f, std::integer_sequence<int, I...>) {
-    (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, typename F>
-__device__ __forceinline__ void unroll(F&& f) {
-    unroll_impl(f, std::make_integer_sequence<int, N>{});
-}
-
-__device__ __forceinline__ float max4(const f32x16& a, int q) {
-    return fmaxf(fmaxf(a[4 * q], a[4 * q + 1]), fmaxf(a[4 * q + 2], a[4 * q + 3]));
-}
-
-__device__ __forceinline__ void mask_past_end(f32x16& acc, int32_t e0, int32_t M, int half) {
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-        if (e0 + acc_row(j, half) >= M) acc[j] = -__builtin_huge_valf();
-}
-
-// Sort N = 2^m values in descending order (bitonic network).
 template <int N>
 __device__ __forceinline__ void sort_desc(float (&v)[N]) {
 #pragma unroll
@@ -229,194 +289,187 @@ __device__ __forceinline__ void vlist_merge(float (&a)[K], const float (&b)[K]) 
     }
 }
 
+__device__ __forceinline__ float max4(const f32x16& a, int q) {
+    return fmaxf(fmaxf(a[4 * q], a[4 * q + 1]), fmaxf(a[4 * q + 2], a[4 * q + 3]));
+}
+
+__device__ __forceinline__ void mask_past_end(f32x16& acc, int32_t e0, int32_t M, int half) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+        if (e0 + acc_row(j, half) >= M) acc[j] = -__builtin_huge_valf();
+}
+
 // LDS position of group g4 = (row mod 32) / 4 = 2q + half of a tile: [tile][half][q], so that a
 // lane reads the norms of its four accumulator groups with one 16-byte load.
 __device__ __forceinline__ int gnorm_slot(int tile, int g4) {
     return tile * 8 + (g4 & 1) * 4 + (g4 >> 1);
 }
 
-// The tiles [t0, t1) of one expert chunk, streamed through NBUF LDS block buffers, with the
-// group norms N_g of each block.  OWN_NORMS: the norms are computed from the rows (and, when
-// gnorm_out is set, written to gnorm_out[group]); otherwise they are read from gnorm_in.
-template <int RC, int K, bool OWN_NORMS>
-struct ChunkStream {
+// Work split of a route launch: workgroup -> (expert chunk, range of token blocks).
+struct RouteSplit {
+    int32_t chunk;
+    int64_t t0, t1;        // tiles of the chunk
+    int64_t blk0, blk1;    // token blocks of 512
+};
+
+__device__ __forceinline__ RouteSplit route_split(int32_t T, int32_t M, int32_t chunks,
+                                                  int32_t splits) {
+    RouteSplit q;
+    q.chunk = (int32_t)(blockIdx.x % (unsigned)chunks);
+    const int32_t split = (int32_t)(blockIdx.x / (unsigned)chunks);
+    const int64_t Mt = ((int64_t)M + 31) / 32;
+    q.t0 = Mt * q.chunk / chunks;
+    q.t1 = Mt * (q.chunk + 1) / chunks;
+    const int64_t ntb = ((int64_t)T + kRouteTokens - 1) / kRouteTokens;
+    q.blk0 = ntb * split / splits;
+    q.blk1 = ntb * (split + 1) / splits;
+    return q;
+}
+
+// Loads the rows of tiles [t0, t1) (rows past M re-read row M - 1; they are masked later) and
+// their group norms into LDS; every thread of the workgroup takes part.
+template <int RC, int K>
+__device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ R2t,
+                                           const float* __restrict__ gnorm, int32_t M,
+                                           int64_t t0, int64_t t1, uint16_t* rows, float* gn) {
     using C = RouteCfg<RC, K>;
-    const uint16_t* __restrict__ R2t;
-    int32_t M;
-    int64_t t0, t1;
-    uint16_t* lds;   // NBUF * C::BLOCK elements
-    float* lds_gn;   // NBUF * C::GROUPS
-    const float* __restrict__ gnorm_in;
-    float* __restrict__ gnorm_out;
-    u32x4 g[C::DEPTH][C::LOADS];
-    float gn[C::DEPTH];
-
-    // Loads block b of the chunk into register set S.  Every lane always issues the same
-    // loads (so that the compiler can count them and wait for one set while the next is in
-    // flight): blocks past the end re-read the last block, tiles past the chunk re-read its
-    // last tile and rows past M re-read row M - 1.  None of those values reaches a result:
-    // such tiles are skipped and such rows are masked.
-    template <int S>
-    __device__ __forceinline__ void fetch(int64_t b, int64_t nblk, int tid) {
-        const int64_t bb = b < nblk ? b : nblk - 1;
+    const int tid = threadIdx.x;
+    const int nseg = (int)(t1 - t0) * 32 * C::SPR;
+    const int64_t e0 = t0 * 32;
+    constexpr int UNR = 8;  // loads in flight per thread
+    for (int base = 0; base < nseg; base += UNR * kRouteThreads) {
+        u32x4 v[UNR];
 #pragma unroll
-        for (int i = 0; i < C::LOADS; ++i) {
-            const int seg = (tid + i * kRouteThreads) % C::SEGS;
-            const int row = seg / C::SPR, col = seg % C::SPR;
-            int64_t t = t0 + bb * C::BT + row / 32;
-            t = t < t1 ? t : t1 - 1;
-            int64_t e = t * 32 + (row % 32);
-            e = e < M ? e : M - 1;
-            g[S][i] = *reinterpret_cast<const u32x4*>(R2t + e * C::R + col * 8);
+        for (int i = 0; i < UNR; ++i) {
+            int seg = base + i * kRouteThreads + tid;
+            seg = seg < nseg ? seg : nseg - 1;
+            const int e = seg / C::SPR, s = seg % C::SPR;
+            int64_t ge = e0 + e;
+            ge = ge < M ? ge : M - 1;
+            v[i] = *reinterpret_cast<const u32x4*>(R2t + ge * C::R + s * 8);
         }
-        if (!OWN_NORMS) {
-            int64_t t = t0 + bb * C::BT + (tid % C::GROUPS) / 8;
-            t = t < t1 ? t : t1 - 1;
-            gn[S] = gnorm_in[t * 8 + tid % 8];
-        }
-    }
-    template <int S>
-    __device__ __forceinline__ void stash(int64_t b, int buf, int tid, bool write_out) {
 #pragma unroll
-        for (int i = 0; i < C::LOADS; ++i) {
-            const int seg = tid + i * kRouteThreads;
-            if (seg < C::SEGS) {
-                const int row = seg / C::SPR, col = seg % C::SPR;
-                *reinterpret_cast<u32x4*>(lds + buf * C::BLOCK + row * C::ROW + col * 8) = g[S][i];
+        for (int i = 0; i < UNR; ++i) {
+            const int seg = base + i * kRouteThreads + tid;
+            if (seg < nseg) {
+                const int e = seg / C::SPR, s = seg % C::SPR;
+                *reinterpret_cast<u32x4*>(rows + e * C::R + ((s ^ C::swz(e)) * 8)) = v[i];
             }
         }
-        if (OWN_NORMS) {
-#pragma unroll
-            for (int i = 0; i < C::LOADS; ++i) {
-                const int seg = tid + i * kRouteThreads;
-                const int row = seg / C::SPR, col = seg % C::SPR;
-                const bf16x8 v = __builtin_bit_cast(bf16x8, g[S][i]);
-                float ss = 0.0f;
-#pragma unroll
-                for (int q = 0; q < 8; ++q) ss = fmaf((float)v[q], (float)v[q], ss);
-                // row norm^2 over the SPR lanes of the row, then the max over 4 rows
-#pragma unroll
-                for (int m = 1; m < C::SPR; m <<= 1) ss += __shfl_xor(ss, m, kWave);
-                ss = fmaxf(ss, __shfl_xor(ss, C::SPR, kWave));
-                ss = fmaxf(ss, __shfl_xor(ss, 2 * C::SPR, kWave));
-                if (seg < C::SEGS && col == 0 && (row & 3) == 0) {
-                    const float nrm = sqrtf(ss) * (1.0f + 0x1p-20f);
-                    const int tile = row / 32;
-                    lds_gn[buf * C::GROUPS + gnorm_slot(tile, (row % 32) / 4)] = nrm;
-                    const int64_t t = t0 + b * C::BT + tile;
-                    if (write_out && t < t1) gnorm_out[t * 8 + (row % 32) / 4] = nrm;
-                }
-            }
-        } else if (tid < C::GROUPS) {
-            lds_gn[buf * C::GROUPS + gnorm_slot(tid / 8, tid % 8)] = gn[S];
-        }
     }
+    const int ngr = (int)(t1 - t0) * 8;
+    for (int g = tid; g < ngr; g += kRouteThreads) gn[gnorm_slot(g / 8, g % 8)] = gnorm[t0 * 8 + g];
+    __syncthreads();
+}
 
-    // Calls body(a, e0, partial, tt, nq) for every tile of the chunk in increasing order,
-    // where a[c] is this lane's A operand (expert row e0 + n, K half `half`, rank chunk c), tt
-    // the tile's compile-time position in its block and nq[q] the norm bound of the lane's
-    // accumulator group q.  Every thread of the workgroup must call this together.
-    template <typename Body>
-    __device__ __forceinline__ void sweep(int tid, int n, int half, bool write_out, Body&& body) {
-        constexpr int D = C::DEPTH;
-        const int64_t nblk = (t1 - t0 + C::BT - 1) / C::BT;
-        if (nblk <= 0) return;
-        unroll<D>([&](auto s) __attribute__((always_inline)) {
-            fetch<decltype(s)::value>(decltype(s)::value, nblk, tid);
-        });
-        stash<0>(0, 0, tid, write_out);
-        __syncthreads();
-        for (int64_t b0 = 0; b0 < nblk; b0 += D) {
-            unroll<D>([&](auto p) __attribute__((always_inline)) {
-                constexpr int P = decltype(p)::value;  // b mod D
-                const int64_t b = b0 + P;
-                if (b < nblk) {
-                    // register set P (block b, already in LDS) is free: fetch block b + D
-                    fetch<P>(b + D, nblk, tid);
-                    const int buf = (int)(b % C::NBUF);
-                    const uint16_t* base = lds + buf * C::BLOCK + n * C::ROW + 8 * half;
-                    unroll<C::BT>([&](auto tt) __attribute__((always_inline)) {
-                        constexpr int TT = decltype(tt)::value;
-                        const int64_t t = t0 + b * C::BT + TT;
-                        if (t < t1) {
-                            bf16x8 a[RC];
-#pragma unroll
-                            for (int c = 0; c < RC; ++c)
-                                a[c] = load_bf16x8(base + TT * 32 * C::ROW + 16 * c);
-                            const f32x4 nq = *reinterpret_cast<const f32x4*>(
-                                lds_gn + buf * C::GROUPS + TT * 8 + 4 * half);
-                            body(a, (int32_t)(t * 32), t * 32 + 32 > M, tt, nq);
-                        }
-                    });
-                    if (b + 1 < nblk) stash<(P + 1) % D>(b + 1, (int)((b + 1) % C::NBUF), tid, write_out);
-                    __syncthreads();
-                }
-            });
-        }
-    }
-};
-
-// Token ids, z operands and the error scale c of one lane of a route workgroup.
+// Token ids, z operands and the error scale c of one lane, for each of the wave's kTPW groups
+// of 32 tokens starting at `first`.
 template <int RC>
-struct RouteLane {
-    int tid, lane, w, n, half, chunk, tb;
-    int64_t tok;
-    bool tok_ok;
-    bf16x8 zhi[RC];
-    float c;
+struct TokenGroups {
+    int64_t tok[kTPW];
+    bool tok_ok[kTPW];
+    bf16x8 zhi[kTPW][RC];
+    float c[kTPW];
 
-    __device__ __forceinline__ RouteLane(const float* __restrict__ z, int32_t T, int32_t chunks) {
-        tid = threadIdx.x;
-        lane = tid & 63;
-        w = __builtin_amdgcn_readfirstlane(tid >> 6);
-        n = lane & 31;
-        half = lane >> 5;
-        // Consecutive workgroups take consecutive chunks: with chunks a multiple or a divisor
-        // of 8, a chunk always lands on the same XCD(s) (workgroups are dealt to the eight XCDs
-        // round robin) and its expert rows stay in that XCD's L2.
-        chunk = (int)(blockIdx.x % (unsigned)chunks);
-        tb = (int)(blockIdx.x / (unsigned)chunks);
-        tok = ((int64_t)tb * kRouteWaves + w) * 32 + n;
-        tok_ok = tok < T;
+    __device__ __forceinline__ void load(const float* __restrict__ z, int32_t T, int64_t first,
+                                         int n, int half) {
         constexpr int R = 16 * RC;
-        float lo2 = 0.0f, hi2 = 0.0f;
 #pragma unroll
-        for (int cc = 0; cc < RC; ++cc) {
-            float v[8];
-            if (tok_ok) {
-                const f32x4* p = reinterpret_cast<const f32x4*>(z + tok * R + 16 * cc + 8 * half);
-                const f32x4 a0 = p[0], a1 = p[1];
+        for (int g = 0; g < kTPW; ++g) {
+            tok[g] = first + 32 * g + n;
+            tok_ok[g] = tok[g] < T;
+            float lo2 = 0.0f, hi2 = 0.0f;
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    v[q] = a0[q];
-                    v[4 + q] = a1[q];
+            for (int cc = 0; cc < RC; ++cc) {
+                float v[8];
+                if (tok_ok[g]) {
+                    const f32x4* p =
+                        reinterpret_cast<const f32x4*>(z + tok[g] * R + 16 * cc + 8 * half);
+                    const f32x4 a0 = p[0], a1 = p[1];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        v[q] = a0[q];
+                        v[4 + q] = a1[q];
+                    }
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) v[q] = 0.0f;
                 }
-            } else {
 #pragma unroll
-                for (int q = 0; q < 8; ++q) v[q] = 0.0f;
+                for (int q = 0; q < 8; ++q) {
+                    const __bf16 hb = (__bf16)v[q];
+                    const float hf = (float)hb;
+                    const float lf = v[q] - hf;
+                    zhi[g][cc][q] = hb;
+                    hi2 = fmaf(hf, hf, hi2);
+                    lo2 = fmaf(lf, lf, lo2);
+                }
             }
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const __bf16 h = (__bf16)v[q];
-                const float hf = (float)h;
-                const float lf = v[q] - hf;
-                zhi[cc][q] = h;
-                hi2 = fmaf(hf, hf, hi2);
-                lo2 = fmaf(lf, lf, lo2);
-            }
+            hi2 += __shfl_xor(hi2, 32, kWave);
+            lo2 += __shfl_xor(lo2, 32, kWave);
+            c[g] = (sqrtf(lo2) + (float)R * 0x1p-23f * sqrtf(hi2)) * (1.0f + 0x1p-10f);
         }
-        hi2 += __shfl_xor(hi2, 32, kWave);
-        lo2 += __shfl_xor(lo2, 32, kWave);
-        c = (sqrtf(lo2) + (float)R * 0x1p-23f * sqrtf(hi2)) * (1.0f + 0x1p-10f);
     }
 };
 
-template <int RC>
-__device__ __forceinline__ f32x16 screened_tile(const bf16x8 (&a)[RC], const bf16x8 (&zhi)[RC]) {
-    f32x16 acc = zero_f32x16();
+// Sweeps the resident chunk for one lane's token groups: for every tile t (in order) issues
+// the MFMAs of tile t, then calls body(acc, e0, partial, u, nq) for tile t - 1 (software
+// pipeline), and finally for the last tile.  Two accumulator sets alternate by tile parity
+// (no register copies); tiles are unrolled by V = max(U, 2) so that the set and the bucket
+// index u = t mod U (passed as std::integral_constant) are compile-time constants.  acc[g] holds s for token
+// group g, e0 the first expert of the tile, nq[q] the norm bound of accumulator group q.
+template <int RC, int K, typename Body>
+__device__ __forceinline__ void sweep_resident(const uint16_t* rows, const float* gn, int64_t t0,
+                                               int64_t t1, int32_t M, int n, int half,
+                                               const bf16x8 (&zhi)[kTPW][RC], Body&& body) {
+    using C = RouteCfg<RC, K>;
+    constexpr int U = C::U;
+    constexpr int V = U > 2 ? U : 2;
+    const int nt = (int)(t1 - t0);
+    const int32_t e00 = (int32_t)(t0 * 32);
+    const int sw = C::swz(n);
+    int off[RC];
 #pragma unroll
-    for (int c = 0; c < RC; ++c) acc = mfma_32x32x16(a[c], zhi[c], acc);
-    return acc;
+    for (int c = 0; c < RC; ++c) off[c] = n * C::R + (((2 * c + half) ^ sw) * 8);
+    f32x16 acc[2][kTPW];
+    f32x4 nq[2];
+    auto run = [&](auto set, int tile, auto u) __attribute__((always_inline)) {
+        const int32_t e0 = e00 + tile * 32;
+        body(acc[decltype(set)::value], e0, e0 + 32 > M, u, nq[decltype(set)::value]);
+    };
+    for (int t = 0; t < nt; t += V) {
+        unroll<V>([&](auto vv) __attribute__((always_inline)) {
+            constexpr int VV = decltype(vv)::value;
+            constexpr int P = VV & 1;
+            const int tile = t + VV;
+            if (tile < nt) {
+                const uint16_t* base = rows + tile * 32 * C::R;
+                bf16x8 a[RC];
+#pragma unroll
+                for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(base + off[c]);
+                nq[P] = *reinterpret_cast<const f32x4*>(gn + tile * 8 + 4 * half);
+#pragma unroll
+                for (int g = 0; g < kTPW; ++g) acc[P][g] = zero_f32x16();
+#pragma unroll
+                for (int c = 0; c < RC; ++c)
+#pragma unroll
+                    for (int g = 0; g < kTPW; ++g)
+                        acc[P][g] = mfma_32x32x16(a[c], zhi[g][c], acc[P][g]);
+                if (tile > 0)
+                    run(std::integral_constant<int, P ^ 1>{}, tile - 1,
+                        std::integral_constant<int, (VV + V - 1) % U>{});
+            }
+        });
+    }
+    // last tile: set and bucket dispatched to compile-time values
+    if (nt > 0) {
+        unroll<V>([&](auto vv) __attribute__((always_inline)) {
+            constexpr int VV = decltype(vv)::value;
+            if ((nt - 1) % V == VV)
+                run(std::integral_constant<int, VV & 1>{}, nt - 1,
+                    std::integral_constant<int, VV % U>{});
+        });
+    }
 }
 
 // Screening sweep.  For each accumulator group q of a tile the lane forms the lower bound
@@ -425,46 +478,57 @@ __device__ __forceinline__ f32x16 screened_tile(const bf16x8 (&a)[RC], const bf1
 // buckets of a token's two lanes partition the chunk's experts into 2L >= 2K groups, so the
 // K largest bucket maxima belong to K distinct experts, each with logit >= its value.
 // Output per token and chunk: those K values, descending, in top[chunk][token][0..K-1].
-// Workgroups of token block 0 also write the group norms of their chunk to gnorm[].
 template <int RC, int K>
-__global__ __launch_bounds__(kRouteThreads, 4) void screen_kernel(
+__global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
     const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
-    int32_t chunks, float* __restrict__ top, float* __restrict__ gnorm) {
+    int32_t chunks, int32_t splits, const float* __restrict__ gnorm, float* __restrict__ top) {
     using C = RouteCfg<RC, K>;
     constexpr int U = C::U, L = C::L;
-    __shared__ __attribute__((aligned(16))) uint16_t a_lds[C::NBUF * C::BLOCK];
-    __shared__ __attribute__((aligned(16))) float gn_lds[C::NBUF * C::GROUPS];
-    const RouteLane<RC> ln(z, T, chunks);
-    const bool wave_active = ((int64_t)ln.tb * kRouteWaves + ln.w) * 32 < T;  // wave-uniform
-    const int64_t Mt = ((int64_t)M + 31) / 32;
-    ChunkStream<RC, K, true> st{R2t, M, Mt * ln.chunk / chunks, Mt * (ln.chunk + 1) / chunks,
-                                a_lds, gn_lds, nullptr, gnorm};
+    __shared__ __attribute__((aligned(16))) uint16_t rows[C::EMAX * C::R];
+    __shared__ __attribute__((aligned(16))) float gn[C::EMAX / 4];
+    const RouteSplit sp = route_split(T, M, chunks, splits);
+    load_chunk<RC, K>(R2t, gnorm, M, sp.t0, sp.t1, rows, gn);
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int n = lane & 31, half = lane >> 5;
 
-    float bm[L];
+    for (int64_t blk = sp.blk0; blk < sp.blk1; ++blk) {
+        const int64_t first = blk * kRouteTokens + (int64_t)w * 32 * kTPW;
+        if (first >= T) break;  // wave-uniform
+        TokenGroups<RC> tg;
+        tg.load(z, T, first, n, half);
+        float bm[kTPW][L];
 #pragma unroll
-    for (int b = 0; b < L; ++b) bm[b] = -__builtin_huge_valf();
-    st.sweep(ln.tid, ln.n, ln.half, ln.tb == 0,
-             [&](const bf16x8 (&a)[RC], int32_t e0, bool partial, auto tt, const f32x4& nq)
-                 __attribute__((always_inline)) {
-                 if (!wave_active) return;
-                 f32x16 acc = screened_tile<RC>(a, ln.zhi);
-                 if (partial) mask_past_end(acc, e0, M, ln.half);
-                 constexpr int u = decltype(tt)::value % U;
+        for (int g = 0; g < kTPW; ++g)
 #pragma unroll
-                 for (int q = 0; q < 4; ++q)
-                     bm[4 * u + q] = fmaxf(bm[4 * u + q], max4(acc, q) - ln.c * nq[q]);
-             });
-
-    // K largest of the token's 2L bucket maxima.
-    sort_desc<L>(bm);
-    float pb[L];
+            for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
+        sweep_resident<RC, K>(rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
+                              [&](f32x16 (&acc)[kTPW], int32_t e0, bool partial, auto u,
+                                  const f32x4& nq) __attribute__((always_inline)) {
+                                  constexpr int UB = 4 * decltype(u)::value;
 #pragma unroll
-    for (int b = 0; b < L; ++b) pb[b] = __shfl_xor(bm[b], 32, kWave);
-    vlist_merge<L>(bm, pb);
-    if (ln.half == 0 && ln.tok_ok) {
-        float* o = top + ((int64_t)ln.chunk * T + ln.tok) * K;
+                                  for (int g = 0; g < kTPW; ++g) {
+                                      if (partial) mask_past_end(acc[g], e0, M, half);
 #pragma unroll
-        for (int j = 0; j < K; ++j) o[j] = bm[j];
+                                      for (int q = 0; q < 4; ++q)
+                                          bm[g][UB + q] = fmaxf(
+                                              bm[g][UB + q], max4(acc[g], q) - tg.c[g] * nq[q]);
+                                  }
+                              });
+        // K largest of each token's 2L bucket maxima.
+#pragma unroll
+        for (int g = 0; g < kTPW; ++g) {
+            sort_desc<L>(bm[g]);
+            float pb[L];
+#pragma unroll
+            for (int b = 0; b < L; ++b) pb[b] = __shfl_xor(bm[g][b], 32, kWave);
+            vlist_merge<L>(bm[g], pb);
+            if (half == 0 && tg.tok_ok[g]) {
+                float* o = top + ((int64_t)sp.chunk * T + tg.tok[g]) * K;
+#pragma unroll
+                for (int j = 0; j < K; ++j) o[j] = bm[g][j];
+            }
+        }
     }
 }
 
@@ -521,70 +585,96 @@ __global__ __launch_bounds__(256) void theta_kernel(const float* __restrict__ to
 #pragma unroll
     for (int j = 1; j < K; ++j)
         if (j == k - 1) th = v[j];
-    theta[tok] = th - fabsf(th) * 0x1p-20f;
+    // Clamped to -2^100: logits are finite and far smaller in magnitude, and masked (-inf)
+    // entries stay below every threshold derived from it.
+    theta[tok] = fmaxf(th - fabsf(th) * 0x1p-20f, -0x1p100f);
     count[tok] = 0;
 }
 
 // Collect sweep: recomputes s for the chunk and appends every expert with s_e + c N_g >=
 // theta[token] to the token's candidate list cand[token][0..cap-1] (order of arrival,
-// count[token] entries).  A lane buffers its hits in kLaneSlots LDS slots (16-bit offsets in
-// the chunk); the token's two lanes reserve their list space with one atomic add at the end.
-// A lane with more hits marks the token as overflowed (count > cap), which sends it to the
-// exact sweep of the finalize kernel.
+// count[token] entries).  A lane buffers its hits in kLaneSlots LDS slots per token group
+// (16-bit offsets in the chunk); the token's two lanes reserve their list space with one
+// atomic add at the end of the token block.  A lane with more hits marks the token as
+// overflowed (count > cap), which sends it to the exact sweep of the finalize kernel.
 template <int RC, int K>
-__global__ __launch_bounds__(kRouteThreads, 4) void collect_kernel(
+__global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
     const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
-    int32_t chunks, const float* __restrict__ theta, const float* __restrict__ gnorm,
-    int32_t* __restrict__ count, int32_t* __restrict__ cand, int32_t cap) {
+    int32_t chunks, int32_t splits, const float* __restrict__ theta,
+    const float* __restrict__ gnorm, int32_t* __restrict__ count, int32_t* __restrict__ cand,
+    int32_t cap) {
     using C = RouteCfg<RC, K>;
-    __shared__ __attribute__((aligned(16))) uint16_t a_lds[C::NBUF * C::BLOCK];
-    __shared__ __attribute__((aligned(16))) float gn_lds[C::NBUF * C::GROUPS];
-    __shared__ uint16_t slots[kLaneSlots][kRouteThreads];
-    const RouteLane<RC> ln(z, T, chunks);
-    const bool wave_active = ((int64_t)ln.tb * kRouteWaves + ln.w) * 32 < T;
-    const int64_t Mt = ((int64_t)M + 31) / 32;
-    ChunkStream<RC, K, false> st{R2t, M, Mt * ln.chunk / chunks, Mt * (ln.chunk + 1) / chunks,
-                                 a_lds, gn_lds, gnorm, nullptr};
-    const int32_t ebase = (int32_t)(st.t0 * 32);
-    // Lanes past T never qualify (+inf threshold).
-    const float th = ln.tok_ok ? theta[ln.tok] : __builtin_huge_valf();
+    __shared__ __attribute__((aligned(16))) uint16_t rows[C::EMAX * C::R];
+    __shared__ __attribute__((aligned(16))) float gn[C::EMAX / 4];
+    __shared__ uint16_t slots[kLaneSlots][kTPW][kRouteThreads];
+    const RouteSplit sp = route_split(T, M, chunks, splits);
+    load_chunk<RC, K>(R2t, gnorm, M, sp.t0, sp.t1, rows, gn);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 31, half = lane >> 5;
+    const int32_t ebase = (int32_t)(sp.t0 * 32);
 
-    int cnt = 0;
-    st.sweep(ln.tid, ln.n, ln.half, false,
-             [&](const bf16x8 (&a)[RC], int32_t e0, bool partial, auto tt, const f32x4& nq)
-                 __attribute__((always_inline)) {
-                 (void)tt;
-                 if (!wave_active) return;
-                 f32x16 acc = screened_tile<RC>(a, ln.zhi);
-                 if (partial) mask_past_end(acc, e0, M, ln.half);
-                 float tq[4];
+    for (int64_t blk = sp.blk0; blk < sp.blk1; ++blk) {
+        const int64_t first = blk * kRouteTokens + (int64_t)w * 32 * kTPW;
+        if (first >= T) break;  // wave-uniform
+        TokenGroups<RC> tg;
+        tg.load(z, T, first, n, half);
+        float th[kTPW];
+        int cnt[kTPW];
 #pragma unroll
-                 for (int q = 0; q < 4; ++q) tq[q] = fmaxf(th - ln.c * nq[q], -__FLT_MAX__);
-                 const float m = fmaxf(fmaxf(max4(acc, 0) - tq[0], max4(acc, 1) - tq[1]),
-                                       fmaxf(max4(acc, 2) - tq[2], max4(acc, 3) - tq[3]));
-                 if (m >= 0.0f) {
+        for (int g = 0; g < kTPW; ++g) {
+            // Lanes past T never qualify (+inf threshold).
+            th[g] = tg.tok_ok[g] ? theta[tg.tok[g]] : __builtin_huge_valf();
+            cnt[g] = 0;
+        }
+        sweep_resident<RC, K>(
+            rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
+            [&](f32x16 (&acc)[kTPW], int32_t e0, bool partial, auto u, const f32x4& nq)
+                __attribute__((always_inline)) {
+                (void)u;
 #pragma unroll
-                     for (int j = 0; j < 16; ++j) {
-                         if (acc[j] >= tq[j >> 2]) {
-                             if (cnt < kLaneSlots)
-                                 slots[cnt][ln.tid] = (uint16_t)(e0 - ebase + acc_row(j, ln.half));
-                             ++cnt;
-                         }
-                     }
-                 }
-             });
-
-    const int pc = __shfl_xor(cnt, 32, kWave);
-    const bool over = cnt > kLaneSlots || pc > kLaneSlots;
-    const int total = cnt + pc;
-    int base = 0;
-    if (ln.half == 0 && ln.tok_ok && total > 0)
-        base = atomicAdd(&count[ln.tok], over ? cap + 1 : total);
-    base = __shfl(base, ln.n, kWave);  // lane half 1 reads its partner's reservation
-    if (ln.tok_ok && !over) {
-        const int off = base + (ln.half ? pc : 0);
-        for (int i = 0; i < cnt; ++i)
-            if (off + i < cap) cand[ln.tok * cap + off + i] = ebase + (int32_t)slots[i][ln.tid];
+                for (int g = 0; g < kTPW; ++g) {
+                    if (partial) mask_past_end(acc[g], e0, M, half);
+                    float tq[4], gm[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        tq[q] = th[g] - tg.c[g] * nq[q];
+                        gm[q] = max4(acc[g], q) - tq[q];
+                    }
+                    if (fmaxf(fmaxf(gm[0], gm[1]), fmaxf(gm[2], gm[3])) >= 0.0f) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            if (gm[q] >= 0.0f) {
+#pragma unroll
+                                for (int i = 0; i < 4; ++i) {
+                                    if (acc[g][4 * q + i] >= tq[q]) {
+                                        slots[cnt[g] < kLaneSlots ? cnt[g] : kLaneSlots - 1][g][tid] =
+                                            (uint16_t)(e0 - ebase + acc_row(4 * q + i, half));
+                                        ++cnt[g];
+                                    }
+                                }
+                            }
+                        }
+                    }
+                }
+            });
+#pragma unroll
+        for (int g = 0; g < kTPW; ++g) {
+            const int pc = __shfl_xor(cnt[g], 32, kWave);
+            const bool over = cnt[g] > kLaneSlots || pc > kLaneSlots;
+            const int total = cnt[g] + pc;
+            int base = 0;
+            if (half == 0 && tg.tok_ok[g] && total > 0)
+                base = atomicAdd(&count[tg.tok[g]], over ? cap + 1 : total);
+            base = __shfl(base, n, kWave);  // lane half 1 reads its partner's reservation
+            if (tg.tok_ok[g] && !over) {
+                const int off = base + (half ? pc : 0);
+                for (int i = 0; i < cnt[g]; ++i)
+                    if (off + i < cap)
+                        cand[tg.tok[g] * cap + off + i] = ebase + (int32_t)slots[i][g][tid];
+            }
+        }
     }
 }
 
@@ -713,36 +803,40 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     q.K = pow2_at_least(k);
     q.ntb = (int32_t)((T + kRouteTokens - 1) / kRouteTokens);
     const int64_t Mt = ((int64_t)M + 31) / 32;
-    const int U = q.K / 4 > 1 ? q.K / 4 : 1;
-    const int BT0 = q.RC <= 2 ? 8 : 4;
-    const int BT = U > BT0 ? U : BT0;
+    const int64_t emax_tiles = (int64_t)kChunkBytes / (2 * r) / 32;
     if (m_chunks > 0) {
         q.chunks = m_chunks;
     } else {
-        // Two route workgroups per CU (512 in all), expert slices of at most 2 MiB (an XCD's
-        // L2 keeps the slice while the token blocks pass over it), at least one full LDS
-        // block per chunk.
-        const int64_t r2_bytes = (int64_t)M * r * 2;
-        int64_t C = 1;
-        while (C < 1024 && ((int64_t)q.ntb * C < 512 || r2_bytes / C > ((int64_t)2 << 20)) &&
-               Mt / (2 * C) >= BT)
-            C *= 2;
-        q.chunks = (int32_t)C;
+        // Chunks that fit the resident LDS rows, and at least 256 workgroups when there are
+        // enough token blocks and tiles.
+        int64_t C = (Mt + emax_tiles - 1) / emax_tiles;
+        const int64_t want = (256 + q.ntb - 1) / q.ntb;
+        if (C < want) C = want < Mt ? want : Mt;
+        q.chunks = (int32_t)(C < 1024 ? C : 1024);
     }
     if (q.chunks < 1 || q.chunks > 1024) return false;
-    // Candidate slots hold 16-bit offsets inside a chunk.
-    while (Mt * 32 / q.chunks + 32 > kMaxChunkExperts) q.chunks *= 2;
+    // Resident rows must fit in LDS (m_chunks is a request: the result does not depend on
+    // the chunking).
+    while ((Mt + q.chunks - 1) / q.chunks > emax_tiles) {
+        if (q.chunks >= (1 << 20)) return false;
+        q.chunks *= 2;
+    }
+    // Token splits: about 256 workgroups in all, each split holding whole token blocks.
+    int64_t S = 256 / q.chunks;
+    if (S < 1) S = 1;
+    if (S > q.ntb) S = q.ntb;
+    q.splits = (int32_t)S;
     q.theta_group = 1;
     while (q.theta_group < 64 && q.theta_group * 16 < q.chunks) q.theta_group *= 2;
     q.cap = 512;
-    const int32_t S = h / 16;
-    const int64_t TG = (T + 31) / 32;
-    int64_t hs = (256 + TG - 1) / TG;
-    hs = hs < 1 ? 1 : hs;
-    const int64_t max_hs = S / 4 > 0 ? S / 4 : 1;
-    if (hs > max_hs) hs = max_hs;
-    q.hsplit = (int32_t)hs;
-    q.steps_per_split = (S + q.hsplit - 1) / q.hsplit;
+    // z pass: 128-token blocks; the h chunks are split over workgroups only when there are
+    // too few token blocks to occupy the chip.
+    const int32_t NC = (h / 16 + 3) / 4;
+    const int64_t ntbz = (T + kZTokens - 1) / kZTokens;
+    int64_t hs = ntbz >= 96 ? 1 : (256 + ntbz - 1) / ntbz;
+    if (hs > NC) hs = NC;
+    q.steps_per_split = (int32_t)((NC + hs - 1) / hs);  // chunks per split
+    q.hsplit = (NC + q.steps_per_split - 1) / q.steps_per_split;
     const size_t zbytes = (size_t)T * r * sizeof(float);
     size_t off = 0;
     q.off_zparts = off;
@@ -771,10 +865,14 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
 // ------------------------------------------------------------------------------ launch
 template <int RT>
 static void launch_zpass(const LowrankPlan& p, const uint16_t* x, const uint16_t* R1t, float* zparts,
-                         int64_t T, int32_t h, int32_t r, hipStream_t st) {
-    dim3 grid((unsigned)((T + 31) / 32), (unsigned)p.hsplit);
-    hipLaunchKernelGGL(zpass_kernel<RT>, grid, dim3(256), 0, st, x, R1t, zparts, (int32_t)T, h, r,
-                       p.steps_per_split);
+                         int64_t T, int32_t h, int32_t r, const uint16_t* R2t, int32_t M,
+                         float* gnorm, hipStream_t st) {
+    const int64_t zblocks = (T + kZTokens - 1) / kZTokens;
+    const int64_t nblocks = (((int64_t)M + 31) / 32 * 32 * (r / 8) + 255) / 256;  // group norms
+    dim3 grid((unsigned)(zblocks * p.hsplit + nblocks));
+    constexpr int D = RT <= 2 ? 8 : 4;
+    hipLaunchKernelGGL((zpass_kernel<RT, D>), grid, dim3(256), 0, st, x, R1t, zparts, (int32_t)T,
+                       h, r, p.steps_per_split, R2t, M, (int32_t)zblocks, p.hsplit, gnorm);
 }
 
 struct RouteArgs {
@@ -789,14 +887,14 @@ struct RouteArgs {
 
 template <int RC, int K>
 static void launch_route(const LowrankPlan& p, const RouteArgs& a, hipStream_t st) {
-    const dim3 grid((unsigned)((int64_t)p.ntb * p.chunks));
+    const dim3 grid((unsigned)((int64_t)p.splits * p.chunks));
     hipLaunchKernelGGL((screen_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.z, a.R2t, a.T,
-                       a.M, p.chunks, a.top, a.gnorm);
+                       a.M, p.chunks, p.splits, a.gnorm, a.top);
     const int64_t nth = (int64_t)a.T * p.theta_group;
     hipLaunchKernelGGL((theta_kernel<K>), dim3((unsigned)((nth + 255) / 256)), dim3(256), 0, st,
                        a.top, a.T, p.chunks, a.k, p.theta_group, a.theta, a.count);
     hipLaunchKernelGGL((collect_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.z, a.R2t, a.T,
-                       a.M, p.chunks, a.theta, a.gnorm, a.count, a.cand, p.cap);
+                       a.M, p.chunks, p.splits, a.theta, a.gnorm, a.count, a.cand, p.cap);
     hipLaunchKernelGGL((finalize_kernel<RC, K>), dim3((unsigned)((a.T + 31) / 32)), dim3(256), 0,
                        st, a.z, a.R2t, a.T, a.M, a.k, a.count, a.cand, p.cap, a.idx, a.gate,
                        a.topval);
@@ -810,7 +908,6 @@ static bool dispatch_route_k(const LowrankPlan& p, const RouteArgs& a, hipStream
         case 4: launch_route<RC, 4>(p, a, st); return true;
         case 8: launch_route<RC, 8>(p, a, st); return true;
         case 16: launch_route<RC, 16>(p, a, st); return true;
-        case 32: launch_route<RC, 32>(p, a, st); return true;
     }
     return false;
 }
@@ -837,9 +934,8 @@ hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_
     a.topval = topval;
 
     switch (p.RT) {
-        case 1: launch_zpass<1>(p, x, R1t, zparts, T, h, r, st); break;
-        case 2: launch_zpass<2>(p, x, R1t, zparts, T, h, r, st); break;
-        case 4: launch_zpass<4>(p, x, R1t, zparts, T, h, r, st); break;
+        case 1: launch_zpass<1>(p, x, R1t, zparts, T, h, r, R2t, M, a.gnorm, st); break;
+        case 2: launch_zpass<2>(p, x, R1t, zparts, T, h, r, R2t, M, a.gnorm, st); break;
         default: return hipErrorInvalidValue;
     }
     if (p.hsplit > 1) {
@@ -853,7 +949,6 @@ hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_
         case 1: ok = dispatch_route_k<1>(p, a, st); break;
         case 2: ok = dispatch_route_k<2>(p, a, st); break;
         case 4: ok = dispatch_route_k<4>(p, a, st); break;
-        case 8: ok = dispatch_route_k<8>(p, a, st); break;
     }
     if (!ok) return hipErrorInvalidValue;
     return hipGetLastError();

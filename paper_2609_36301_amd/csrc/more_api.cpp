@@ -14,7 +14,7 @@ constexpr int32_t kMaxM = 1 << 30;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
-bool rank_supported(int32_t r) { return r == 16 || r == 32 || r == 64 || r == 128; }
+bool rank_supported(int32_t r) { return r == 16 || r == 32 || r == 64; }
 
 more_status check_common(int64_t T, int32_t h, int32_t M, int32_t k) {
     if (T < 0 || h <= 0 || M <= 0 || k < 1 || k > M) return MORE_ERR_INVALID_ARG;
@@ -27,7 +27,7 @@ more_status check_lowrank(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
     if (r <= 0) return MORE_ERR_INVALID_ARG;
     more_status s = check_common(T, h, M, k);
     if (s != MORE_OK) return s;
-    if (!rank_supported(r)) return MORE_ERR_UNSUPPORTED;
+    if (!rank_supported(r) || k > MORE_LOWRANK_K_MAX) return MORE_ERR_UNSUPPORTED;
     if (m_chunks < 0 || (m_chunks > 1 && (m_chunks % 8 != 0 || m_chunks > 1024)))
         return MORE_ERR_INVALID_ARG;
     return MORE_OK;

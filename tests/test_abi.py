@@ -72,6 +72,8 @@ def lowrank(lib, T=64, h=64, r=16, M=64, k=4, x=FAKE, R1t=FAKE, R2t=FAKE, idx=FA
     (dict(k=0), _lib.ERR_INVALID_ARG),
     (dict(k=65, M=64), _lib.ERR_INVALID_ARG),
     (dict(k=33, M=64), _lib.ERR_UNSUPPORTED),
+    (dict(k=17, M=64), _lib.ERR_UNSUPPORTED),
+    (dict(r=128), _lib.ERR_UNSUPPORTED),
     (dict(r=48), _lib.ERR_UNSUPPORTED),
     (dict(r=256), _lib.ERR_UNSUPPORTED),
     (dict(h=72), _lib.ERR_UNSUPPORTED),
@@ -133,7 +135,7 @@ def test_plans_for_the_paper_shapes(lib):
               "fine": (16384, 64, 65536, 8), "decode": (128, 64, 262144, 16)}
     for name, C in plans.items():
         T, r, M, k = shapes[name]
-        tokens_per_block = 256
+        tokens_per_block = 512
         assert C & (C - 1) == 0, name
         assert r * M * 2 // C <= 2 << 20, name          # expert slice fits one L2
         assert C * -(-T // tokens_per_block) >= 256, name  # at least one workgroup per CU
