@@ -43,7 +43,12 @@ def algorithmic(w):
     return nbytes, flops
 
 
+SCOPE = ("one routing call: the z pass, screen, threshold, collect and finalize kernels "
+         "(+ histogram), timed together as one step")
+
+
 def roofline(w, seconds):
+    """Position of one routing call against max(flops / MFMA peak, bytes / HBM peak)."""
     nbytes, flops = algorithmic(w)
     t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
     t_mfma = flops / (PEAK_BF16_TFLOPS * 1e12)
@@ -51,11 +56,11 @@ def roofline(w, seconds):
         achieved = nbytes / seconds / 1e9
         return {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
-                "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+                "kernel": SCOPE, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
     achieved = flops / seconds / 1e12
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-            "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+            "kernel": SCOPE, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
 
 
 def timed(fn, steps, warmup, stream):
