@@ -1,9 +1,10 @@
 // Per-expert selection counts (the bincount behind the load-balancing statistic f,
 // Appendix "Training"): counts[e] = #{(t, j) : idx[t][j] == e}.
 //
-// Small expert counts use a per-workgroup LDS histogram flushed with one global atomic per
-// non-empty bin; large ones add straight into global memory.  Counts are cleared by a fill
-// kernel (not a memset) so the sequence stays valid inside a captured HIP graph.
+// Each workgroup counts one slice of the ids for one range of 16384 experts in an LDS
+// histogram and flushes it with one global atomic per non-empty bin.  Counts are cleared by a
+// fill kernel (not a memset) so the sequence stays valid inside a captured HIP graph; the
+// routing call clears them in its threshold kernel instead.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -19,54 +20,47 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* __restrict__ p,
         p[i] = 0;
 }
 
+// Counts the ids in [b0, b0 + kLdsBins) over one slice of idx in an LDS histogram, then adds
+// the non-empty bins to counts with one global atomic each.  blockIdx.y selects the bin range,
+// blockIdx.x the slice; the per-workgroup aggregation keeps hot experts from serialising on
+// one global address.
 __global__ __launch_bounds__(256) void histogram_lds_kernel(const int32_t* __restrict__ idx,
                                                             int64_t n, int32_t M,
                                                             int32_t* __restrict__ counts) {
     __shared__ int32_t bins[kLdsBins];
-    for (int32_t e = threadIdx.x; e < M; e += blockDim.x) bins[e] = 0;
+    const int32_t b0 = (int32_t)blockIdx.y * kLdsBins;
+    const int32_t nb = M - b0 < kLdsBins ? M - b0 : kLdsBins;
+    for (int32_t e = threadIdx.x; e < nb; e += blockDim.x) bins[e] = 0;
     __syncthreads();
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t e = idx[i];
-        if (e >= 0 && e < M) atomicAdd(&bins[e], 1);
+    const int64_t per = (n + gridDim.x - 1) / gridDim.x;
+    const int64_t i0 = (int64_t)blockIdx.x * per;
+    const int64_t i1 = i0 + per < n ? i0 + per : n;
+    for (int64_t i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
+        const int32_t e = idx[i] - b0;
+        if (e >= 0 && e < nb) atomicAdd(&bins[e], 1);
     }
     __syncthreads();
-    for (int32_t e = threadIdx.x; e < M; e += blockDim.x) {
+    for (int32_t e = threadIdx.x; e < nb; e += blockDim.x) {
         const int32_t c = bins[e];
-        if (c) atomicAdd(&counts[e], c);
-    }
-}
-
-__global__ __launch_bounds__(256) void histogram_global_kernel(const int32_t* __restrict__ idx,
-                                                               int64_t n, int32_t M,
-                                                               int32_t* __restrict__ counts) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const int32_t e = idx[i];
-        if (e >= 0 && e < M) atomicAdd(&counts[e], 1);
+        if (c) atomicAdd(&counts[b0 + e], c);
     }
 }
 
 hipError_t histogram_launch(const int32_t* idx, int64_t n, int32_t M, int32_t* counts,
-                            hipStream_t st) {
-    {
+                            hipStream_t st, bool counts_zeroed) {
+    if (!counts_zeroed) {
         int64_t blocks = ((int64_t)M + 255) / 256;
         if (blocks > 1024) blocks = 1024;
         hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, counts,
                            (int64_t)M);
     }
     if (n > 0) {
-        if (M <= kLdsBins) {
-            int64_t blocks = n / 8192;
-            blocks = blocks < 1 ? 1 : (blocks > 128 ? 128 : blocks);
-            hipLaunchKernelGGL(histogram_lds_kernel, dim3((unsigned)blocks), dim3(256), 0, st, idx,
-                               n, M, counts);
-        } else {
-            int64_t blocks = (n + 255) / 256;
-            blocks = blocks > 2048 ? 2048 : blocks;
-            hipLaunchKernelGGL(histogram_global_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
-                               idx, n, M, counts);
-        }
+        const int64_t ranges = ((int64_t)M + kLdsBins - 1) / kLdsBins;
+        int64_t slices = n / 4096;
+        const int64_t max_slices = 256 / ranges > 1 ? 256 / ranges : 1;
+        slices = slices < 1 ? 1 : (slices > max_slices ? max_slices : slices);
+        hipLaunchKernelGGL(histogram_lds_kernel, dim3((unsigned)slices, (unsigned)ranges),
+                           dim3(256), 0, st, idx, n, M, counts);
     }
     return hipGetLastError();
 }

@@ -27,13 +27,15 @@ struct LowrankPlan {
 bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, int32_t m_chunks,
                        LowrankPlan* plan);
 
+// counts (nullable) is cleared by the launch, ready for histogram_launch(..., true).
 hipError_t lowrank_launch(const LowrankPlan& plan, const uint16_t* x, const uint16_t* R1t,
                           const uint16_t* R2t, int64_t T, int32_t h, int32_t r, int32_t M,
-                          int32_t k, int32_t* idx, float* gate, float* topval, void* workspace,
-                          hipStream_t stream);
+                          int32_t k, int32_t* idx, float* gate, float* topval,
+                          int32_t* counts, void* workspace, hipStream_t stream);
 
+// counts_zeroed: the caller has already cleared counts on this stream.
 hipError_t histogram_launch(const int32_t* idx, int64_t n, int32_t M, int32_t* counts,
-                            hipStream_t stream);
+                            hipStream_t stream, bool counts_zeroed = false);
 
 struct FullrankPlan {
     int32_t K;

@@ -45,7 +45,7 @@ __device__ __forceinline__ void unroll(F&& f) {
 // ------------------------------------------------------------------------------ zpass
 // One workgroup = 4 waves = 128 tokens, wave w owning tokens 32w..32w+31 of the block.  The h
 // axis is walked in chunks of 64 (4 MFMA k-steps); the chunk of R1 (all rank rows) is staged
-// in LDS and shared by the four waves, x is prefetched D chunks ahead in registers.  With
+// in LDS and shared by the four waves; x and R1 are prefetched D chunks ahead in registers.  With
 // hsplit > 1 the chunks are split over hsplit workgroups and each split writes a partial z.
 constexpr int kZWaves = 4;
 constexpr int kZTokens = 32 * kZWaves;
@@ -128,8 +128,11 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
             xb[decltype(slot)::value][j] = *reinterpret_cast<const u32x4*>(xrow + 16 * step);
         }
     };
-    u32x4 rb[RLOADS];
-    auto rload = [&](int c) __attribute__((always_inline)) {
+    // R1 chunks use the same D-deep register ring as x: chunk c sits in ring slot c mod D,
+    // is stored to LDS buffer c mod 2 one chunk ahead of its use, and its slot is then
+    // refilled with chunk c + D.
+    u32x4 rb[D][RLOADS];
+    auto rload = [&](auto slot, int c) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < RLOADS; ++i) {
             const int seg = tid + 256 * i;
@@ -137,15 +140,15 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
             const int rr = row < r ? row : r - 1;
             int hc = (cbeg + c) * kZChunk + col * 8;
             hc = hc < h ? hc : h - 8;
-            rb[i] = *reinterpret_cast<const u32x4*>(R1t + (int64_t)rr * h + hc);
+            rb[decltype(slot)::value][i] = *reinterpret_cast<const u32x4*>(R1t + (int64_t)rr * h + hc);
         }
     };
-    auto rstash = [&](int buf) __attribute__((always_inline)) {
+    auto rstash = [&](auto slot, int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < RLOADS; ++i) {
             const int seg = tid + 256 * i;
             const int row = seg >> 3, col = seg & 7;
-            *reinterpret_cast<u32x4*>(&r1s[buf][row * LROW + col * 8]) = rb[i];
+            *reinterpret_cast<u32x4*>(&r1s[buf][row * LROW + col * 8]) = rb[decltype(slot)::value][i];
         }
     };
 
@@ -153,20 +156,23 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
 #pragma unroll
     for (int pt = 0; pt < RT; ++pt) acc[pt] = zero_f32x16();
     if (nc > 0) {
-        unroll<D>([&](auto s) __attribute__((always_inline)) { xload(s, decltype(s)::value); });
-        rload(0);
-        rstash(0);
-        rload(1);
+        unroll<D>([&](auto s) __attribute__((always_inline)) {
+            xload(s, decltype(s)::value);
+            rload(s, decltype(s)::value);
+        });
+        rstash(std::integral_constant<int, 0>{}, 0);
+        rload(std::integral_constant<int, 0>{}, D);
         __syncthreads();
         for (int cb = 0; cb < nc; cb += D) {
             unroll<D>([&](auto p) __attribute__((always_inline)) {
-                const int c = cb + decltype(p)::value;
+                constexpr int P = decltype(p)::value;
+                const int c = cb + P;
                 if (c < nc) {
                     const int buf = c & 1;
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
                         if (4 * (cbeg + c) + j < S) {
-                            const bf16x8 b = __builtin_bit_cast(bf16x8, xb[decltype(p)::value][j]);
+                            const bf16x8 b = __builtin_bit_cast(bf16x8, xb[P][j]);
 #pragma unroll
                             for (int pt = 0; pt < RT; ++pt) {
                                 const bf16x8 a = load_bf16x8(
@@ -176,8 +182,8 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
                         }
                     }
                     xload(p, c + D);
-                    rstash(buf ^ 1);
-                    rload(c + 2);
+                    rstash(std::integral_constant<int, (P + 1) % D>{}, buf ^ 1);
+                    rload(std::integral_constant<int, (P + 1) % D>{}, c + 1 + D);
                     __syncthreads();
                 }
             });
@@ -535,13 +541,18 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
 // Threshold per token: theta = the k-th largest of the union of all chunks' lists, lowered by
 // a rounding guard.  k distinct experts have logit >= theta, so the k-th largest logit is >=
 // theta and every expert of the top k has s_e + c N_g >= theta.  G threads per token (a power
-// of two <= 64) share the chunk lists.  Also clears the token's candidate count.
+// of two <= 64) share the chunk lists.  Also clears the token's candidate count and, when
+// hist is set, the per-expert histogram.
 template <int K>
 __global__ __launch_bounds__(256) void theta_kernel(const float* __restrict__ top, int32_t T,
                                                     int32_t chunks, int32_t k, int32_t G,
                                                     float* __restrict__ theta,
-                                                    int32_t* __restrict__ count) {
+                                                    int32_t* __restrict__ count,
+                                                    int32_t* __restrict__ hist, int32_t M) {
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (hist) {  // clear the per-expert histogram for this call
+        for (int64_t e = gid; e < M; e += (int64_t)gridDim.x * blockDim.x) hist[e] = 0;
+    }
     const int64_t tok = gid / G;
     const int g = (int)(gid % G);
     const bool ok = tok < T;
@@ -633,16 +644,22 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
             [&](f32x16 (&acc)[kTPW], int32_t e0, bool partial, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
                 (void)u;
+                // Tile test with the lane's largest group norm (a looser bound, one compare
+                // per token group); the exact per-group tests run only when it passes.
+                const float nmax = fmaxf(fmaxf(nq[0], nq[1]), fmaxf(nq[2], nq[3]));
 #pragma unroll
                 for (int g = 0; g < kTPW; ++g) {
                     if (partial) mask_past_end(acc[g], e0, M, half);
-                    float tq[4], gm[4];
+                    const float m16 = fmaxf(fmaxf(fmaxf(max4(acc[g], 0), max4(acc[g], 1)),
+                                                  max4(acc[g], 2)),
+                                            max4(acc[g], 3));
+                    if (m16 >= th[g] - tg.c[g] * nmax) {
+                        float tq[4], gm[4];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        tq[q] = th[g] - tg.c[g] * nq[q];
-                        gm[q] = max4(acc[g], q) - tq[q];
-                    }
-                    if (fmaxf(fmaxf(gm[0], gm[1]), fmaxf(gm[2], gm[3])) >= 0.0f) {
+                        for (int q = 0; q < 4; ++q) {
+                            tq[q] = th[g] - tg.c[g] * nq[q];
+                            gm[q] = max4(acc[g], q) - tq[q];
+                        }
 #pragma unroll
                         for (int q = 0; q < 4; ++q) {
                             if (gm[q] >= 0.0f) {
@@ -870,7 +887,7 @@ static void launch_zpass(const LowrankPlan& p, const uint16_t* x, const uint16_t
     const int64_t zblocks = (T + kZTokens - 1) / kZTokens;
     const int64_t nblocks = (((int64_t)M + 31) / 32 * 32 * (r / 8) + 255) / 256;  // group norms
     dim3 grid((unsigned)(zblocks * p.hsplit + nblocks));
-    constexpr int D = RT <= 2 ? 8 : 4;
+    constexpr int D = 2;
     hipLaunchKernelGGL((zpass_kernel<RT, D>), grid, dim3(256), 0, st, x, R1t, zparts, (int32_t)T,
                        h, r, p.steps_per_split, R2t, M, (int32_t)zblocks, p.hsplit, gnorm);
 }
@@ -880,7 +897,7 @@ struct RouteArgs {
     const uint16_t* R2t;
     int32_t T, M, k;
     float *top, *gnorm, *theta;
-    int32_t *count, *cand;
+    int32_t *count, *cand, *hist;
     int32_t* idx;
     float *gate, *topval;
 };
@@ -892,7 +909,7 @@ static void launch_route(const LowrankPlan& p, const RouteArgs& a, hipStream_t s
                        a.M, p.chunks, p.splits, a.gnorm, a.top);
     const int64_t nth = (int64_t)a.T * p.theta_group;
     hipLaunchKernelGGL((theta_kernel<K>), dim3((unsigned)((nth + 255) / 256)), dim3(256), 0, st,
-                       a.top, a.T, p.chunks, a.k, p.theta_group, a.theta, a.count);
+                       a.top, a.T, p.chunks, a.k, p.theta_group, a.theta, a.count, a.hist, a.M);
     hipLaunchKernelGGL((collect_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.z, a.R2t, a.T,
                        a.M, p.chunks, p.splits, a.theta, a.gnorm, a.count, a.cand, p.cap);
     hipLaunchKernelGGL((finalize_kernel<RC, K>), dim3((unsigned)((a.T + 31) / 32)), dim3(256), 0,
@@ -914,8 +931,8 @@ static bool dispatch_route_k(const LowrankPlan& p, const RouteArgs& a, hipStream
 
 hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_t* R1t,
                           const uint16_t* R2t, int64_t T, int32_t h, int32_t r, int32_t M,
-                          int32_t k, int32_t* idx, float* gate, float* topval, void* workspace,
-                          hipStream_t st) {
+                          int32_t k, int32_t* idx, float* gate, float* topval, int32_t* counts,
+                          void* workspace, hipStream_t st) {
     char* ws = static_cast<char*>(workspace);
     float* zparts = reinterpret_cast<float*>(ws + p.off_zparts);
     RouteArgs a;
@@ -929,6 +946,7 @@ hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_
     a.theta = reinterpret_cast<float*>(ws + p.off_tau);
     a.count = reinterpret_cast<int32_t*>(ws + p.off_count);
     a.cand = reinterpret_cast<int32_t*>(ws + p.off_cand);
+    a.hist = counts;
     a.idx = idx;
     a.gate = gate;
     a.topval = topval;

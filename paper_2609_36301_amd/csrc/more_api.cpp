@@ -104,9 +104,10 @@ more_status more_route_lowrank_ex(const uint16_t* x, const uint16_t* R1t, const 
     if (p.workspace_bytes > 0 && (!workspace || workspace_bytes < p.workspace_bytes))
         return MORE_ERR_WORKSPACE;
     hipError_t e = more::lowrank_launch(p, x, R1t, R2t, T, h, r, M, k, idx, gate, topval,
-                                        workspace, st);
+                                        counts, workspace, st);
     if (e != hipSuccess) return MORE_ERR_HIP;
-    if (counts) return from_hip(more::histogram_launch(idx, T * (int64_t)k, M, counts, st));
+    if (counts)  // cleared by the routing launch above
+        return from_hip(more::histogram_launch(idx, T * (int64_t)k, M, counts, st, true));
     return MORE_OK;
 }
 
