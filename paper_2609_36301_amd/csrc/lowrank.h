@@ -15,11 +15,11 @@ struct LowrankPlan {
     int32_t ntb;              // token blocks of 512 tokens
     int32_t chunks;           // expert-axis chunks, each resident in one workgroup's LDS
     int32_t splits;           // token-block ranges per chunk (route grid = chunks * splits)
-    int32_t theta_group;      // threads per token in the threshold kernel
     int32_t cap;              // candidate slots per token
+    int32_t theta_group;      // threads per token in the threshold kernel
     int32_t hsplit;           // workgroups sharing the h axis of one token group in the z pass
     int32_t steps_per_split;  // 64-wide h chunks per z-pass workgroup
-    size_t off_zparts, off_z, off_top, off_gnorm, off_tau, off_count, off_cand;
+    size_t off_zparts, off_z, off_zhi, off_cz, off_top, off_gnorm, off_tau, off_count, off_cand;
     size_t workspace_bytes;
 };
 

@@ -42,6 +42,12 @@ __device__ __forceinline__ void unroll(F&& f) {
     unroll_impl(f, std::make_integer_sequence<int, N>{});
 }
 
+// Error scale of the screened logits of one token (see the route section):
+// c = (||z_lo|| + r 2^-23 ||z_hi||) (1 + 2^-10), from the squared norms.
+__device__ __forceinline__ float screen_scale(float lo2, float hi2, int r) {
+    return (sqrtf(lo2) + (float)r * 0x1p-23f * sqrtf(hi2)) * (1.0f + 0x1p-10f);
+}
+
 // ------------------------------------------------------------------------------ zpass
 // One workgroup = 4 waves = 128 tokens, wave w owning tokens 32w..32w+31 of the block.  The h
 // axis is walked in chunks of 64 (4 MFMA k-steps); the chunk of R1 (all rank rows) is staged
@@ -80,7 +86,9 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
                                                     int32_t r, int32_t chunks_per_split,
                                                     const uint16_t* __restrict__ R2t, int32_t M,
                                                     int32_t zblocks, int32_t hsplit,
-                                                    float* __restrict__ gnorm) {
+                                                    float* __restrict__ gnorm,
+                                                    uint16_t* __restrict__ zhi_out,
+                                                    float* __restrict__ c_out) {
     // Workgroups [0, zblocks * hsplit) compute z (token block bx % zblocks, h split
     // bx / zblocks); the rest compute group norms.
     if ((int)blockIdx.x >= zblocks * hsplit) {  // workgroup-uniform: a group-norm workgroup
@@ -190,37 +198,86 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
         }
     }
 
-    if (tok_ok) {
-        float* zrow = zout + ((int64_t)split * T + tok) * r + 8 * half;
+    // Lane (n, half) holds z[n][16 c + 8 half + 0..7] in accumulator elements 8 c2 .. 8 c2 + 7
+    // of tile pt (c = 2 pt + c2).  Without an h split the z pass also writes the screening
+    // operands: z_hi = bf16(z) in the same layout and the error scale c of the token.
+    float lo2 = 0.0f, hi2 = 0.0f;
+    float* zrow = zout + ((int64_t)split * T + (tok_ok ? tok : 0)) * r + 8 * half;
+    uint16_t* hrow = zhi_out + (tok_ok ? tok : 0) * (int64_t)r + 8 * half;
 #pragma unroll
-        for (int pt = 0; pt < RT; ++pt) {
+    for (int pt = 0; pt < RT; ++pt) {
 #pragma unroll
-            for (int c2 = 0; c2 < 2; ++c2) {
-                const int c = 2 * pt + c2;
-                if (16 * c < r) {
-                    f32x4 lo4, hi4;
+        for (int c2 = 0; c2 < 2; ++c2) {
+            const int c = 2 * pt + c2;
+            if (16 * c < r) {
+                f32x4 lo4, hi4;
+                bf16x8 hb;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        lo4[q] = acc[pt][8 * c2 + q];
-                        hi4[q] = acc[pt][8 * c2 + 4 + q];
-                    }
+                for (int q = 0; q < 4; ++q) {
+                    lo4[q] = acc[pt][8 * c2 + q];
+                    hi4[q] = acc[pt][8 * c2 + 4 + q];
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const float v = acc[pt][8 * c2 + q];
+                    hb[q] = (__bf16)v;
+                    const float hf = (float)hb[q];
+                    const float lf = v - hf;
+                    hi2 = fmaf(hf, hf, hi2);
+                    lo2 = fmaf(lf, lf, lo2);
+                }
+                if (tok_ok) {
                     *reinterpret_cast<f32x4*>(zrow + 16 * c) = lo4;
                     *reinterpret_cast<f32x4*>(zrow + 16 * c + 4) = hi4;
+                    if (hsplit == 1)
+                        *reinterpret_cast<u32x4*>(hrow + 16 * c) = __builtin_bit_cast(u32x4, hb);
                 }
             }
         }
     }
+    if (hsplit == 1) {
+        hi2 += __shfl_xor(hi2, 32, kWave);
+        lo2 += __shfl_xor(lo2, 32, kWave);
+        if (tok_ok && half == 0) c_out[tok] = screen_scale(lo2, hi2, r);
+    }
 }
 
-// z[i] = sum over splits s of zparts[s][i], in split order.
+// Sums the h-split partials of z (per element, splits in increasing order), then writes z,
+// z_hi = bf16(z) and the token's error scale c.  256 threads = 256 / r tokens, one thread per
+// element; the r threads of a token are consecutive lanes of one wave.
 __global__ __launch_bounds__(256) void zreduce_kernel(const float* __restrict__ zparts,
-                                                      float* __restrict__ z, int64_t n,
-                                                      int32_t splits) {
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        float s = 0.0f;
-        for (int p = 0; p < splits; ++p) s += zparts[(int64_t)p * n + i];
+                                                      float* __restrict__ z,
+                                                      uint16_t* __restrict__ zhi,
+                                                      float* __restrict__ cz, int32_t T,
+                                                      int32_t r, int32_t splits) {
+    const int64_t n = (int64_t)T * r;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const bool ok = i < n;
+    float s = 0.0f;
+    if (ok) {
+        // 16 partials are loaded before they are added (still in split order).
+        int p = 0;
+        for (; p + 16 <= splits; p += 16) {
+            float v[16];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) v[j] = zparts[(int64_t)(p + j) * n + i];
+#pragma unroll
+            for (int j = 0; j < 16; ++j) s += v[j];
+        }
+        for (; p < splits; ++p) s += zparts[(int64_t)p * n + i];
+    }
+    const __bf16 hb = (__bf16)s;
+    const float hf = (float)hb;
+    const float lf = s - hf;
+    float hi2 = hf * hf, lo2 = lf * lf;
+    for (int m = 1; m < r; m <<= 1) {
+        hi2 += __shfl_xor(hi2, m, kWave);
+        lo2 += __shfl_xor(lo2, m, kWave);
+    }
+    if (ok) {
         z[i] = s;
+        zhi[i] = __builtin_bit_cast(uint16_t, hb);
+        if (i % r == 0) cz[i / r] = screen_scale(lo2, hi2, r);
     }
 }
 
@@ -368,8 +425,8 @@ __device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ R2t,
     __syncthreads();
 }
 
-// Token ids, z operands and the error scale c of one lane, for each of the wave's kTPW groups
-// of 32 tokens starting at `first`.
+// Token ids, z_hi operands and error scales of one lane, for each of the wave's kTPW groups of
+// 32 tokens starting at `first` (written by the z pass; zeros past T).
 template <int RC>
 struct TokenGroups {
     int64_t tok[kTPW];
@@ -377,43 +434,21 @@ struct TokenGroups {
     bf16x8 zhi[kTPW][RC];
     float c[kTPW];
 
-    __device__ __forceinline__ void load(const float* __restrict__ z, int32_t T, int64_t first,
+    __device__ __forceinline__ void load(const uint16_t* __restrict__ zh,
+                                         const float* __restrict__ cz, int32_t T, int64_t first,
                                          int n, int half) {
         constexpr int R = 16 * RC;
 #pragma unroll
         for (int g = 0; g < kTPW; ++g) {
             tok[g] = first + 32 * g + n;
             tok_ok[g] = tok[g] < T;
-            float lo2 = 0.0f, hi2 = 0.0f;
+            const int64_t t = tok_ok[g] ? tok[g] : 0;
 #pragma unroll
             for (int cc = 0; cc < RC; ++cc) {
-                float v[8];
-                if (tok_ok[g]) {
-                    const f32x4* p =
-                        reinterpret_cast<const f32x4*>(z + tok[g] * R + 16 * cc + 8 * half);
-                    const f32x4 a0 = p[0], a1 = p[1];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        v[q] = a0[q];
-                        v[4 + q] = a1[q];
-                    }
-                } else {
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) v[q] = 0.0f;
-                }
-#pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const __bf16 hb = (__bf16)v[q];
-                    const float hf = (float)hb;
-                    const float lf = v[q] - hf;
-                    zhi[g][cc][q] = hb;
-                    hi2 = fmaf(hf, hf, hi2);
-                    lo2 = fmaf(lf, lf, lo2);
-                }
+                const bf16x8 v = load_bf16x8(zh + t * R + 16 * cc + 8 * half);
+                zhi[g][cc] = tok_ok[g] ? v : zero_bf16x8();
             }
-            hi2 += __shfl_xor(hi2, 32, kWave);
-            lo2 += __shfl_xor(lo2, 32, kWave);
-            c[g] = (sqrtf(lo2) + (float)R * 0x1p-23f * sqrtf(hi2)) * (1.0f + 0x1p-10f);
+            c[g] = tok_ok[g] ? cz[t] : 0.0f;
         }
     }
 };
@@ -486,8 +521,9 @@ __device__ __forceinline__ void sweep_resident(const uint16_t* rows, const float
 // Output per token and chunk: those K values, descending, in top[chunk][token][0..K-1].
 template <int RC, int K>
 __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
-    const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
-    int32_t chunks, int32_t splits, const float* __restrict__ gnorm, float* __restrict__ top) {
+    const uint16_t* __restrict__ zh, const float* __restrict__ cz,
+    const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t chunks, int32_t splits,
+    const float* __restrict__ gnorm, float* __restrict__ top) {
     using C = RouteCfg<RC, K>;
     constexpr int U = C::U, L = C::L;
     __shared__ __attribute__((aligned(16))) uint16_t rows[C::EMAX * C::R];
@@ -498,11 +534,16 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 31, half = lane >> 5;
 
+    // The next block's operands are loaded while the current block is swept.
+    TokenGroups<RC> tg, nx;
+    const int64_t wofs = (int64_t)w * 32 * kTPW;
+    if (sp.blk0 < sp.blk1 && sp.blk0 * kRouteTokens + wofs < T)
+        tg.load(zh, cz, T, sp.blk0 * kRouteTokens + wofs, n, half);
     for (int64_t blk = sp.blk0; blk < sp.blk1; ++blk) {
-        const int64_t first = blk * kRouteTokens + (int64_t)w * 32 * kTPW;
+        const int64_t first = blk * kRouteTokens + wofs;
         if (first >= T) break;  // wave-uniform
-        TokenGroups<RC> tg;
-        tg.load(z, T, first, n, half);
+        const bool has_next = blk + 1 < sp.blk1 && first + kRouteTokens < T;
+        if (has_next) nx.load(zh, cz, T, first + kRouteTokens, n, half);
         float bm[kTPW][L];
 #pragma unroll
         for (int g = 0; g < kTPW; ++g)
@@ -535,6 +576,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
                 for (int j = 0; j < K; ++j) o[j] = bm[g][j];
             }
         }
+        if (has_next) tg = nx;
     }
 }
 
@@ -610,10 +652,10 @@ __global__ __launch_bounds__(256) void theta_kernel(const float* __restrict__ to
 // overflowed (count > cap), which sends it to the exact sweep of the finalize kernel.
 template <int RC, int K>
 __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
-    const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
-    int32_t chunks, int32_t splits, const float* __restrict__ theta,
-    const float* __restrict__ gnorm, int32_t* __restrict__ count, int32_t* __restrict__ cand,
-    int32_t cap) {
+    const uint16_t* __restrict__ zh, const float* __restrict__ cz,
+    const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t chunks, int32_t splits,
+    const float* __restrict__ theta, const float* __restrict__ gnorm,
+    int32_t* __restrict__ count, int32_t* __restrict__ cand, int32_t cap) {
     using C = RouteCfg<RC, K>;
     __shared__ __attribute__((aligned(16))) uint16_t rows[C::EMAX * C::R];
     __shared__ __attribute__((aligned(16))) float gn[C::EMAX / 4];
@@ -626,19 +668,31 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
     const int n = lane & 31, half = lane >> 5;
     const int32_t ebase = (int32_t)(sp.t0 * 32);
 
+    // The next block's operands and thresholds are loaded while the current block is swept.
+    TokenGroups<RC> tg, nx;
+    float th[kTPW], nth[kTPW];
+    auto load_theta = [&](const TokenGroups<RC>& q, float (&o)[kTPW])
+                          __attribute__((always_inline)) {
+#pragma unroll
+        for (int g = 0; g < kTPW; ++g)  // lanes past T never qualify (+inf threshold)
+            o[g] = q.tok_ok[g] ? theta[q.tok[g]] : __builtin_huge_valf();
+    };
+    const int64_t wofs = (int64_t)w * 32 * kTPW;
+    if (sp.blk0 < sp.blk1 && sp.blk0 * kRouteTokens + wofs < T) {
+        tg.load(zh, cz, T, sp.blk0 * kRouteTokens + wofs, n, half);
+        load_theta(tg, th);
+    }
     for (int64_t blk = sp.blk0; blk < sp.blk1; ++blk) {
-        const int64_t first = blk * kRouteTokens + (int64_t)w * 32 * kTPW;
+        const int64_t first = blk * kRouteTokens + wofs;
         if (first >= T) break;  // wave-uniform
-        TokenGroups<RC> tg;
-        tg.load(z, T, first, n, half);
-        float th[kTPW];
+        const bool has_next = blk + 1 < sp.blk1 && first + kRouteTokens < T;
+        if (has_next) {
+            nx.load(zh, cz, T, first + kRouteTokens, n, half);
+            load_theta(nx, nth);
+        }
         int cnt[kTPW];
 #pragma unroll
-        for (int g = 0; g < kTPW; ++g) {
-            // Lanes past T never qualify (+inf threshold).
-            th[g] = tg.tok_ok[g] ? theta[tg.tok[g]] : __builtin_huge_valf();
-            cnt[g] = 0;
-        }
+        for (int g = 0; g < kTPW; ++g) cnt[g] = 0;
         sweep_resident<RC, K>(
             rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
             [&](f32x16 (&acc)[kTPW], int32_t e0, bool partial, auto u, const f32x4& nq)
@@ -691,6 +745,11 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
                     if (off + i < cap)
                         cand[tg.tok[g] * cap + off + i] = ebase + (int32_t)slots[i][g][tid];
             }
+        }
+        if (has_next) {
+            tg = nx;
+#pragma unroll
+            for (int g = 0; g < kTPW; ++g) th[g] = nth[g];
         }
     }
 }
@@ -845,7 +904,6 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     q.splits = (int32_t)S;
     q.theta_group = 1;
     while (q.theta_group < 64 && q.theta_group * 16 < q.chunks) q.theta_group *= 2;
-    q.cap = 512;
     // z pass: 128-token blocks; the h chunks are split over workgroups only when there are
     // too few token blocks to occupy the chip.
     const int32_t NC = (h / 16 + 3) / 4;
@@ -864,12 +922,17 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     } else {
         q.off_z = q.off_zparts;
     }
+    q.off_zhi = off;
+    off += align256((size_t)T * r * sizeof(uint16_t));
+    q.off_cz = off;
+    off += align256((size_t)T * sizeof(float));
     q.off_top = off;
     off += align256((size_t)q.chunks * T * q.K * sizeof(float));
     q.off_gnorm = off;
     off += align256((size_t)Mt * 8 * sizeof(float));
     q.off_tau = off;
     off += align256((size_t)T * sizeof(float));
+    q.cap = 512;
     q.off_count = off;
     off += align256((size_t)T * sizeof(int32_t));
     q.off_cand = off;
@@ -883,17 +946,20 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
 template <int RT>
 static void launch_zpass(const LowrankPlan& p, const uint16_t* x, const uint16_t* R1t, float* zparts,
                          int64_t T, int32_t h, int32_t r, const uint16_t* R2t, int32_t M,
-                         float* gnorm, hipStream_t st) {
+                         float* gnorm, uint16_t* zhi, float* cz, hipStream_t st) {
     const int64_t zblocks = (T + kZTokens - 1) / kZTokens;
     const int64_t nblocks = (((int64_t)M + 31) / 32 * 32 * (r / 8) + 255) / 256;  // group norms
     dim3 grid((unsigned)(zblocks * p.hsplit + nblocks));
     constexpr int D = 2;
     hipLaunchKernelGGL((zpass_kernel<RT, D>), grid, dim3(256), 0, st, x, R1t, zparts, (int32_t)T,
-                       h, r, p.steps_per_split, R2t, M, (int32_t)zblocks, p.hsplit, gnorm);
+                       h, r, p.steps_per_split, R2t, M, (int32_t)zblocks, p.hsplit, gnorm, zhi,
+                       cz);
 }
 
 struct RouteArgs {
     const float* z;
+    uint16_t* zhi;
+    float* cz;
     const uint16_t* R2t;
     int32_t T, M, k;
     float *top, *gnorm, *theta;
@@ -905,13 +971,14 @@ struct RouteArgs {
 template <int RC, int K>
 static void launch_route(const LowrankPlan& p, const RouteArgs& a, hipStream_t st) {
     const dim3 grid((unsigned)((int64_t)p.splits * p.chunks));
-    hipLaunchKernelGGL((screen_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.z, a.R2t, a.T,
-                       a.M, p.chunks, p.splits, a.gnorm, a.top);
+    hipLaunchKernelGGL((screen_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.zhi, a.cz,
+                       a.R2t, a.T, a.M, p.chunks, p.splits, a.gnorm, a.top);
     const int64_t nth = (int64_t)a.T * p.theta_group;
     hipLaunchKernelGGL((theta_kernel<K>), dim3((unsigned)((nth + 255) / 256)), dim3(256), 0, st,
                        a.top, a.T, p.chunks, a.k, p.theta_group, a.theta, a.count, a.hist, a.M);
-    hipLaunchKernelGGL((collect_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.z, a.R2t, a.T,
-                       a.M, p.chunks, p.splits, a.theta, a.gnorm, a.count, a.cand, p.cap);
+    hipLaunchKernelGGL((collect_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.zhi, a.cz,
+                       a.R2t, a.T, a.M, p.chunks, p.splits, a.theta, a.gnorm, a.count, a.cand,
+                       p.cap);
     hipLaunchKernelGGL((finalize_kernel<RC, K>), dim3((unsigned)((a.T + 31) / 32)), dim3(256), 0,
                        st, a.z, a.R2t, a.T, a.M, a.k, a.count, a.cand, p.cap, a.idx, a.gate,
                        a.topval);
@@ -937,6 +1004,8 @@ hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_
     float* zparts = reinterpret_cast<float*>(ws + p.off_zparts);
     RouteArgs a;
     a.z = reinterpret_cast<float*>(ws + p.off_z);
+    a.zhi = reinterpret_cast<uint16_t*>(ws + p.off_zhi);
+    a.cz = reinterpret_cast<float*>(ws + p.off_cz);
     a.R2t = R2t;
     a.T = (int32_t)T;
     a.M = M;
@@ -952,15 +1021,17 @@ hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_
     a.topval = topval;
 
     switch (p.RT) {
-        case 1: launch_zpass<1>(p, x, R1t, zparts, T, h, r, R2t, M, a.gnorm, st); break;
-        case 2: launch_zpass<2>(p, x, R1t, zparts, T, h, r, R2t, M, a.gnorm, st); break;
+        case 1: launch_zpass<1>(p, x, R1t, zparts, T, h, r, R2t, M, a.gnorm, a.zhi, a.cz, st);
+            break;
+        case 2: launch_zpass<2>(p, x, R1t, zparts, T, h, r, R2t, M, a.gnorm, a.zhi, a.cz, st);
+            break;
         default: return hipErrorInvalidValue;
     }
     if (p.hsplit > 1) {
         const int64_t n = T * r;
-        const unsigned blocks = (unsigned)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096);
-        hipLaunchKernelGGL(zreduce_kernel, dim3(blocks), dim3(256), 0, st, zparts,
-                           const_cast<float*>(a.z), n, p.hsplit);
+        hipLaunchKernelGGL(zreduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                           zparts, const_cast<float*>(a.z), a.zhi, a.cz, (int32_t)T, r,
+                           p.hsplit);
     }
     bool ok = false;
     switch (p.RC) {
