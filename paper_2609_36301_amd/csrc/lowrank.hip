@@ -284,9 +284,9 @@ __global__ __launch_bounds__(256) void zreduce_kernel(const float* __restrict__ 
 // ------------------------------------------------------------------------------ route
 // Screen and collect workgroups are expert-resident: a workgroup loads one chunk of the
 // expert axis (up to 128 KiB of R2t rows, with their group norms) into LDS once, then its 8
-// waves sweep that chunk for token blocks of 512 tokens (wave w takes the kTPW groups of 32
-// tokens 64w .. 64w+63 of the block), with no barrier inside the token loop.  Each A operand
-// read from LDS feeds kTPW MFMAs.
+// waves sweep that chunk for token blocks of 8 * 32 * TPW tokens (wave w takes the TPW groups
+// of 32 tokens starting at 32 TPW w), with no barrier inside the token loop.  Each A operand
+// read from LDS feeds TPW MFMAs, so a larger TPW means less LDS traffic per MFMA.
 //
 // Screening precision.  The sweeps compute s_e = z_hi . u_e on the matrix cores, with z_hi =
 // bf16(z) and fp32 accumulation, instead of the logit l_e = z . u_e.  With z_lo = z - z_hi,
@@ -295,11 +295,12 @@ __global__ __launch_bounds__(256) void zreduce_kernel(const float* __restrict__ 
 // and ||u_e|| <= N_g, the largest row norm of the 4-expert group g holding e.  So s_e - c N_g
 // is a lower and s_e + c N_g an upper bound of l_e.
 constexpr int kRouteWaves = 8;
-constexpr int kTPW = 2;
 constexpr int kRouteThreads = 64 * kRouteWaves;
-constexpr int kRouteTokens = 32 * kTPW * kRouteWaves;
-constexpr int kLaneSlots = 8;                 // candidate slots per lane and token group
 constexpr int kChunkBytes = 128 * 1024;       // LDS for the resident expert rows
+
+// Token groups of 32 per wave: 4 at r = 64 and K <= 8 (the A-operand reads from LDS, which do not
+// overlap the MFMAs, then cost half as much per MFMA), else 2.
+__host__ __device__ constexpr int route_tpw(int RC, int K) { return RC == 4 && K <= 8 ? 4 : 2; }
 
 template <int RC, int K>
 struct RouteCfg {
@@ -308,6 +309,12 @@ struct RouteCfg {
     static constexpr int U = K / 4 > 1 ? K / 4 : 1;       // bucket period, in tiles
     static constexpr int L = 4 * U;                       // bucket maxima per lane (>= K)
     static constexpr int EMAX = kChunkBytes / (2 * R);    // experts per chunk (multiple of 32)
+    static constexpr int TPW = route_tpw(RC, K);          // token groups per wave
+    static constexpr int TOK = 32 * TPW * kRouteWaves;    // tokens per block
+    // candidate slots per lane and token group (the collect kernel's LDS must stay <= 160 KiB)
+    static constexpr int SLOTS = TPW == 4 ? 7 : 8;
+    // The next token block's operands are prefetched into registers only at TPW = 2.
+    static constexpr bool PREFETCH = TPW == 2;
     // Rows are stored unpadded; segment s of row e sits at position s ^ swz(e), which spreads
     // the 16-byte reads of 16 consecutive rows over all 64 banks.
     static constexpr int RPL = 16 / SPR;                  // rows per 256-byte bank line
@@ -372,18 +379,18 @@ __device__ __forceinline__ int gnorm_slot(int tile, int g4) {
 struct RouteSplit {
     int32_t chunk;
     int64_t t0, t1;        // tiles of the chunk
-    int64_t blk0, blk1;    // token blocks of 512
+    int64_t blk0, blk1;    // token blocks
 };
 
 __device__ __forceinline__ RouteSplit route_split(int32_t T, int32_t M, int32_t chunks,
-                                                  int32_t splits) {
+                                                  int32_t splits, int tokens_per_block) {
     RouteSplit q;
     q.chunk = (int32_t)(blockIdx.x % (unsigned)chunks);
     const int32_t split = (int32_t)(blockIdx.x / (unsigned)chunks);
     const int64_t Mt = ((int64_t)M + 31) / 32;
     q.t0 = Mt * q.chunk / chunks;
     q.t1 = Mt * (q.chunk + 1) / chunks;
-    const int64_t ntb = ((int64_t)T + kRouteTokens - 1) / kRouteTokens;
+    const int64_t ntb = ((int64_t)T + tokens_per_block - 1) / tokens_per_block;
     q.blk0 = ntb * split / splits;
     q.blk1 = ntb * (split + 1) / splits;
     return q;
@@ -425,92 +432,144 @@ __device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ R2t,
     __syncthreads();
 }
 
-// Token ids, z_hi operands and error scales of one lane, for each of the wave's kTPW groups of
+// Token ids, z_hi operands and error scales of one lane, for each of the wave's TPW groups of
 // 32 tokens starting at `first` (written by the z pass; zeros past T).
-template <int RC>
+template <int RC, int TPW>
 struct TokenGroups {
-    int64_t tok[kTPW];
-    bool tok_ok[kTPW];
-    bf16x8 zhi[kTPW][RC];
-    float c[kTPW];
+    int64_t first;  // wave-uniform
+    int32_t T;
+    bf16x8 zhi[TPW][RC];
+    float c[TPW];
+
+    __device__ __forceinline__ int64_t tok(int g, int n) const { return first + 32 * g + n; }
+    __device__ __forceinline__ bool tok_ok(int g, int n) const { return tok(g, n) < T; }
 
     __device__ __forceinline__ void load(const uint16_t* __restrict__ zh,
-                                         const float* __restrict__ cz, int32_t T, int64_t first,
+                                         const float* __restrict__ cz, int32_t T_, int64_t first_,
                                          int n, int half) {
         constexpr int R = 16 * RC;
+        first = first_;
+        T = T_;
 #pragma unroll
-        for (int g = 0; g < kTPW; ++g) {
-            tok[g] = first + 32 * g + n;
-            tok_ok[g] = tok[g] < T;
-            const int64_t t = tok_ok[g] ? tok[g] : 0;
+        for (int g = 0; g < TPW; ++g) {
+            const bool ok = tok_ok(g, n);
+            const int64_t t = ok ? tok(g, n) : 0;
 #pragma unroll
             for (int cc = 0; cc < RC; ++cc) {
                 const bf16x8 v = load_bf16x8(zh + t * R + 16 * cc + 8 * half);
-                zhi[g][cc] = tok_ok[g] ? v : zero_bf16x8();
+                zhi[g][cc] = ok ? v : zero_bf16x8();
             }
-            c[g] = tok_ok[g] ? cz[t] : 0.0f;
+            c[g] = ok ? cz[t] : 0.0f;
         }
     }
 };
 
-// Sweeps the resident chunk for one lane's token groups: for every tile t (in order) issues
-// the MFMAs of tile t, then calls body(acc, e0, partial, u, nq) for tile t - 1 (software
-// pipeline), and finally for the last tile.  Two accumulator sets alternate by tile parity
-// (no register copies); tiles are unrolled by V = max(U, 2) so that the set and the bucket
-// index u = t mod U (passed as std::integral_constant) are compile-time constants.  acc[g] holds s for token
-// group g, e0 the first expert of the tile, nq[q] the norm bound of accumulator group q.
+// Sweeps the resident chunk for one lane's token groups and calls body(g, acc, e0, partial, u,
+// nq) once per token group g and tile: acc holds s for the group's 32 tokens and the tile's 32
+// experts starting at e0, nq[q] is the norm bound of accumulator group q, u = tile mod U the
+// bucket index (g and u are std::integral_constant).
+//
+// Schedule.  The token groups form two halves H0 = [0, TPW/2) and H1 = [TPW/2, TPW), with one
+// accumulator per group.  Per tile t the wave issues the MFMAs of H0(t), finishes H1(t - 1),
+// issues the MFMAs of H1(t) and finishes H0(t): every epilogue runs while the other half's
+// MFMAs execute, and the A operands of tile t + 1 are read from LDS while H0(t) is finished.
+// The steady-state loop runs groups of V = max(U, 2) tiles, so
+// that parity, bucket indices and partial = false are compile-time constants there and each
+// tile is one basic block.
 template <int RC, int K, typename Body>
 __device__ __forceinline__ void sweep_resident(const uint16_t* rows, const float* gn, int64_t t0,
                                                int64_t t1, int32_t M, int n, int half,
-                                               const bf16x8 (&zhi)[kTPW][RC], Body&& body) {
+                                               const bf16x8 (&zhi)[RouteCfg<RC, K>::TPW][RC],
+                                               Body&& body) {
     using C = RouteCfg<RC, K>;
+    constexpr int TPW = C::TPW, H = TPW / 2;
     constexpr int U = C::U;
     constexpr int V = U > 2 ? U : 2;
     const int nt = (int)(t1 - t0);
+    if (nt <= 0) return;
     const int32_t e00 = (int32_t)(t0 * 32);
     const int sw = C::swz(n);
     int off[RC];
 #pragma unroll
     for (int c = 0; c < RC; ++c) off[c] = n * C::R + (((2 * c + half) ^ sw) * 8);
-    f32x16 acc[2][kTPW];
+    f32x16 acc[TPW];
     f32x4 nq[2];
-    auto run = [&](auto set, int tile, auto u) __attribute__((always_inline)) {
-        const int32_t e0 = e00 + tile * 32;
-        body(acc[decltype(set)::value], e0, e0 + 32 > M, u, nq[decltype(set)::value]);
+    bf16x8 a[RC];
+    auto fetch = [&](int tile) __attribute__((always_inline)) {
+        tile = tile < nt ? tile : nt - 1;  // past the end: re-read the last tile (unused)
+        const uint16_t* base = rows + tile * 32 * C::R;
+#pragma unroll
+        for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(base + off[c]);
     };
-    for (int t = 0; t < nt; t += V) {
+    auto mfmas = [&](auto hh) __attribute__((always_inline)) {
+        constexpr int G0 = decltype(hh)::value * H;
+#pragma unroll
+        for (int g = G0; g < G0 + H; ++g) acc[g] = zero_f32x16();
+#pragma unroll
+        for (int c = 0; c < RC; ++c)
+#pragma unroll
+            for (int g = G0; g < G0 + H; ++g) acc[g] = mfma_32x32x16(a[c], zhi[g][c], acc[g]);
+    };
+    auto finish = [&](auto set, auto hh, int tile, bool partial, auto u)
+                      __attribute__((always_inline)) {
+        constexpr int P = decltype(set)::value;
+        constexpr int G0 = decltype(hh)::value * H;
+        const int32_t e0 = e00 + tile * 32;
+        unroll<H>([&](auto gg) __attribute__((always_inline)) {
+            constexpr int G = G0 + decltype(gg)::value;
+            body(std::integral_constant<int, G>{}, acc[G], e0, partial, u, nq[P]);
+        });
+    };
+    // Tile `tile` of parity P and bucket UT; the previous tile has bucket UP.
+    auto step = [&](auto set, auto ut, auto up, auto has_prev, int tile, bool partial)
+                    __attribute__((always_inline)) {
+        constexpr int P = decltype(set)::value;
+        using I0 = std::integral_constant<int, 0>;
+        using I1 = std::integral_constant<int, 1>;
+        nq[P] = *reinterpret_cast<const f32x4*>(gn + tile * 8 + 4 * half);
+        mfmas(I0{});
+        if constexpr (decltype(has_prev)::value)
+            finish(std::integral_constant<int, P ^ 1>{}, I1{}, tile - 1, false, up);
+        mfmas(I1{});
+        fetch(tile + 1);
+        finish(set, I0{}, tile, partial, ut);
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using F = std::false_type;
+    using Tr = std::true_type;
+    const int32_t elast = e00 + (nt - 1) * 32;
+    const bool plast = elast + 32 > M;
+    fetch(0);
+    step(I0{}, I0{}, I0{}, F{}, 0, nt == 1 && plast);
+    // Tiles 1 .. nt - 2 (t = 1 mod V in the loop: parity (1 + VV) & 1, buckets (1 + VV) mod U
+    // and VV mod U).
+    int t = 1;
+    for (; t + V <= nt - 1; t += V)
         unroll<V>([&](auto vv) __attribute__((always_inline)) {
             constexpr int VV = decltype(vv)::value;
-            constexpr int P = VV & 1;
-            const int tile = t + VV;
-            if (tile < nt) {
-                const uint16_t* base = rows + tile * 32 * C::R;
-                bf16x8 a[RC];
-#pragma unroll
-                for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(base + off[c]);
-                nq[P] = *reinterpret_cast<const f32x4*>(gn + tile * 8 + 4 * half);
-#pragma unroll
-                for (int g = 0; g < kTPW; ++g) acc[P][g] = zero_f32x16();
-#pragma unroll
-                for (int c = 0; c < RC; ++c)
-#pragma unroll
-                    for (int g = 0; g < kTPW; ++g)
-                        acc[P][g] = mfma_32x32x16(a[c], zhi[g][c], acc[P][g]);
-                if (tile > 0)
-                    run(std::integral_constant<int, P ^ 1>{}, tile - 1,
-                        std::integral_constant<int, (VV + V - 1) % U>{});
-            }
+            step(std::integral_constant<int, (1 + VV) & 1>{},
+                 std::integral_constant<int, (1 + VV) % U>{}, std::integral_constant<int, VV % U>{},
+                 Tr{}, t + VV, false);
         });
-    }
-    // last tile: set and bucket dispatched to compile-time values
-    if (nt > 0) {
-        unroll<V>([&](auto vv) __attribute__((always_inline)) {
-            constexpr int VV = decltype(vv)::value;
-            if ((nt - 1) % V == VV)
-                run(std::integral_constant<int, VV & 1>{}, nt - 1,
-                    std::integral_constant<int, VV % U>{});
-        });
-    }
+    unroll<V>([&](auto vv) __attribute__((always_inline)) {
+        constexpr int VV = decltype(vv)::value;
+        if (t + VV < nt - 1)
+            step(std::integral_constant<int, (1 + VV) & 1>{},
+                 std::integral_constant<int, (1 + VV) % U>{}, std::integral_constant<int, VV % U>{},
+                 Tr{}, t + VV, false);
+    });
+    // Last tile (when nt > 1), then the second half of the last tile; parity and buckets are
+    // dispatched to compile-time values.
+    unroll<V>([&](auto vv) __attribute__((always_inline)) {
+        constexpr int VV = decltype(vv)::value;
+        if ((nt - 1) % V == VV) {
+            if (nt > 1)
+                step(std::integral_constant<int, VV & 1>{}, std::integral_constant<int, VV % U>{},
+                     std::integral_constant<int, (VV + V - 1) % U>{}, Tr{}, nt - 1, plast);
+            finish(std::integral_constant<int, VV & 1>{}, std::integral_constant<int, 1>{}, nt - 1,
+                   plast, std::integral_constant<int, VV % U>{});
+        }
+    });
 }
 
 // Screening sweep.  For each accumulator group q of a tile the lane forms the lower bound
@@ -525,58 +584,64 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
     const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t chunks, int32_t splits,
     const float* __restrict__ gnorm, float* __restrict__ top) {
     using C = RouteCfg<RC, K>;
-    constexpr int U = C::U, L = C::L;
+    constexpr int L = C::L, TPW = C::TPW;
     __shared__ __attribute__((aligned(16))) uint16_t rows[C::EMAX * C::R];
     __shared__ __attribute__((aligned(16))) float gn[C::EMAX / 4];
-    const RouteSplit sp = route_split(T, M, chunks, splits);
+    const RouteSplit sp = route_split(T, M, chunks, splits, C::TOK);
     load_chunk<RC, K>(R2t, gnorm, M, sp.t0, sp.t1, rows, gn);
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 31, half = lane >> 5;
 
-    // The next block's operands are loaded while the current block is swept.
-    TokenGroups<RC> tg, nx;
-    const int64_t wofs = (int64_t)w * 32 * kTPW;
-    if (sp.blk0 < sp.blk1 && sp.blk0 * kRouteTokens + wofs < T)
-        tg.load(zh, cz, T, sp.blk0 * kRouteTokens + wofs, n, half);
+    TokenGroups<RC, TPW> tg, nx;
+    const int64_t wofs = (int64_t)w * 32 * TPW;
+    if constexpr (C::PREFETCH) {
+        if (sp.blk0 < sp.blk1 && sp.blk0 * C::TOK + wofs < T)
+            tg.load(zh, cz, T, sp.blk0 * C::TOK + wofs, n, half);
+    }
     for (int64_t blk = sp.blk0; blk < sp.blk1; ++blk) {
-        const int64_t first = blk * kRouteTokens + wofs;
+        const int64_t first = blk * C::TOK + wofs;
         if (first >= T) break;  // wave-uniform
-        const bool has_next = blk + 1 < sp.blk1 && first + kRouteTokens < T;
-        if (has_next) nx.load(zh, cz, T, first + kRouteTokens, n, half);
-        float bm[kTPW][L];
+        const bool has_next = blk + 1 < sp.blk1 && first + C::TOK < T;
+        if constexpr (C::PREFETCH) {
+            // the next block's operands are loaded while the current block is swept
+            if (has_next) nx.load(zh, cz, T, first + C::TOK, n, half);
+        } else {
+            tg.load(zh, cz, T, first, n, half);
+        }
+        float bm[TPW][L];
 #pragma unroll
-        for (int g = 0; g < kTPW; ++g)
+        for (int g = 0; g < TPW; ++g)
 #pragma unroll
             for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
-        sweep_resident<RC, K>(rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
-                              [&](f32x16 (&acc)[kTPW], int32_t e0, bool partial, auto u,
-                                  const f32x4& nq) __attribute__((always_inline)) {
-                                  constexpr int UB = 4 * decltype(u)::value;
+        sweep_resident<RC, K>(
+            rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
+            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
+                __attribute__((always_inline)) {
+                constexpr int g = decltype(gg)::value;
+                constexpr int UB = 4 * decltype(u)::value;
+                if (partial) mask_past_end(acc, e0, M, half);
 #pragma unroll
-                                  for (int g = 0; g < kTPW; ++g) {
-                                      if (partial) mask_past_end(acc[g], e0, M, half);
-#pragma unroll
-                                      for (int q = 0; q < 4; ++q)
-                                          bm[g][UB + q] = fmaxf(
-                                              bm[g][UB + q], max4(acc[g], q) - tg.c[g] * nq[q]);
-                                  }
-                              });
+                for (int q = 0; q < 4; ++q)
+                    bm[g][UB + q] = fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
+            });
         // K largest of each token's 2L bucket maxima.
 #pragma unroll
-        for (int g = 0; g < kTPW; ++g) {
+        for (int g = 0; g < TPW; ++g) {
             sort_desc<L>(bm[g]);
             float pb[L];
 #pragma unroll
             for (int b = 0; b < L; ++b) pb[b] = __shfl_xor(bm[g][b], 32, kWave);
             vlist_merge<L>(bm[g], pb);
-            if (half == 0 && tg.tok_ok[g]) {
-                float* o = top + ((int64_t)sp.chunk * T + tg.tok[g]) * K;
+            if (half == 0 && tg.tok_ok(g, n)) {
+                float* o = top + ((int64_t)sp.chunk * T + tg.tok(g, n)) * K;
 #pragma unroll
                 for (int j = 0; j < K; ++j) o[j] = bm[g][j];
             }
         }
-        if (has_next) tg = nx;
+        if constexpr (C::PREFETCH) {
+            if (has_next) tg = nx;
+        }
     }
 }
 
@@ -646,10 +711,10 @@ __global__ __launch_bounds__(256) void theta_kernel(const float* __restrict__ to
 
 // Collect sweep: recomputes s for the chunk and appends every expert with s_e + c N_g >=
 // theta[token] to the token's candidate list cand[token][0..cap-1] (order of arrival,
-// count[token] entries).  A lane buffers its hits in kLaneSlots LDS slots per token group
-// (16-bit offsets in the chunk); the token's two lanes reserve their list space with one
-// atomic add at the end of the token block.  A lane with more hits marks the token as
-// overflowed (count > cap), which sends it to the exact sweep of the finalize kernel.
+// count[token] entries).  A lane buffers its hits in SLOTS LDS slots per token group (16-bit
+// offsets in the chunk); the token's two lanes reserve their list space with one atomic add
+// at the end of the token block.  A lane with more hits marks the token as overflowed (count
+// > cap), which sends it to the exact sweep of the finalize kernel.
 template <int RC, int K>
 __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
     const uint16_t* __restrict__ zh, const float* __restrict__ cz,
@@ -657,10 +722,11 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
     const float* __restrict__ theta, const float* __restrict__ gnorm,
     int32_t* __restrict__ count, int32_t* __restrict__ cand, int32_t cap) {
     using C = RouteCfg<RC, K>;
+    constexpr int TPW = C::TPW, S = C::SLOTS;
     __shared__ __attribute__((aligned(16))) uint16_t rows[C::EMAX * C::R];
     __shared__ __attribute__((aligned(16))) float gn[C::EMAX / 4];
-    __shared__ uint16_t slots[kLaneSlots][kTPW][kRouteThreads];
-    const RouteSplit sp = route_split(T, M, chunks, splits);
+    __shared__ uint16_t slots[S][TPW][kRouteThreads];
+    const RouteSplit sp = route_split(T, M, chunks, splits, C::TOK);
     load_chunk<RC, K>(R2t, gnorm, M, sp.t0, sp.t1, rows, gn);
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -668,62 +734,66 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
     const int n = lane & 31, half = lane >> 5;
     const int32_t ebase = (int32_t)(sp.t0 * 32);
 
-    // The next block's operands and thresholds are loaded while the current block is swept.
-    TokenGroups<RC> tg, nx;
-    float th[kTPW], nth[kTPW];
-    auto load_theta = [&](const TokenGroups<RC>& q, float (&o)[kTPW])
+    TokenGroups<RC, TPW> tg, nx;
+    float th[TPW], nth[TPW];
+    auto load_theta = [&](const TokenGroups<RC, TPW>& q, float (&o)[TPW])
                           __attribute__((always_inline)) {
 #pragma unroll
-        for (int g = 0; g < kTPW; ++g)  // lanes past T never qualify (+inf threshold)
-            o[g] = q.tok_ok[g] ? theta[q.tok[g]] : __builtin_huge_valf();
+        for (int g = 0; g < TPW; ++g)  // lanes past T never qualify (+inf threshold)
+            o[g] = q.tok_ok(g, n) ? theta[q.tok(g, n)] : __builtin_huge_valf();
     };
-    const int64_t wofs = (int64_t)w * 32 * kTPW;
-    if (sp.blk0 < sp.blk1 && sp.blk0 * kRouteTokens + wofs < T) {
-        tg.load(zh, cz, T, sp.blk0 * kRouteTokens + wofs, n, half);
-        load_theta(tg, th);
+    const int64_t wofs = (int64_t)w * 32 * TPW;
+    if constexpr (C::PREFETCH) {
+        if (sp.blk0 < sp.blk1 && sp.blk0 * C::TOK + wofs < T) {
+            tg.load(zh, cz, T, sp.blk0 * C::TOK + wofs, n, half);
+            load_theta(tg, th);
+        }
     }
     for (int64_t blk = sp.blk0; blk < sp.blk1; ++blk) {
-        const int64_t first = blk * kRouteTokens + wofs;
+        const int64_t first = blk * C::TOK + wofs;
         if (first >= T) break;  // wave-uniform
-        const bool has_next = blk + 1 < sp.blk1 && first + kRouteTokens < T;
-        if (has_next) {
-            nx.load(zh, cz, T, first + kRouteTokens, n, half);
-            load_theta(nx, nth);
+        const bool has_next = blk + 1 < sp.blk1 && first + C::TOK < T;
+        if constexpr (C::PREFETCH) {
+            // the next block's operands and thresholds are loaded while this block is swept
+            if (has_next) {
+                nx.load(zh, cz, T, first + C::TOK, n, half);
+                load_theta(nx, nth);
+            }
+        } else {
+            tg.load(zh, cz, T, first, n, half);
+            load_theta(tg, th);
         }
-        int cnt[kTPW];
+        int cnt[TPW];
 #pragma unroll
-        for (int g = 0; g < kTPW; ++g) cnt[g] = 0;
+        for (int g = 0; g < TPW; ++g) cnt[g] = 0;
         sweep_resident<RC, K>(
             rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
-            [&](f32x16 (&acc)[kTPW], int32_t e0, bool partial, auto u, const f32x4& nq)
+            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
+                constexpr int g = decltype(gg)::value;
                 (void)u;
-                // Tile test with the lane's largest group norm (a looser bound, one compare
-                // per token group); the exact per-group tests run only when it passes.
+                if (partial) mask_past_end(acc, e0, M, half);
+                // Tile test with the lane's largest group norm (a looser bound, one compare);
+                // the exact per-group tests run only when it passes.
                 const float nmax = fmaxf(fmaxf(nq[0], nq[1]), fmaxf(nq[2], nq[3]));
+                const float m16 = fmaxf(fmaxf(fmaxf(max4(acc, 0), max4(acc, 1)), max4(acc, 2)),
+                                        max4(acc, 3));
+                if (m16 >= th[g] - tg.c[g] * nmax) {
+                    float tq[4], gm[4];
 #pragma unroll
-                for (int g = 0; g < kTPW; ++g) {
-                    if (partial) mask_past_end(acc[g], e0, M, half);
-                    const float m16 = fmaxf(fmaxf(fmaxf(max4(acc[g], 0), max4(acc[g], 1)),
-                                                  max4(acc[g], 2)),
-                                            max4(acc[g], 3));
-                    if (m16 >= th[g] - tg.c[g] * nmax) {
-                        float tq[4], gm[4];
+                    for (int q = 0; q < 4; ++q) {
+                        tq[q] = th[g] - tg.c[g] * nq[q];
+                        gm[q] = max4(acc, q) - tq[q];
+                    }
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            tq[q] = th[g] - tg.c[g] * nq[q];
-                            gm[q] = max4(acc[g], q) - tq[q];
-                        }
+                    for (int q = 0; q < 4; ++q) {
+                        if (gm[q] >= 0.0f) {
 #pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            if (gm[q] >= 0.0f) {
-#pragma unroll
-                                for (int i = 0; i < 4; ++i) {
-                                    if (acc[g][4 * q + i] >= tq[q]) {
-                                        slots[cnt[g] < kLaneSlots ? cnt[g] : kLaneSlots - 1][g][tid] =
-                                            (uint16_t)(e0 - ebase + acc_row(4 * q + i, half));
-                                        ++cnt[g];
-                                    }
+                            for (int i = 0; i < 4; ++i) {
+                                if (acc[4 * q + i] >= tq[q]) {
+                                    slots[cnt[g] < S ? cnt[g] : S - 1][g][tid] =
+                                        (uint16_t)(e0 - ebase + acc_row(4 * q + i, half));
+                                    ++cnt[g];
                                 }
                             }
                         }
@@ -731,25 +801,28 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
                 }
             });
 #pragma unroll
-        for (int g = 0; g < kTPW; ++g) {
+        for (int g = 0; g < TPW; ++g) {
             const int pc = __shfl_xor(cnt[g], 32, kWave);
-            const bool over = cnt[g] > kLaneSlots || pc > kLaneSlots;
+            const bool over = cnt[g] > S || pc > S;
             const int total = cnt[g] + pc;
             int base = 0;
-            if (half == 0 && tg.tok_ok[g] && total > 0)
-                base = atomicAdd(&count[tg.tok[g]], over ? cap + 1 : total);
+            const int64_t tk = tg.tok(g, n);
+            if (half == 0 && tk < T && total > 0)
+                base = atomicAdd(&count[tk], over ? cap + 1 : total);
             base = __shfl(base, n, kWave);  // lane half 1 reads its partner's reservation
-            if (tg.tok_ok[g] && !over) {
+            if (tk < T && !over) {
                 const int off = base + (half ? pc : 0);
                 for (int i = 0; i < cnt[g]; ++i)
                     if (off + i < cap)
-                        cand[tg.tok[g] * cap + off + i] = ebase + (int32_t)slots[i][g][tid];
+                        cand[tk * cap + off + i] = ebase + (int32_t)slots[i][g][tid];
             }
         }
-        if (has_next) {
-            tg = nx;
+        if constexpr (C::PREFETCH) {
+            if (has_next) {
+                tg = nx;
 #pragma unroll
-            for (int g = 0; g < kTPW; ++g) th[g] = nth[g];
+                for (int g = 0; g < TPW; ++g) th[g] = nth[g];
+            }
         }
     }
 }
@@ -877,7 +950,8 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     q.RC = r / 16;
     q.RT = (q.RC + 1) / 2;
     q.K = pow2_at_least(k);
-    q.ntb = (int32_t)((T + kRouteTokens - 1) / kRouteTokens);
+    const int tokens_per_block = 32 * route_tpw(q.RC, q.K) * kRouteWaves;
+    q.ntb = (int32_t)((T + tokens_per_block - 1) / tokens_per_block);
     const int64_t Mt = ((int64_t)M + 31) / 32;
     const int64_t emax_tiles = (int64_t)kChunkBytes / (2 * r) / 32;
     if (m_chunks > 0) {
