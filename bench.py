@@ -43,11 +43,13 @@ def algorithmic(w):
     return nbytes, flops
 
 
-SCOPE = ("one routing call: the z pass, screen, threshold, collect and finalize kernels "
-         "(+ histogram), timed together as one step")
+SCOPE_RESIDENT = ("one routing call: the z pass, screen, threshold, collect and finalize "
+                  "kernels (+ histogram), timed together as one step")
+SCOPE_FUSED = ("one routing call: the z pass and the fused route kernel (screen, threshold, "
+               "collect and finalize in one launch) (+ histogram), timed together as one step")
 
 
-def roofline(w, seconds):
+def roofline(w, seconds, scope):
     """Position of one routing call against max(flops / MFMA peak, bytes / HBM peak)."""
     nbytes, flops = algorithmic(w)
     t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
@@ -56,11 +58,11 @@ def roofline(w, seconds):
         achieved = nbytes / seconds / 1e9
         return {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
-                "kernel": SCOPE, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+                "kernel": scope, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
     achieved = flops / seconds / 1e12
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-            "kernel": SCOPE, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+            "kernel": scope, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
 
 
 def timed(fn, steps, warmup, stream):
@@ -172,6 +174,7 @@ def main():
 
     sec = timed_graph(step, args.steps, args.warmup)
     plan_chunks = router.lowrank_plan(w.T, w.h, w.r, w.M, w.k)
+    route = "fused" if plan_chunks == 0 else "expert-resident"
 
     result = {
         "metric": METRIC,
@@ -187,9 +190,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "T": w.T, "h": w.h, "r": w.r, "M": w.M, "k": w.k,
-                   "histogram": w.histogram, "expert_chunks": plan_chunks,
+                   "histogram": w.histogram, "route": route, "expert_chunks": plan_chunks,
                    "rotating_batches": nbuf, "launch": "hip graph of the timed steps"},
-        "roofline": roofline(w, sec),
+        "roofline": roofline(w, sec, SCOPE_FUSED if route == "fused" else SCOPE_RESIDENT),
     }
 
     if not args.no_fullrank:

@@ -12,8 +12,10 @@ struct LowrankPlan {
     int32_t RC;               // rank chunks of 16 (r = 16 RC)
     int32_t RT;               // 32-row tiles of the rank axis in the z pass
     int32_t K;                // top-K list length (power of two >= k)
-    int32_t ntb;              // token blocks of 512 tokens
+    int32_t fused;            // 1: one fused route kernel per 64 tokens (small expert sets)
+    int32_t ntb;              // token blocks of the route kernels
     int32_t chunks;           // expert-axis chunks, each resident in one workgroup's LDS
+                              // (1 for the fused route)
     int32_t splits;           // token-block ranges per chunk (route grid = chunks * splits)
     int32_t cap;              // candidate slots per token
     int32_t theta_group;      // threads per token in the threshold kernel

@@ -57,8 +57,11 @@ constexpr int kZWaves = 4;
 constexpr int kZTokens = 32 * kZWaves;
 constexpr int kZChunk = 64;
 
-// Group norms: gnorm[g] = (largest Euclidean norm among expert rows 4g..4g+3 of R2t) rounded
-// up, for every group of the rows < `rows` (all tiles); rows past M count as zero.  Lane (row, 16-byte segment) layout: the
+// Group norms: the largest Euclidean norm among expert rows 4g..4g+3 of R2t, rounded up, for
+// every group of the rows < `rows` (all tiles); rows past M count as zero.  Within each tile of
+// 32 rows the 8 groups are stored in the order [half][q] (group 2q + half at 4 half + q), so
+// that MFMA lane half `half` reads the norms of its four accumulator groups q with one 16-byte
+// load.  Lane (row, 16-byte segment) layout: the
 // r/8 segments of a row sit in consecutive lanes and the 4 rows of a group next to each other.
 template <int SPR>
 __device__ __forceinline__ void group_norms(const uint16_t* __restrict__ R2t, int32_t M,
@@ -76,7 +79,11 @@ __device__ __forceinline__ void group_norms(const uint16_t* __restrict__ R2t, in
     for (int m = 1; m < SPR; m <<= 1) ss += __shfl_xor(ss, m, kWave);
     ss = fmaxf(ss, __shfl_xor(ss, SPR, kWave));
     ss = fmaxf(ss, __shfl_xor(ss, 2 * SPR, kWave));
-    if (col == 0 && (row & 3) == 0 && row < rows) gnorm[row / 4] = sqrtf(ss) * (1.0f + 0x1p-20f);
+    if (col == 0 && (row & 3) == 0 && row < rows) {
+        // slot of group g4 = (row mod 32) / 4 = 2q + half of tile row / 32: [tile][half][q]
+        const int g4 = (int)(row & 31) >> 2;
+        gnorm[(row >> 5) * 8 + (g4 & 1) * 4 + (g4 >> 1)] = sqrtf(ss) * (1.0f + 0x1p-20f);
+    }
 }
 
 template <int RT, int D>
@@ -369,12 +376,6 @@ __device__ __forceinline__ void mask_past_end(f32x16& acc, int32_t e0, int32_t M
         if (e0 + acc_row(j, half) >= M) acc[j] = -__builtin_huge_valf();
 }
 
-// LDS position of group g4 = (row mod 32) / 4 = 2q + half of a tile: [tile][half][q], so that a
-// lane reads the norms of its four accumulator groups with one 16-byte load.
-__device__ __forceinline__ int gnorm_slot(int tile, int g4) {
-    return tile * 8 + (g4 & 1) * 4 + (g4 >> 1);
-}
-
 // Work split of a route launch: workgroup -> (expert chunk, range of token blocks).
 struct RouteSplit {
     int32_t chunk;
@@ -428,7 +429,7 @@ __device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ R2t,
         }
     }
     const int ngr = (int)(t1 - t0) * 8;
-    for (int g = tid; g < ngr; g += kRouteThreads) gn[gnorm_slot(g / 8, g % 8)] = gnorm[t0 * 8 + g];
+    for (int g = tid; g < ngr; g += kRouteThreads) gn[g] = gnorm[t0 * 8 + g];
     __syncthreads();
 }
 
@@ -464,110 +465,150 @@ struct TokenGroups {
     }
 };
 
-// Sweeps the resident chunk for one lane's token groups and calls body(g, acc, e0, partial, u,
-// nq) once per token group g and tile: acc holds s for the group's 32 tokens and the tile's 32
-// experts starting at e0, nq[q] is the norm bound of accumulator group q, u = tile mod U the
-// bucket index (g and u are std::integral_constant).
+// Operand sources of a sweep: the A operands (expert rows 32 t + n, rank entries 16 c + 8 half
+// + 0..7 for c < RC) and the norm bounds of lane half `half` for tile t of the sweep.
+//
+// LdsRows: a chunk resident in LDS (rows stored with the XOR swizzle of RouteCfg).
+template <int RC, int K>
+struct LdsRows {
+    const uint16_t* rows;
+    const float* gn;
+    int off[RC];
+    int half;
+    __device__ __forceinline__ LdsRows(const uint16_t* rows_, const float* gn_, int n, int half_)
+        : rows(rows_), gn(gn_), half(half_) {
+        using C = RouteCfg<RC, K>;
+        const int sw = C::swz(n);
+#pragma unroll
+        for (int c = 0; c < RC; ++c) off[c] = n * C::R + (((2 * c + half) ^ sw) * 8);
+    }
+    __device__ __forceinline__ void load_a(int tile, bf16x8 (&a)[RC]) const {
+        const uint16_t* base = rows + tile * 32 * RouteCfg<RC, K>::R;
+#pragma unroll
+        for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(base + off[c]);
+    }
+    __device__ __forceinline__ f32x4 load_nq(int tile) const {
+        return *reinterpret_cast<const f32x4*>(gn + tile * 8 + 4 * half);
+    }
+};
+
+// GlobalRows: rows read straight from R2t (L2-resident when the expert set is small), norms
+// from a copy of the group norms in LDS; tiles are counted from global tile tile0, rows past M
+// re-read row M - 1 (masked by the caller).
+template <int RC>
+struct GlobalRows {
+    const uint16_t* row;   // R2t + (32 tile0 + n) * R + 8 half
+    const float* gn;       // LDS group norms + 8 tile0 + 4 half
+    int32_t rmax;          // rows past this one (M - 1 - 32 tile0 - n) are clamped
+    __device__ __forceinline__ GlobalRows(const uint16_t* R2t, const float* gn_lds, int32_t M,
+                                          int64_t tile0, int n, int half)
+        : row(R2t + (tile0 * 32 + n) * (16 * RC) + 8 * half),
+          gn(gn_lds + tile0 * 8 + 4 * half),
+          rmax((int32_t)(M - 1 - tile0 * 32 - n)) {}
+    __device__ __forceinline__ void load_a(int tile, bf16x8 (&a)[RC]) const {
+        int rr = tile * 32;
+        rr = rr < rmax ? rr : rmax;
+        const uint16_t* p = row + (int64_t)rr * (16 * RC);
+#pragma unroll
+        for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(p + 16 * c);
+    }
+    __device__ __forceinline__ f32x4 load_nq(int tile) const {
+        return *reinterpret_cast<const f32x4*>(gn + tile * 8);
+    }
+};
+
+// Sweeps nt tiles (experts e00 .. e00 + 32 nt - 1) for one lane's token groups and calls
+// body(g, acc, e0, partial, u, nq) once per token group g and tile: acc holds s for the group's
+// 32 tokens and the tile's 32 experts starting at e0, nq[q] is the norm bound of accumulator
+// group q, u = tile mod U the bucket index (g and u are std::integral_constant).
 //
 // Schedule.  The token groups form two halves H0 = [0, TPW/2) and H1 = [TPW/2, TPW), with one
 // accumulator per group.  Per tile t the wave issues the MFMAs of H0(t), finishes H1(t - 1),
 // issues the MFMAs of H1(t) and finishes H0(t): every epilogue runs while the other half's
-// MFMAs execute, and the A operands of tile t + 1 are read from LDS while H0(t) is finished.
-// The steady-state loop runs groups of V = max(U, 2) tiles, so
-// that parity, bucket indices and partial = false are compile-time constants there and each
-// tile is one basic block.
-template <int RC, int K, typename Body>
-__device__ __forceinline__ void sweep_resident(const uint16_t* rows, const float* gn, int64_t t0,
-                                               int64_t t1, int32_t M, int n, int half,
-                                               const bf16x8 (&zhi)[RouteCfg<RC, K>::TPW][RC],
-                                               Body&& body) {
+// MFMAs execute.  The A operands and norms of the next D tiles are held in a register ring (the
+// refill of a slot is issued once its last reader has been issued).  The steady-state loop runs
+// groups of V = max(U, D, 2) tiles, so that ring slots, bucket indices and partial = false are
+// compile-time constants there and each tile is one basic block.
+template <int RC, int K, int TPW, int D, typename Src, typename Body>
+__device__ __forceinline__ void sweep(const Src& src, int nt, int32_t e00, int32_t M, int half,
+                                      const bf16x8 (&zhi)[TPW][RC], Body&& body) {
     using C = RouteCfg<RC, K>;
-    constexpr int TPW = C::TPW, H = TPW / 2;
+    constexpr int H = TPW / 2;
     constexpr int U = C::U;
-    constexpr int V = U > 2 ? U : 2;
-    const int nt = (int)(t1 - t0);
+    constexpr int ND = 2;  // norm slots (norms come from LDS; a slot lives for two steps)
+    constexpr int V = U > D ? (U > ND ? U : ND) : (D > ND ? D : ND);
     if (nt <= 0) return;
-    const int32_t e00 = (int32_t)(t0 * 32);
-    const int sw = C::swz(n);
-    int off[RC];
-#pragma unroll
-    for (int c = 0; c < RC; ++c) off[c] = n * C::R + (((2 * c + half) ^ sw) * 8);
     f32x16 acc[TPW];
-    f32x4 nq[2];
-    bf16x8 a[RC];
-    auto fetch = [&](int tile) __attribute__((always_inline)) {
-        tile = tile < nt ? tile : nt - 1;  // past the end: re-read the last tile (unused)
-        const uint16_t* base = rows + tile * 32 * C::R;
-#pragma unroll
-        for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(base + off[c]);
+    f32x4 nq[ND];
+    bf16x8 a[D][RC];
+    auto fetch = [&](auto slot, int tile) __attribute__((always_inline)) {
+        src.load_a(tile < nt ? tile : nt - 1, a[decltype(slot)::value]);  // past the end: unused
     };
-    auto mfmas = [&](auto hh) __attribute__((always_inline)) {
+    auto fetch_nq = [&](auto slot, int tile) __attribute__((always_inline)) {
+        nq[decltype(slot)::value] = src.load_nq(tile < nt ? tile : nt - 1);
+    };
+    auto mfmas = [&](auto slot, auto hh) __attribute__((always_inline)) {
+        constexpr int A = decltype(slot)::value;
         constexpr int G0 = decltype(hh)::value * H;
 #pragma unroll
         for (int g = G0; g < G0 + H; ++g) acc[g] = zero_f32x16();
 #pragma unroll
         for (int c = 0; c < RC; ++c)
 #pragma unroll
-            for (int g = G0; g < G0 + H; ++g) acc[g] = mfma_32x32x16(a[c], zhi[g][c], acc[g]);
+            for (int g = G0; g < G0 + H; ++g) acc[g] = mfma_32x32x16(a[A][c], zhi[g][c], acc[g]);
     };
-    auto finish = [&](auto set, auto hh, int tile, bool partial, auto u)
+    auto finish = [&](auto nslot, auto hh, int tile, bool partial, auto u)
                       __attribute__((always_inline)) {
-        constexpr int P = decltype(set)::value;
+        constexpr int NS = decltype(nslot)::value;
         constexpr int G0 = decltype(hh)::value * H;
         const int32_t e0 = e00 + tile * 32;
         unroll<H>([&](auto gg) __attribute__((always_inline)) {
             constexpr int G = G0 + decltype(gg)::value;
-            body(std::integral_constant<int, G>{}, acc[G], e0, partial, u, nq[P]);
+            body(std::integral_constant<int, G>{}, acc[G], e0, partial, u, nq[NS]);
         });
     };
-    // Tile `tile` of parity P and bucket UT; the previous tile has bucket UP.
-    auto step = [&](auto set, auto ut, auto up, auto has_prev, int tile, bool partial)
-                    __attribute__((always_inline)) {
-        constexpr int P = decltype(set)::value;
-        using I0 = std::integral_constant<int, 0>;
-        using I1 = std::integral_constant<int, 1>;
-        nq[P] = *reinterpret_cast<const f32x4*>(gn + tile * 8 + 4 * half);
-        mfmas(I0{});
-        if constexpr (decltype(has_prev)::value)
-            finish(std::integral_constant<int, P ^ 1>{}, I1{}, tile - 1, false, up);
-        mfmas(I1{});
-        fetch(tile + 1);
-        finish(set, I0{}, tile, partial, ut);
-    };
     using I0 = std::integral_constant<int, 0>;
-    using F = std::false_type;
-    using Tr = std::true_type;
-    const int32_t elast = e00 + (nt - 1) * 32;
-    const bool plast = elast + 32 > M;
-    fetch(0);
-    step(I0{}, I0{}, I0{}, F{}, 0, nt == 1 && plast);
-    // Tiles 1 .. nt - 2 (t = 1 mod V in the loop: parity (1 + VV) & 1, buckets (1 + VV) mod U
-    // and VV mod U).
+    using I1 = std::integral_constant<int, 1>;
+    // Tile `tile` = j (mod V) with j = J: A slot j mod D, norm slot j mod ND, bucket j mod U.
+    auto step = [&](auto jj, auto has_prev, int tile, bool partial)
+                    __attribute__((always_inline)) {
+        constexpr int J = decltype(jj)::value;
+        using SA = std::integral_constant<int, J % D>;
+        using SN = std::integral_constant<int, J % ND>;
+        using SP = std::integral_constant<int, (J + ND - 1) % ND>;
+        mfmas(SA{}, I0{});
+        if constexpr (decltype(has_prev)::value) {
+            finish(SP{}, I1{}, tile - 1, false, std::integral_constant<int, (J + V - 1) % U>{});
+            fetch_nq(SP{}, tile - 1 + ND);
+        }
+        mfmas(SA{}, I1{});
+        fetch(SA{}, tile + D);
+        finish(SN{}, I0{}, tile, partial, std::integral_constant<int, J % U>{});
+    };
+    const bool plast = e00 + nt * 32 > M;
+    unroll<D>([&](auto s) __attribute__((always_inline)) { fetch(s, decltype(s)::value); });
+    unroll<ND>([&](auto s) __attribute__((always_inline)) { fetch_nq(s, decltype(s)::value); });
+    step(I0{}, std::false_type{}, 0, nt == 1 && plast);
+    // Tiles 1 .. nt - 2 (t = 1 mod V in the loop, so tile t + VV has residue 1 + VV).
     int t = 1;
     for (; t + V <= nt - 1; t += V)
         unroll<V>([&](auto vv) __attribute__((always_inline)) {
-            constexpr int VV = decltype(vv)::value;
-            step(std::integral_constant<int, (1 + VV) & 1>{},
-                 std::integral_constant<int, (1 + VV) % U>{}, std::integral_constant<int, VV % U>{},
-                 Tr{}, t + VV, false);
+            step(std::integral_constant<int, (1 + decltype(vv)::value) % V>{}, std::true_type{},
+                 t + decltype(vv)::value, false);
         });
     unroll<V>([&](auto vv) __attribute__((always_inline)) {
-        constexpr int VV = decltype(vv)::value;
-        if (t + VV < nt - 1)
-            step(std::integral_constant<int, (1 + VV) & 1>{},
-                 std::integral_constant<int, (1 + VV) % U>{}, std::integral_constant<int, VV % U>{},
-                 Tr{}, t + VV, false);
+        if (t + decltype(vv)::value < nt - 1)
+            step(std::integral_constant<int, (1 + decltype(vv)::value) % V>{}, std::true_type{},
+                 t + decltype(vv)::value, false);
     });
-    // Last tile (when nt > 1), then the second half of the last tile; parity and buckets are
-    // dispatched to compile-time values.
+    // Last tile (when nt > 1), then the second half of the last tile; residues dispatched to
+    // compile-time values.
     unroll<V>([&](auto vv) __attribute__((always_inline)) {
-        constexpr int VV = decltype(vv)::value;
-        if ((nt - 1) % V == VV) {
-            if (nt > 1)
-                step(std::integral_constant<int, VV & 1>{}, std::integral_constant<int, VV % U>{},
-                     std::integral_constant<int, (VV + V - 1) % U>{}, Tr{}, nt - 1, plast);
-            finish(std::integral_constant<int, VV & 1>{}, std::integral_constant<int, 1>{}, nt - 1,
-                   plast, std::integral_constant<int, VV % U>{});
+        constexpr int J = decltype(vv)::value;
+        if ((nt - 1) % V == J) {
+            if (nt > 1) step(vv, std::true_type{}, nt - 1, plast);
+            finish(std::integral_constant<int, J % ND>{}, I1{}, nt - 1, plast,
+                   std::integral_constant<int, J % U>{});
         }
     });
 }
@@ -592,6 +633,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 31, half = lane >> 5;
+    const LdsRows<RC, K> src(rows, gn, n, half);
 
     TokenGroups<RC, TPW> tg, nx;
     const int64_t wofs = (int64_t)w * 32 * TPW;
@@ -614,8 +656,8 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
         for (int g = 0; g < TPW; ++g)
 #pragma unroll
             for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
-        sweep_resident<RC, K>(
-            rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
+        sweep<RC, K, TPW, 1>(
+            src, (int)(sp.t1 - sp.t0), (int32_t)(sp.t0 * 32), M, half, tg.zhi,
             [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
                 constexpr int g = decltype(gg)::value;
@@ -733,6 +775,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, half = lane >> 5;
     const int32_t ebase = (int32_t)(sp.t0 * 32);
+    const LdsRows<RC, K> src(rows, gn, n, half);
 
     TokenGroups<RC, TPW> tg, nx;
     float th[TPW], nth[TPW];
@@ -766,8 +809,8 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
         int cnt[TPW];
 #pragma unroll
         for (int g = 0; g < TPW; ++g) cnt[g] = 0;
-        sweep_resident<RC, K>(
-            rows, gn, sp.t0, sp.t1, M, n, half, tg.zhi,
+        sweep<RC, K, TPW, 1>(
+            src, (int)(sp.t1 - sp.t0), (int32_t)(sp.t0 * 32), M, half, tg.zhi,
             [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
                 constexpr int g = decltype(gg)::value;
@@ -842,69 +885,85 @@ __device__ __forceinline__ float exact_logit(const ZRow& zr, const uint16_t* __r
     return acc;
 }
 
-// Final selection: 8 lanes per token evaluate the token's candidates exactly, keep a top-K
-// list each and merge; lane 0 of the group writes the softmax over the best k.  Tokens whose
-// candidate list overflowed are recomputed by the whole workgroup with an exact sweep over
-// all M experts.
-template <int RC, int K>
-__global__ __launch_bounds__(256) void finalize_kernel(
-    const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
-    int32_t k, const int32_t* __restrict__ count, const int32_t* __restrict__ cand, int32_t cap,
-    int32_t* __restrict__ idx, float* __restrict__ gate, float* __restrict__ topval) {
+// Final selection for the NTOK = NTHREADS / 8 tokens tok0 .. tok0 + NTOK - 1 of a workgroup: 8
+// lanes per token evaluate the token's candidates exactly, keep a top-K list each and merge;
+// lane 0 of the group writes the softmax over the best k.  count_of(j) is the number of
+// candidates of local token j and cand_of(j, i) its i-th candidate.  Tokens whose candidate list
+// overflowed (count > cap) are recomputed by the whole workgroup with an exact sweep over all M
+// experts.  Must be reached by every thread of the workgroup.
+template <int RC, int K, int NTHREADS, typename CountOf, typename CandOf>
+__device__ __forceinline__ void finalize_tokens(const float* __restrict__ z,
+                                                const uint16_t* __restrict__ R2t, int32_t T,
+                                                int32_t M, int32_t k, int64_t tok0, int32_t cap,
+                                                CountOf&& count_of, CandOf&& cand_of,
+                                                int32_t* __restrict__ idx,
+                                                float* __restrict__ gate,
+                                                float* __restrict__ topval) {
     constexpr int R = 16 * RC;
-    __shared__ int32_t over_flag[32];
-    __shared__ float wv[4][K];
-    __shared__ int32_t wi[4][K];
+    constexpr int NTOK = NTHREADS / 8, NW = NTHREADS / 64;
+    __shared__ int32_t over_flag[NTOK];
+    __shared__ float wv[NW][K];
+    __shared__ int32_t wi[NW][K];
     const int tid = threadIdx.x;
     const int sub = tid & 7;
-    const int64_t tok = (int64_t)blockIdx.x * 32 + (tid >> 3);
+    const int j = tid >> 3;
+    const int64_t tok = tok0 + j;
     const bool ok = tok < T;
-    const int32_t n = ok ? count[tok] : 0;
+    const int32_t n = ok ? count_of(j) : 0;
     // n >= k always holds (k experts reach theta); the test is a guard, not a path.
     const bool exact_sweep = ok && (n > cap || n < k);
-    if (sub == 0) over_flag[tid >> 3] = exact_sweep;
+    if (sub == 0) over_flag[j] = exact_sweep;
     float v[K];
     int32_t ix[K];
     list_init<K>(v, ix);
     if (!exact_sweep && n > sub) {
         const float* zp = z + (ok ? tok : 0) * R;
-        auto eval = [&](auto zr) __attribute__((always_inline)) {
-            // candidates sub, sub + 8, ...: two per round so that their loads overlap
-            for (int i = sub; i < n; i += 16) {
-                const bool two = i + 8 < n;
-                const int32_t e0 = cand[tok * cap + i];
-                const int32_t e1 = two ? cand[tok * cap + i + 8] : e0;
-                const float l0 = exact_logit<RC>(zr, R2t + (int64_t)e0 * R);
-                const float l1 = exact_logit<RC>(zr, R2t + (int64_t)e1 * R);
-                if (better(l0, e0, v[K - 1], ix[K - 1])) list_insert<K>(v, ix, l0, e0);
-                if (two && better(l1, e1, v[K - 1], ix[K - 1])) list_insert<K>(v, ix, l1, e1);
-            }
-        };
-        if constexpr (RC <= 4) {
-            float zreg[R];
+        float zreg[R];
 #pragma unroll
-            for (int i = 0; i < R; i += 4) {
-                const f32x4 q = *reinterpret_cast<const f32x4*>(zp + i);
+        for (int i = 0; i < R; i += 4) {
+            const f32x4 q = *reinterpret_cast<const f32x4*>(zp + i);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) zreg[i + j] = q[j];
+            for (int jj = 0; jj < 4; ++jj) zreg[i + jj] = q[jj];
+        }
+        // Candidates sub, sub + 8, ...: FB per round, all their rows loaded before any is used.
+        constexpr int FB = RC <= 2 ? 4 : 2;
+        for (int i0 = sub; i0 < n; i0 += 8 * FB) {
+            int32_t e[FB];
+            bf16x8 u[FB][2 * RC];
+#pragma unroll
+            for (int b = 0; b < FB; ++b) {
+                const int i = i0 + 8 * b;
+                e[b] = cand_of(j, i < n ? i : i0);
             }
-            eval([&](int i) __attribute__((always_inline)) { return zreg[i]; });
-        } else {
-            eval([&](int i) __attribute__((always_inline)) { return zp[i]; });
+#pragma unroll
+            for (int b = 0; b < FB; ++b)
+#pragma unroll
+                for (int c = 0; c < 2 * RC; ++c) u[b][c] = load_bf16x8(R2t + (int64_t)e[b] * R + 8 * c);
+#pragma unroll
+            for (int b = 0; b < FB; ++b) {
+                // z . u_e in fp32, rank entries in increasing order (as exact_logit)
+                float l = 0.0f;
+#pragma unroll
+                for (int c = 0; c < 2 * RC; ++c)
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) l = fmaf(zreg[8 * c + q], (float)u[b][c][q], l);
+                if (i0 + 8 * b < n && better(l, e[b], v[K - 1], ix[K - 1]))
+                    list_insert<K>(v, ix, l, e[b]);
+            }
         }
     }
 #pragma unroll
     for (int s = 1; s < 8; s <<= 1) list_merge_xor<K>(v, ix, s);
     if (ok && sub == 0 && !exact_sweep) store_selection<K>(v, ix, k, tok, idx, gate, topval);
-    __syncthreads();
     // Overflowed tokens (rare): the whole workgroup sweeps all experts, thread tid taking
-    // experts tid, tid + 256, ...
-    for (int j = 0; j < 32; ++j) {
-        if (!over_flag[j]) continue;  // workgroup-uniform
-        const int64_t t = (int64_t)blockIdx.x * 32 + j;
+    // experts tid, tid + NTHREADS, ...
+    if (!__syncthreads_or(exact_sweep)) return;  // workgroup-uniform
+    for (int jt = 0; jt < NTOK; ++jt) {
+        if (!over_flag[jt]) continue;  // workgroup-uniform
+        const int64_t t = tok0 + jt;
         const float* zp = z + t * R;
         list_init<K>(v, ix);
-        for (int32_t e = tid; e < M; e += 256) {
+        for (int32_t e = tid; e < M; e += NTHREADS) {
             const float l = exact_logit<RC>([&](int i) { return zp[i]; }, R2t + (int64_t)e * R);
             if (better(l, e, v[K - 1], ix[K - 1])) list_insert<K>(v, ix, l, e);
         }
@@ -919,7 +978,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
         }
         __syncthreads();
         if (tid == 0) {
-            for (int q = 1; q < 4; ++q) {
+            for (int q = 1; q < NW; ++q) {
                 float bv[K];
                 int32_t bi[K];
 #pragma unroll
@@ -933,6 +992,188 @@ __global__ __launch_bounds__(256) void finalize_kernel(
         }
         __syncthreads();
     }
+}
+
+// Final selection over the global candidate lists of the collect kernel, 32 tokens per
+// workgroup.
+template <int RC, int K>
+__global__ __launch_bounds__(256) void finalize_kernel(
+    const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
+    int32_t k, const int32_t* __restrict__ count, const int32_t* __restrict__ cand, int32_t cap,
+    int32_t* __restrict__ idx, float* __restrict__ gate, float* __restrict__ topval) {
+    const int64_t tok0 = (int64_t)blockIdx.x * 32;
+    finalize_tokens<RC, K, 256>(
+        z, R2t, T, M, k, tok0, cap,
+        [&](int j) __attribute__((always_inline)) { return count[tok0 + j]; },
+        [&](int j, int i) __attribute__((always_inline)) { return cand[(tok0 + j) * cap + i]; },
+        idx, gate, topval);
+}
+
+// ------------------------------------------------------------------------------ fused route
+// One workgroup routes 64 tokens against the whole expert axis, for expert sets small enough
+// that every workgroup can read all of R2t from L2 twice: wave w sweeps tiles [Mt w / 8,
+// Mt (w + 1) / 8) for the workgroup's two token groups, with A operands loaded straight from
+// memory D tiles ahead (group norms copied to LDS first).  The screening pass, the threshold, the collect pass and the final
+// selection run in the workgroup with LDS for the exchanges, so one launch replaces the screen,
+// threshold, collect and finalize kernels (same screening bounds, same candidate guarantee, the
+// same exact evaluation: the result is bitwise identical to theirs).
+constexpr int kFusedTokens = 64;
+constexpr int kFusedCap = 256;   // candidates per token (uint16 expert ids)
+// A-operand ring depth (tiles loaded ahead), bounded by the registers at r = 64
+__host__ __device__ constexpr int fused_ring(int RC) { return RC == 2 ? 8 : (RC == 1 ? 4 : 2); }
+constexpr int kFusedMaxTiles = 512;  // expert tiles whose norms fit the LDS copy (M <= 16384)
+
+template <int RC, int K>
+__global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
+    const float* __restrict__ z, const uint16_t* __restrict__ zh, const float* __restrict__ cz,
+    const uint16_t* __restrict__ R2t, const float* __restrict__ gnorm, int32_t T, int32_t M,
+    int32_t k, int32_t* __restrict__ hist, int32_t* __restrict__ idx, float* __restrict__ gate,
+    float* __restrict__ topval) {
+    using C = RouteCfg<RC, K>;
+    constexpr int L = C::L, TPW = 2;
+    __shared__ float tops[kRouteWaves][kFusedTokens][K];
+    __shared__ float theta_s[kFusedTokens];
+    __shared__ int32_t cnt_s[kFusedTokens];
+    __shared__ uint16_t cand_s[kFusedTokens][kFusedCap];
+    constexpr int S = 8;  // candidate slots per lane and token group during the collect pass
+    __shared__ uint16_t slots[S][TPW][kRouteThreads];
+    __shared__ __attribute__((aligned(16))) float gn[kFusedMaxTiles * 8];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 31, half = lane >> 5;
+    const int64_t tok0 = (int64_t)blockIdx.x * kFusedTokens;
+    if (hist) {  // clear the per-expert histogram for this call
+        for (int64_t e = (int64_t)blockIdx.x * kRouteThreads + tid; e < M;
+             e += (int64_t)gridDim.x * kRouteThreads)
+            hist[e] = 0;
+    }
+    if (tid < kFusedTokens) cnt_s[tid] = 0;
+    const int64_t Mt = ((int64_t)M + 31) / 32;
+    for (int i = tid; i < (int)Mt * 8; i += kRouteThreads) gn[i] = gnorm[i];
+    __syncthreads();
+
+    TokenGroups<RC, TPW> tg;
+    tg.load(zh, cz, T, tok0, n, half);
+    const int64_t t0 = Mt * w / kRouteWaves, t1 = Mt * (w + 1) / kRouteWaves;
+    const GlobalRows<RC> src(R2t, gn, M, t0, n, half);
+    const int nt = (int)(t1 - t0);
+    const int32_t e00 = (int32_t)(t0 * 32);
+
+    // Screening pass (as in screen_kernel): the wave's bucket maxima per token.
+    {
+        float bm[TPW][L];
+#pragma unroll
+        for (int g = 0; g < TPW; ++g)
+#pragma unroll
+            for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
+        sweep<RC, K, TPW, fused_ring(RC)>(
+            src, nt, e00, M, half, tg.zhi,
+            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
+                __attribute__((always_inline)) {
+                constexpr int g = decltype(gg)::value;
+                constexpr int UB = 4 * decltype(u)::value;
+                if (partial) mask_past_end(acc, e0, M, half);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    bm[g][UB + q] = fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
+            });
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            sort_desc<L>(bm[g]);
+            float pb[L];
+#pragma unroll
+            for (int b = 0; b < L; ++b) pb[b] = __shfl_xor(bm[g][b], 32, kWave);
+            vlist_merge<L>(bm[g], pb);
+            if (half == 0) {
+#pragma unroll
+                for (int j = 0; j < K; ++j) tops[w][32 * g + n][j] = bm[g][j];
+            }
+        }
+    }
+    __syncthreads();
+    // Threshold per token (as in theta_kernel): 8 threads per token merge the waves' lists.
+    {
+        const int jt = tid >> 3, sub = tid & 7;
+        float v[K];
+#pragma unroll
+        for (int j = 0; j < K; ++j) v[j] = tops[sub][jt][j];
+#pragma unroll
+        for (int s = 1; s < 8; s <<= 1) {
+            float b[K];
+#pragma unroll
+            for (int j = 0; j < K; ++j) b[j] = __shfl_xor(v[j], s, kWave);
+            vlist_merge<K>(v, b);
+        }
+        if (sub == 0) {
+            float th = v[0];
+#pragma unroll
+            for (int j = 1; j < K; ++j)
+                if (j == k - 1) th = v[j];
+            theta_s[jt] = fmaxf(th - fabsf(th) * 0x1p-20f, -0x1p100f);
+        }
+    }
+    __syncthreads();
+    // Collect pass (as in collect_kernel): hits go to lane-private slots first, then into the
+    // token's LDS list with one reservation per lane (a lane with more than S hits overflows
+    // the token, which is then swept exactly).
+    {
+        int cnt[TPW];
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) cnt[g] = 0;
+        float th[TPW];
+#pragma unroll
+        for (int g = 0; g < TPW; ++g)  // tokens past T never qualify (+inf threshold)
+            th[g] = tg.tok_ok(g, n) ? theta_s[32 * g + n] : __builtin_huge_valf();
+        sweep<RC, K, TPW, fused_ring(RC)>(
+            src, nt, e00, M, half, tg.zhi,
+            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
+                __attribute__((always_inline)) {
+                constexpr int g = decltype(gg)::value;
+                (void)u;
+                if (partial) mask_past_end(acc, e0, M, half);
+                const float nmax = fmaxf(fmaxf(nq[0], nq[1]), fmaxf(nq[2], nq[3]));
+                const float m16 = fmaxf(fmaxf(fmaxf(max4(acc, 0), max4(acc, 1)), max4(acc, 2)),
+                                        max4(acc, 3));
+                if (m16 >= th[g] - tg.c[g] * nmax) {
+                    float tq[4], gm[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        tq[q] = th[g] - tg.c[g] * nq[q];
+                        gm[q] = max4(acc, q) - tq[q];
+                    }
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (gm[q] >= 0.0f) {
+#pragma unroll
+                            for (int i = 0; i < 4; ++i) {
+                                if (acc[4 * q + i] >= tq[q]) {
+                                    slots[cnt[g] < S ? cnt[g] : S - 1][g][tid] =
+                                        (uint16_t)(e0 + acc_row(4 * q + i, half));
+                                    ++cnt[g];
+                                }
+                            }
+                        }
+                    }
+                }
+            });
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            if (cnt[g] > 0) {
+                const int tl = 32 * g + n;
+                const int base = atomicAdd(&cnt_s[tl], cnt[g] > S ? kFusedCap + 1 : cnt[g]);
+                if (cnt[g] <= S)
+                    for (int i = 0; i < cnt[g]; ++i)
+                        if (base + i < kFusedCap) cand_s[tl][base + i] = slots[i][g][tid];
+            }
+        }
+    }
+    __syncthreads();
+    finalize_tokens<RC, K, kRouteThreads>(
+        z, R2t, T, M, k, tok0, kFusedCap,
+        [&](int j) __attribute__((always_inline)) { return cnt_s[j]; },
+        [&](int j, int i) __attribute__((always_inline)) { return (int32_t)cand_s[j][i]; }, idx,
+        gate, topval);
 }
 
 // ------------------------------------------------------------------------------ planning
@@ -950,11 +1191,16 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     q.RC = r / 16;
     q.RT = (q.RC + 1) / 2;
     q.K = pow2_at_least(k);
-    const int tokens_per_block = 32 * route_tpw(q.RC, q.K) * kRouteWaves;
-    q.ntb = (int32_t)((T + tokens_per_block - 1) / tokens_per_block);
     const int64_t Mt = ((int64_t)M + 31) / 32;
+    // Library's choice on a small expert set (r M <= 2^18, i.e. R2t <= 512 KiB, read from L2 by
+    // every workgroup twice): the fused route kernel.
+    q.fused = m_chunks == 0 && (int64_t)r * M <= (1 << 18) && Mt <= kFusedMaxTiles;
+    const int tokens_per_block = q.fused ? kFusedTokens : 32 * route_tpw(q.RC, q.K) * kRouteWaves;
+    q.ntb = (int32_t)((T + tokens_per_block - 1) / tokens_per_block);
     const int64_t emax_tiles = (int64_t)kChunkBytes / (2 * r) / 32;
-    if (m_chunks > 0) {
+    if (q.fused) {
+        q.chunks = 1;
+    } else if (m_chunks > 0) {
         q.chunks = m_chunks;
     } else {
         // Chunks that fit the resident LDS rows, and at least 256 workgroups when there are
@@ -967,12 +1213,12 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     if (q.chunks < 1 || q.chunks > 1024) return false;
     // Resident rows must fit in LDS (m_chunks is a request: the result does not depend on
     // the chunking).
-    while ((Mt + q.chunks - 1) / q.chunks > emax_tiles) {
+    while (!q.fused && (Mt + q.chunks - 1) / q.chunks > emax_tiles) {
         if (q.chunks >= (1 << 20)) return false;
         q.chunks *= 2;
     }
     // Token splits: about 256 workgroups in all, each split holding whole token blocks.
-    int64_t S = 256 / q.chunks;
+    int64_t S = q.fused ? q.ntb : 256 / q.chunks;
     if (S < 1) S = 1;
     if (S > q.ntb) S = q.ntb;
     q.splits = (int32_t)S;
@@ -1000,17 +1246,19 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     off += align256((size_t)T * r * sizeof(uint16_t));
     q.off_cz = off;
     off += align256((size_t)T * sizeof(float));
+    // (the fused route keeps its lists, thresholds and candidates in LDS)
+    const size_t route_ws = q.fused ? 0 : 1;
     q.off_top = off;
-    off += align256((size_t)q.chunks * T * q.K * sizeof(float));
+    off += route_ws * align256((size_t)q.chunks * T * q.K * sizeof(float));
     q.off_gnorm = off;
     off += align256((size_t)Mt * 8 * sizeof(float));
     q.off_tau = off;
-    off += align256((size_t)T * sizeof(float));
-    q.cap = 512;
+    off += route_ws * align256((size_t)T * sizeof(float));
+    q.cap = q.fused ? kFusedCap : 512;
     q.off_count = off;
-    off += align256((size_t)T * sizeof(int32_t));
+    off += route_ws * align256((size_t)T * sizeof(int32_t));
     q.off_cand = off;
-    off += align256((size_t)T * q.cap * sizeof(int32_t));
+    off += route_ws * align256((size_t)T * q.cap * sizeof(int32_t));
     q.workspace_bytes = off;
     *p = q;
     return true;
@@ -1044,6 +1292,12 @@ struct RouteArgs {
 
 template <int RC, int K>
 static void launch_route(const LowrankPlan& p, const RouteArgs& a, hipStream_t st) {
+    if (p.fused) {
+        hipLaunchKernelGGL((fused_route_kernel<RC, K>), dim3((unsigned)p.ntb),
+                           dim3(kRouteThreads), 0, st, a.z, a.zhi, a.cz, a.R2t, a.gnorm, a.T,
+                           a.M, a.k, a.hist, a.idx, a.gate, a.topval);
+        return;
+    }
     const dim3 grid((unsigned)((int64_t)p.splits * p.chunks));
     hipLaunchKernelGGL((screen_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.zhi, a.cz,
                        a.R2t, a.T, a.M, p.chunks, p.splits, a.gnorm, a.top);

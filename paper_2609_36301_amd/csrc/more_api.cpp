@@ -79,7 +79,7 @@ more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, 
     if (s != MORE_OK) return s;
     more::LowrankPlan p;
     if (!more::lowrank_make_plan(T > 0 ? T : 1, h, r, M, k, 0, &p)) return MORE_ERR_INVALID_ARG;
-    *m_chunks = p.chunks;
+    *m_chunks = p.fused ? 0 : p.chunks;
     return MORE_OK;
 }
 

@@ -55,7 +55,7 @@ def lowrank_workspace_size(T: int, h: int, r: int, M: int, k: int, m_chunks: int
 
 
 def lowrank_plan(T: int, h: int, r: int, M: int, k: int) -> int:
-    """Number of expert-axis chunks the library picks for this shape."""
+    """Number of expert-axis chunks the library picks for this shape (0: the fused route)."""
     c = ctypes.c_int32(0)
     _lib.check(_lib.load().more_route_lowrank_plan(T, h, r, M, k, ctypes.byref(c)),
                "more_route_lowrank_plan")

@@ -135,7 +135,11 @@ def test_plans_for_the_paper_shapes(lib):
               "fine": (16384, 64, 65536, 8), "decode": (128, 64, 262144, 16)}
     for name, C in plans.items():
         T, r, M, k = shapes[name]
-        tokens_per_block = 1024 if (k <= 8 and r == 64) else 512  # 8 waves x 32 x (4 or 2) tokens
+        if r * M <= 1 << 18:  # fused route: 64 tokens per workgroup, the whole expert axis
+            assert C == 0, name
+            assert -(-T // 64) >= 256, name
+            continue
+        tokens_per_block = 1024 if (k <= 8 and r == 64) else 512  # 8 waves x 32 x (4 or 2)
         assert C & (C - 1) == 0, name
         assert r * M * 2 // C <= 2 << 20, name          # expert slice fits one L2
         assert C * -(-T // tokens_per_block) >= 256, name  # at least one workgroup per CU

@@ -123,6 +123,22 @@ def test_expert_chunking_is_bitwise_identical(chunks):
     _check(inp, 8, base[0], base[1], base[2], label="chunks")
 
 
+@pytest.mark.parametrize("shape", [(16384, 512, 32, 4096, 8), (300, 96, 64, 4100, 16),
+                                   (77, 64, 16, 1000, 5), (129, 128, 32, 33, 1)],
+                         ids=lambda s: "T%d_h%d_r%d_M%d_k%d" % s)
+def test_fused_route_matches_resident_route_bitwise(shape):
+    # m_chunks=0 picks the one-kernel fused route on these small expert sets; m_chunks=1 forces
+    # the expert-resident route (screen, threshold, collect and finalize kernels).
+    T, h, r, M, k = shape
+    inp = make_inputs(T, h, r, M, seed=T + 3 * M)
+    fused = route_lowrank(inp, k, histogram=True, tag="fused")
+    resident = route_lowrank(inp, k, histogram=True, m_chunks=1, tag="resident")
+    for a, b in zip(fused, resident):
+        assert np.array_equal(a, b)
+    rows = None if T <= 4096 else _sample_rows(T, 512, seed=5)
+    _check(inp, k, fused[0], fused[1], fused[2], rows=rows, label="fused %s" % (shape,))
+
+
 def test_repeat_runs_bitwise_identical():
     inp = make_inputs(1000, 512, 64, 3000, seed=12)
     a = route_lowrank(inp, 16, tag="run1")
