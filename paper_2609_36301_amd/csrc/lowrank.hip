@@ -44,8 +44,9 @@ __device__ __forceinline__ void unroll(F&& f) {
 
 // Error scale of the screened logits of one token (see the route section):
 // c = (||z_lo|| + r 2^-23 ||z_hi||) (1 + 2^-10), from the squared norms.
+// It is kept >= 2^-126 (a looser bound), so that c 2^100 always dominates a logit.
 __device__ __forceinline__ float screen_scale(float lo2, float hi2, int r) {
-    return (sqrtf(lo2) + (float)r * 0x1p-23f * sqrtf(hi2)) * (1.0f + 0x1p-10f);
+    return fmaxf((sqrtf(lo2) + (float)r * 0x1p-23f * sqrtf(hi2)) * (1.0f + 0x1p-10f), 0x1p-126f);
 }
 
 // ------------------------------------------------------------------------------ zpass
@@ -54,11 +55,15 @@ __device__ __forceinline__ float screen_scale(float lo2, float hi2, int r) {
 // in LDS and shared by the four waves; x and R1 are prefetched D chunks ahead in registers.  With
 // hsplit > 1 the chunks are split over hsplit workgroups and each split writes a partial z.
 constexpr int kZWaves = 4;
+constexpr float kPhantomNorm = 0x1p100f;  // norm bound of a 4-expert group reaching past M
 constexpr int kZTokens = 32 * kZWaves;
 constexpr int kZChunk = 64;
 
 // Group norms: the largest Euclidean norm among expert rows 4g..4g+3 of R2t, rounded up, for
-// every group of the rows < `rows` (all tiles); rows past M count as zero.  Within each tile of
+// every group of the rows < `rows` (all tiles).  A group holding a row past M gets the norm bound
+// 2^100 instead: its screening bounds s -+ c 2^100 then never raise a threshold and always pass
+// the collect test, so the sweeps need no masking of the rows past M (they re-read row M - 1)
+// and the candidate expansion drops the ids >= M.  Within each tile of
 // 32 rows the 8 groups are stored in the order [half][q] (group 2q + half at 4 half + q), so
 // that MFMA lane half `half` reads the norms of its four accumulator groups q with one 16-byte
 // load.  Lane (row, 16-byte segment) layout: the
@@ -82,7 +87,8 @@ __device__ __forceinline__ void group_norms(const uint16_t* __restrict__ R2t, in
     if (col == 0 && (row & 3) == 0 && row < rows) {
         // slot of group g4 = (row mod 32) / 4 = 2q + half of tile row / 32: [tile][half][q]
         const int g4 = (int)(row & 31) >> 2;
-        gnorm[(row >> 5) * 8 + (g4 & 1) * 4 + (g4 >> 1)] = sqrtf(ss) * (1.0f + 0x1p-20f);
+        gnorm[(row >> 5) * 8 + (g4 & 1) * 4 + (g4 >> 1)] =
+            row + 3 < M ? sqrtf(ss) * (1.0f + 0x1p-20f) : kPhantomNorm;
     }
 }
 
@@ -370,12 +376,6 @@ __device__ __forceinline__ float max4(const f32x16& a, int q) {
     return fmaxf(fmaxf(a[4 * q], a[4 * q + 1]), fmaxf(a[4 * q + 2], a[4 * q + 3]));
 }
 
-__device__ __forceinline__ void mask_past_end(f32x16& acc, int32_t e0, int32_t M, int half) {
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-        if (e0 + acc_row(j, half) >= M) acc[j] = -__builtin_huge_valf();
-}
-
 // Work split of a route launch: workgroup -> (expert chunk, range of token blocks).
 struct RouteSplit {
     int32_t chunk;
@@ -397,7 +397,7 @@ __device__ __forceinline__ RouteSplit route_split(int32_t T, int32_t M, int32_t 
     return q;
 }
 
-// Loads the rows of tiles [t0, t1) (rows past M re-read row M - 1; they are masked later) and
+// Loads the rows of tiles [t0, t1) (rows past M re-read row M - 1; see group_norms) and
 // their group norms into LDS; every thread of the workgroup takes part.
 template <int RC, int K>
 __device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ R2t,
@@ -494,7 +494,7 @@ struct LdsRows {
 
 // GlobalRows: rows read straight from R2t (L2-resident when the expert set is small), norms
 // from a copy of the group norms in LDS; tiles are counted from global tile tile0, rows past M
-// re-read row M - 1 (masked by the caller).
+// re-read row M - 1 (see group_norms).
 template <int RC>
 struct GlobalRows {
     const uint16_t* row;   // R2t + (32 tile0 + n) * R + 8 half
@@ -518,7 +518,7 @@ struct GlobalRows {
 };
 
 // Sweeps nt tiles (experts e00 .. e00 + 32 nt - 1) for one lane's token groups and calls
-// body(g, acc, e0, partial, u, nq) once per token group g and tile: acc holds s for the group's
+// body(g, acc, e0, u, nq) once per token group g and tile: acc holds s for the group's
 // 32 tokens and the tile's 32 experts starting at e0, nq[q] is the norm bound of accumulator
 // group q, u = tile mod U the bucket index (g and u are std::integral_constant).
 //
@@ -527,8 +527,8 @@ struct GlobalRows {
 // issues the MFMAs of H1(t) and finishes H0(t): every epilogue runs while the other half's
 // MFMAs execute.  The A operands and norms of the next D tiles are held in a register ring (the
 // refill of a slot is issued once its last reader has been issued).  The steady-state loop runs
-// groups of V = max(U, D, 2) tiles, so that ring slots, bucket indices and partial = false are
-// compile-time constants there and each tile is one basic block.
+// groups of V = max(U, D, 2) tiles, so that ring slots and bucket indices are compile-time
+// constants there and each tile is one basic block.
 template <int RC, int K, int TPW, int D, typename Src, typename Body>
 __device__ __forceinline__ void sweep(const Src& src, int nt, int32_t e00, int32_t M, int half,
                                       const bf16x8 (&zhi)[TPW][RC], Body&& body) {
@@ -557,60 +557,165 @@ __device__ __forceinline__ void sweep(const Src& src, int nt, int32_t e00, int32
 #pragma unroll
             for (int g = G0; g < G0 + H; ++g) acc[g] = mfma_32x32x16(a[A][c], zhi[g][c], acc[g]);
     };
-    auto finish = [&](auto nslot, auto hh, int tile, bool partial, auto u)
-                      __attribute__((always_inline)) {
+    auto finish = [&](auto nslot, auto hh, int tile, auto u) __attribute__((always_inline)) {
         constexpr int NS = decltype(nslot)::value;
         constexpr int G0 = decltype(hh)::value * H;
         const int32_t e0 = e00 + tile * 32;
         unroll<H>([&](auto gg) __attribute__((always_inline)) {
             constexpr int G = G0 + decltype(gg)::value;
-            body(std::integral_constant<int, G>{}, acc[G], e0, partial, u, nq[NS]);
+            body(std::integral_constant<int, G>{}, acc[G], e0, u, nq[NS]);
         });
     };
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
     // Tile `tile` = j (mod V) with j = J: A slot j mod D, norm slot j mod ND, bucket j mod U.
-    auto step = [&](auto jj, auto has_prev, int tile, bool partial)
-                    __attribute__((always_inline)) {
+    auto step = [&](auto jj, auto has_prev, int tile) __attribute__((always_inline)) {
         constexpr int J = decltype(jj)::value;
         using SA = std::integral_constant<int, J % D>;
         using SN = std::integral_constant<int, J % ND>;
         using SP = std::integral_constant<int, (J + ND - 1) % ND>;
         mfmas(SA{}, I0{});
         if constexpr (decltype(has_prev)::value) {
-            finish(SP{}, I1{}, tile - 1, false, std::integral_constant<int, (J + V - 1) % U>{});
+            finish(SP{}, I1{}, tile - 1, std::integral_constant<int, (J + V - 1) % U>{});
             fetch_nq(SP{}, tile - 1 + ND);
         }
         mfmas(SA{}, I1{});
         fetch(SA{}, tile + D);
-        finish(SN{}, I0{}, tile, partial, std::integral_constant<int, J % U>{});
+        finish(SN{}, I0{}, tile, std::integral_constant<int, J % U>{});
     };
-    const bool plast = e00 + nt * 32 > M;
     unroll<D>([&](auto s) __attribute__((always_inline)) { fetch(s, decltype(s)::value); });
     unroll<ND>([&](auto s) __attribute__((always_inline)) { fetch_nq(s, decltype(s)::value); });
-    step(I0{}, std::false_type{}, 0, nt == 1 && plast);
+    step(I0{}, std::false_type{}, 0);
     // Tiles 1 .. nt - 2 (t = 1 mod V in the loop, so tile t + VV has residue 1 + VV).
     int t = 1;
     for (; t + V <= nt - 1; t += V)
         unroll<V>([&](auto vv) __attribute__((always_inline)) {
             step(std::integral_constant<int, (1 + decltype(vv)::value) % V>{}, std::true_type{},
-                 t + decltype(vv)::value, false);
+                 t + decltype(vv)::value);
         });
     unroll<V>([&](auto vv) __attribute__((always_inline)) {
         if (t + decltype(vv)::value < nt - 1)
             step(std::integral_constant<int, (1 + decltype(vv)::value) % V>{}, std::true_type{},
-                 t + decltype(vv)::value, false);
+                 t + decltype(vv)::value);
     });
     // Last tile (when nt > 1), then the second half of the last tile; residues dispatched to
     // compile-time values.
     unroll<V>([&](auto vv) __attribute__((always_inline)) {
         constexpr int J = decltype(vv)::value;
         if ((nt - 1) % V == J) {
-            if (nt > 1) step(vv, std::true_type{}, nt - 1, plast);
-            finish(std::integral_constant<int, J % ND>{}, I1{}, nt - 1, plast,
+            if (nt > 1) step(vv, std::true_type{}, nt - 1);
+            finish(std::integral_constant<int, J % ND>{}, I1{}, nt - 1,
                    std::integral_constant<int, J % U>{});
         }
     });
+}
+
+// The same sweep over tiles whose A operands are held in registers (a[t] for tile t < nt <=
+// NTW, loaded by the caller) and whose norms sit in LDS (gn + 8 t + 4 half).  Tiles are fully
+// unrolled, so register indices are compile-time constants.
+template <int RC, int K, int TPW, int NTW, typename Body>
+__device__ __forceinline__ void sweep_regs(const bf16x8 (&a)[NTW][RC], const float* gn, int nt,
+                                           int32_t e00, int32_t M, int half,
+                                           const bf16x8 (&zhi)[TPW][RC], Body&& body) {
+    using C = RouteCfg<RC, K>;
+    constexpr int H = TPW / 2;
+    constexpr int U = C::U;
+    f32x16 acc[TPW];
+    f32x4 nq[2];
+    auto mfmas = [&](auto jj, auto hh) __attribute__((always_inline)) {
+        constexpr int J = decltype(jj)::value;
+        constexpr int G0 = decltype(hh)::value * H;
+#pragma unroll
+        for (int g = G0; g < G0 + H; ++g) acc[g] = zero_f32x16();
+#pragma unroll
+        for (int c = 0; c < RC; ++c)
+#pragma unroll
+            for (int g = G0; g < G0 + H; ++g) acc[g] = mfma_32x32x16(a[J][c], zhi[g][c], acc[g]);
+    };
+    auto finish = [&](auto jj, auto hh) __attribute__((always_inline)) {
+        constexpr int J = decltype(jj)::value;
+        constexpr int G0 = decltype(hh)::value * H;
+        unroll<H>([&](auto gg) __attribute__((always_inline)) {
+            constexpr int G = G0 + decltype(gg)::value;
+            body(std::integral_constant<int, G>{}, acc[G], e00 + J * 32,
+                 std::integral_constant<int, J % U>{}, nq[J & 1]);
+        });
+    };
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+        constexpr int J = decltype(jj)::value;
+        if (J < nt) {  // wave-uniform
+            nq[J & 1] = *reinterpret_cast<const f32x4*>(gn + J * 8 + 4 * half);
+            mfmas(jj, I0{});
+            if constexpr (J > 0) finish(std::integral_constant<int, J - 1>{}, I1{});
+            mfmas(jj, I1{});
+            finish(jj, I0{});
+        }
+    });
+    unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+        if (decltype(jj)::value == nt - 1) finish(jj, I1{});
+    });
+}
+
+// Collect test of one token group and tile.  For every accumulator group q of the lane (rows
+// 8q + 4 half + 0..3 of the tile, i.e. 4-expert group 2q + half) holding an expert with
+// s_e + c N_g >= theta, appends one entry (group index gbase + 2q << 4 | bit mask of those
+// experts) to the lane's slots (slot(i) = address of entry i, the last slot takes every
+// entry past it) and returns the new entry count.  A first test with the lane's largest group
+// norm (one compare) skips most tiles.
+template <int S, typename Slot>
+__device__ __forceinline__ int collect_tile(const f32x16& acc, float th, float c, const f32x4& nq,
+                                            int32_t gbase, int cnt, Slot&& slot) {
+    const float nmax = fmaxf(fmaxf(nq[0], nq[1]), fmaxf(nq[2], nq[3]));
+    const float m16 = fmaxf(fmaxf(fmaxf(max4(acc, 0), max4(acc, 1)), max4(acc, 2)), max4(acc, 3));
+    if (m16 >= th - c * nmax) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float tq = th - c * nq[q];
+            if (max4(acc, q) >= tq) {
+                const uint32_t m = (acc[4 * q] >= tq ? 1u : 0u) | (acc[4 * q + 1] >= tq ? 2u : 0u) |
+                                   (acc[4 * q + 2] >= tq ? 4u : 0u) | (acc[4 * q + 3] >= tq ? 8u : 0u);
+                *slot(cnt < S ? cnt : S - 1) = (uint16_t)(((uint32_t)(gbase + 2 * q) << 4) | m);
+                ++cnt;
+            }
+        }
+    }
+    return cnt;
+}
+
+// Bit mask of the experts of slot entry v that exist (ebase + 4 group + bit < M).
+__device__ __forceinline__ uint32_t slot_bits(uint32_t v, int32_t ebase, int32_t M) {
+    const int32_t left = M - ebase - 4 * (int32_t)(v >> 4);  // experts of the group below M
+    return v & (left >= 4 ? 15u : (left > 0 ? (1u << left) - 1u : 0u));
+}
+
+// Number of experts in the first min(cnt, S) slot entries of a lane.
+template <int S, typename Slot>
+__device__ __forceinline__ int slot_experts(int cnt, Slot&& slot, int32_t ebase, int32_t M) {
+    int ne = 0;
+    for (int i = 0; i < cnt && i < S; ++i) ne += __builtin_popcount(slot_bits(*slot(i), ebase, M));
+    return ne;
+}
+
+// Writes the experts of a lane's slot entries (ebase + 4 group + bit, ids < M only) to
+// out[0..), at most `room` of them.
+template <typename Slot>
+__device__ __forceinline__ void slot_expand(int cnt, Slot&& slot, int32_t ebase, int32_t M,
+                                            int32_t* out, int room) {
+    int o = 0;
+    for (int i = 0; i < cnt; ++i) {
+        const uint32_t v = *slot(i);
+        const uint32_t m = slot_bits(v, ebase, M);
+        const int32_t e = ebase + 4 * (int32_t)(v >> 4);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            if ((m >> b) & 1u) {
+                if (o < room) out[o] = e + b;
+                ++o;
+            }
+        }
+    }
 }
 
 // Screening sweep.  For each accumulator group q of a tile the lane forms the lower bound
@@ -658,11 +763,11 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
             for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
         sweep<RC, K, TPW, 1>(
             src, (int)(sp.t1 - sp.t0), (int32_t)(sp.t0 * 32), M, half, tg.zhi,
-            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
+            [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
                 constexpr int g = decltype(gg)::value;
                 constexpr int UB = 4 * decltype(u)::value;
-                if (partial) mask_past_end(acc, e0, M, half);
+                (void)e0;
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     bm[g][UB + q] = fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
@@ -811,53 +916,30 @@ __global__ __launch_bounds__(kRouteThreads, 2) void collect_kernel(
         for (int g = 0; g < TPW; ++g) cnt[g] = 0;
         sweep<RC, K, TPW, 1>(
             src, (int)(sp.t1 - sp.t0), (int32_t)(sp.t0 * 32), M, half, tg.zhi,
-            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
+            [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
                 constexpr int g = decltype(gg)::value;
                 (void)u;
-                if (partial) mask_past_end(acc, e0, M, half);
-                // Tile test with the lane's largest group norm (a looser bound, one compare);
-                // the exact per-group tests run only when it passes.
-                const float nmax = fmaxf(fmaxf(nq[0], nq[1]), fmaxf(nq[2], nq[3]));
-                const float m16 = fmaxf(fmaxf(fmaxf(max4(acc, 0), max4(acc, 1)), max4(acc, 2)),
-                                        max4(acc, 3));
-                if (m16 >= th[g] - tg.c[g] * nmax) {
-                    float tq[4], gm[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        tq[q] = th[g] - tg.c[g] * nq[q];
-                        gm[q] = max4(acc, q) - tq[q];
-                    }
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        if (gm[q] >= 0.0f) {
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                if (acc[4 * q + i] >= tq[q]) {
-                                    slots[cnt[g] < S ? cnt[g] : S - 1][g][tid] =
-                                        (uint16_t)(e0 - ebase + acc_row(4 * q + i, half));
-                                    ++cnt[g];
-                                }
-                            }
-                        }
-                    }
-                }
+                cnt[g] = collect_tile<S>(acc, th[g], tg.c[g], nq, (e0 - ebase) / 4 + half, cnt[g],
+                                         [&](int i) { return &slots[i][g][tid]; });
             });
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
+            auto slot = [&](int i) { return &slots[i][g][tid]; };
+            const int ne = slot_experts<S>(cnt[g], slot, ebase, M);
+            const int pe = __shfl_xor(ne, 32, kWave);
             const int pc = __shfl_xor(cnt[g], 32, kWave);
             const bool over = cnt[g] > S || pc > S;
-            const int total = cnt[g] + pc;
+            const int total = ne + pe;
             int base = 0;
             const int64_t tk = tg.tok(g, n);
             if (half == 0 && tk < T && total > 0)
                 base = atomicAdd(&count[tk], over ? cap + 1 : total);
             base = __shfl(base, n, kWave);  // lane half 1 reads its partner's reservation
             if (tk < T && !over) {
-                const int off = base + (half ? pc : 0);
-                for (int i = 0; i < cnt[g]; ++i)
-                    if (off + i < cap)
-                        cand[tk * cap + off + i] = ebase + (int32_t)slots[i][g][tid];
+                const int off = base + (half ? pe : 0);
+                if (off < cap)
+                    slot_expand(cnt[g], slot, ebase, M, cand + tk * cap + off, cap - off);
             }
         }
         if constexpr (C::PREFETCH) {
@@ -1018,12 +1100,15 @@ __global__ __launch_bounds__(256) void finalize_kernel(
 // threshold, collect and finalize kernels (same screening bounds, same candidate guarantee, the
 // same exact evaluation: the result is bitwise identical to theirs).
 constexpr int kFusedTokens = 64;
-constexpr int kFusedCap = 256;   // candidates per token (uint16 expert ids)
+constexpr int kFusedCap = 128;   // candidates per token
 // A-operand ring depth (tiles loaded ahead), bounded by the registers at r = 64
 __host__ __device__ constexpr int fused_ring(int RC) { return RC == 2 ? 8 : (RC == 1 ? 4 : 2); }
 constexpr int kFusedMaxTiles = 512;  // expert tiles whose norms fit the LDS copy (M <= 16384)
 
-template <int RC, int K>
+// Tiles per wave whose A operands fit in 128 registers (REG variant: r M <= 2^17).
+__host__ __device__ constexpr int fused_reg_tiles(int RC) { return 32 / RC; }
+
+template <int RC, int K, bool REG>
 __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
     const float* __restrict__ z, const uint16_t* __restrict__ zh, const float* __restrict__ cz,
     const uint16_t* __restrict__ R2t, const float* __restrict__ gnorm, int32_t T, int32_t M,
@@ -1034,7 +1119,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
     __shared__ float tops[kRouteWaves][kFusedTokens][K];
     __shared__ float theta_s[kFusedTokens];
     __shared__ int32_t cnt_s[kFusedTokens];
-    __shared__ uint16_t cand_s[kFusedTokens][kFusedCap];
+    __shared__ int32_t cand_s32[kFusedTokens * kFusedCap];
     constexpr int S = 8;  // candidate slots per lane and token group during the collect pass
     __shared__ uint16_t slots[S][TPW][kRouteThreads];
     __shared__ __attribute__((aligned(16))) float gn[kFusedMaxTiles * 8];
@@ -1059,6 +1144,21 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
     const GlobalRows<RC> src(R2t, gn, M, t0, n, half);
     const int nt = (int)(t1 - t0);
     const int32_t e00 = (int32_t)(t0 * 32);
+    // REG: the wave's A operands stay in registers for both passes (loaded once, here).
+    constexpr int NTW = REG ? fused_reg_tiles(RC) : 1;
+    bf16x8 areg[NTW][RC];
+    if constexpr (REG) {
+        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+            src.load_a(decltype(jj)::value < nt ? decltype(jj)::value : (nt > 0 ? nt - 1 : 0),
+                       areg[decltype(jj)::value]);
+        });
+    }
+    auto run_sweep = [&](auto&& body) __attribute__((always_inline)) {
+        if constexpr (REG)
+            sweep_regs<RC, K, TPW, NTW>(areg, gn + t0 * 8, nt, e00, M, half, tg.zhi, body);
+        else
+            sweep<RC, K, TPW, fused_ring(RC)>(src, nt, e00, M, half, tg.zhi, body);
+    };
 
     // Screening pass (as in screen_kernel): the wave's bucket maxima per token.
     {
@@ -1067,13 +1167,12 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
         for (int g = 0; g < TPW; ++g)
 #pragma unroll
             for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
-        sweep<RC, K, TPW, fused_ring(RC)>(
-            src, nt, e00, M, half, tg.zhi,
-            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
+        run_sweep(
+            [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
                 constexpr int g = decltype(gg)::value;
                 constexpr int UB = 4 * decltype(u)::value;
-                if (partial) mask_past_end(acc, e0, M, half);
+                (void)e0;
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     bm[g][UB + q] = fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
@@ -1125,46 +1224,24 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
 #pragma unroll
         for (int g = 0; g < TPW; ++g)  // tokens past T never qualify (+inf threshold)
             th[g] = tg.tok_ok(g, n) ? theta_s[32 * g + n] : __builtin_huge_valf();
-        sweep<RC, K, TPW, fused_ring(RC)>(
-            src, nt, e00, M, half, tg.zhi,
-            [&](auto gg, f32x16& acc, int32_t e0, bool partial, auto u, const f32x4& nq)
+        run_sweep(
+            [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
                 __attribute__((always_inline)) {
                 constexpr int g = decltype(gg)::value;
                 (void)u;
-                if (partial) mask_past_end(acc, e0, M, half);
-                const float nmax = fmaxf(fmaxf(nq[0], nq[1]), fmaxf(nq[2], nq[3]));
-                const float m16 = fmaxf(fmaxf(fmaxf(max4(acc, 0), max4(acc, 1)), max4(acc, 2)),
-                                        max4(acc, 3));
-                if (m16 >= th[g] - tg.c[g] * nmax) {
-                    float tq[4], gm[4];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        tq[q] = th[g] - tg.c[g] * nq[q];
-                        gm[q] = max4(acc, q) - tq[q];
-                    }
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        if (gm[q] >= 0.0f) {
-#pragma unroll
-                            for (int i = 0; i < 4; ++i) {
-                                if (acc[4 * q + i] >= tq[q]) {
-                                    slots[cnt[g] < S ? cnt[g] : S - 1][g][tid] =
-                                        (uint16_t)(e0 + acc_row(4 * q + i, half));
-                                    ++cnt[g];
-                                }
-                            }
-                        }
-                    }
-                }
+                cnt[g] = collect_tile<S>(acc, th[g], tg.c[g], nq, e0 / 4 + half, cnt[g],
+                                         [&](int i) { return &slots[i][g][tid]; });
             });
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
             if (cnt[g] > 0) {
+                auto slot = [&](int i) { return &slots[i][g][tid]; };
                 const int tl = 32 * g + n;
-                const int base = atomicAdd(&cnt_s[tl], cnt[g] > S ? kFusedCap + 1 : cnt[g]);
-                if (cnt[g] <= S)
-                    for (int i = 0; i < cnt[g]; ++i)
-                        if (base + i < kFusedCap) cand_s[tl][base + i] = slots[i][g][tid];
+                const int ne = slot_experts<S>(cnt[g], slot, 0, M);
+                const int base = atomicAdd(&cnt_s[tl], cnt[g] > S ? kFusedCap + 1 : ne);
+                if (cnt[g] <= S && base < kFusedCap)
+                    slot_expand(cnt[g], slot, 0, M, cand_s32 + tl * kFusedCap + base,
+                                kFusedCap - base);
             }
         }
     }
@@ -1172,7 +1249,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
     finalize_tokens<RC, K, kRouteThreads>(
         z, R2t, T, M, k, tok0, kFusedCap,
         [&](int j) __attribute__((always_inline)) { return cnt_s[j]; },
-        [&](int j, int i) __attribute__((always_inline)) { return (int32_t)cand_s[j][i]; }, idx,
+        [&](int j, int i) __attribute__((always_inline)) { return cand_s32[j * kFusedCap + i]; }, idx,
         gate, topval);
 }
 
@@ -1293,7 +1370,18 @@ struct RouteArgs {
 template <int RC, int K>
 static void launch_route(const LowrankPlan& p, const RouteArgs& a, hipStream_t st) {
     if (p.fused) {
-        hipLaunchKernelGGL((fused_route_kernel<RC, K>), dim3((unsigned)p.ntb),
+        // A operands in registers when the wave's tiles fit (r M <= 2^17; K <= 8, where the
+        // bucket maxima leave room for them).
+        const int64_t Mt = ((int64_t)a.M + 31) / 32;
+        if constexpr (K <= 8) {
+            if ((Mt + kRouteWaves - 1) / kRouteWaves <= fused_reg_tiles(RC)) {
+                hipLaunchKernelGGL((fused_route_kernel<RC, K, true>), dim3((unsigned)p.ntb),
+                                   dim3(kRouteThreads), 0, st, a.z, a.zhi, a.cz, a.R2t, a.gnorm,
+                                   a.T, a.M, a.k, a.hist, a.idx, a.gate, a.topval);
+                return;
+            }
+        }
+        hipLaunchKernelGGL((fused_route_kernel<RC, K, false>), dim3((unsigned)p.ntb),
                            dim3(kRouteThreads), 0, st, a.z, a.zhi, a.cz, a.R2t, a.gnorm, a.T,
                            a.M, a.k, a.hist, a.idx, a.gate, a.topval);
         return;
