@@ -91,10 +91,15 @@ more_status more_route_lowrank_workspace_size(int64_t T, int32_t h, int32_t r, i
 /*
  * Same as more_route_lowrank with the expert axis split into (at least) `m_chunks` slices
  * processed by separate workgroups and merged afterwards (0 = the library's choice, which may be
- * the fused single-kernel route on small expert sets; 1 = no split, else a multiple of 8 up to
- * 1024; the library raises it when a slice would not fit in one workgroup's LDS).  Every choice returns bitwise identical results; this entry point
- * exists for tuning and for tests of that property.  Its workspace size comes from
- * more_route_lowrank_workspace_size_ex with the same m_chunks.
+ * a fused route on small expert sets; 1 = no split, else a multiple of 8 up to 1024; the library
+ * raises it when a slice would not fit in one workgroup's LDS).  Every m_chunks >= 1 returns
+ * bitwise identical results, and so does the fused route that reads the z pass (r M <= 2^18).
+ * The one-launch fused route (r M <= 2^17 with K <= 8, and M <= 1024 at r = 64) computes z
+ * inside the routing workgroup, summing the h axis in another order: its logits can differ from
+ * the others' in the last bits (selections only where logits tie to rounding).  This entry
+ * point exists for tuning and for tests of these properties.  Its workspace size comes from
+ * more_route_lowrank_workspace_size_ex with the same m_chunks (0 bytes for the one-launch
+ * route).
  */
 more_status more_route_lowrank_ex(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
                                   int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
@@ -106,8 +111,8 @@ more_status more_route_lowrank_workspace_size_ex(int64_t T, int32_t h, int32_t r
 
 /* The m_chunks value the library picks for this shape (written to *m_chunks, host): the
  * number of expert-axis slices of the expert-resident route, or 0 when the library routes this
- * shape with the fused single-kernel route (expert sets with r * M <= 2^18 and M <= 16384: one
- * workgroup per 64 tokens sweeps all experts; same results bit for bit). */
+ * shape with a fused route (expert sets with r * M <= 2^18 and M <= 16384: one workgroup per 64
+ * tokens sweeps all experts; see more_route_lowrank_ex). */
 more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
                                     int32_t* m_chunks);
 

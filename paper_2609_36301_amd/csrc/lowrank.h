@@ -13,6 +13,7 @@ struct LowrankPlan {
     int32_t RT;               // 32-row tiles of the rank axis in the z pass
     int32_t K;                // top-K list length (power of two >= k)
     int32_t fused;            // 1: one fused route kernel per 64 tokens (small expert sets)
+    int32_t local;            // 1: the fused kernel also computes z (one launch in all)
     int32_t ntb;              // token blocks of the route kernels
     int32_t chunks;           // expert-axis chunks, each resident in one workgroup's LDS
                               // (1 for the fused route)

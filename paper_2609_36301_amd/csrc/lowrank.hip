@@ -690,6 +690,38 @@ __device__ __forceinline__ uint32_t slot_bits(uint32_t v, int32_t ebase, int32_t
     return v & (left >= 4 ? 15u : (left > 0 ? (1u << left) - 1u : 0u));
 }
 
+// Collect test of the fused kernels (LDS for 32-bit entries): one entry per lane and tile with a
+// hit, (2 tile + half) << 16 | the 16-bit mask of accumulator elements with s_e + c N_g >= theta
+// (element 4q + i is expert 32 tile + 8q + 4 half + i), built without branches.
+template <int S, typename Slot>
+__device__ __forceinline__ int collect_tile16(const f32x16& acc, float th, float c, const f32x4& nq,
+                                              int32_t code, int cnt, Slot&& slot) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const float tq = th - c * nq[q];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m |= acc[4 * q + i] >= tq ? (1u << (4 * q + i)) : 0u;
+    }
+    if (m) {
+        *slot(cnt < S ? cnt : S - 1) = ((uint32_t)code << 16) | m;
+        ++cnt;
+    }
+    return cnt;
+}
+
+// Experts of a 32-bit entry that exist (< M), as a 16-bit mask.
+__device__ __forceinline__ uint32_t entry16_bits(uint32_t v, int32_t M) {
+    const int32_t tile = (int32_t)(v >> 17), half = (int32_t)(v >> 16) & 1;
+    uint32_t m = v & 0xFFFFu;
+    if (tile * 32 + 32 > M) {  // last tile only
+#pragma unroll
+        for (int b = 0; b < 16; ++b)
+            if (tile * 32 + 8 * (b >> 2) + 4 * half + (b & 3) >= M) m &= ~(1u << b);
+    }
+    return m;
+}
+
 // Number of experts in the first min(cnt, S) slot entries of a lane.
 template <int S, typename Slot>
 __device__ __forceinline__ int slot_experts(int cnt, Slot&& slot, int32_t ebase, int32_t M) {
@@ -967,17 +999,25 @@ __device__ __forceinline__ float exact_logit(const ZRow& zr, const uint16_t* __r
     return acc;
 }
 
-// Final selection for the NTOK = NTHREADS / 8 tokens tok0 .. tok0 + NTOK - 1 of a workgroup: 8
-// lanes per token evaluate the token's candidates exactly, keep a top-K list each and merge;
-// lane 0 of the group writes the softmax over the best k.  count_of(j) is the number of
-// candidates of local token j and cand_of(j, i) its i-th candidate.  Tokens whose candidate list
-// overflowed (count > cap) are recomputed by the whole workgroup with an exact sweep over all M
-// experts.  Must be reached by every thread of the workgroup.
-template <int RC, int K, int NTHREADS, typename CountOf, typename CandOf>
-__device__ __forceinline__ void finalize_tokens(const float* __restrict__ z,
+// Final selection for the NTOK = NTHREADS / 8 tokens tok0 .. tok0 + NTOK - 1 of a workgroup.  8
+// lanes per token evaluate the token's candidates exactly (fp32 z times the bf16 expert rows, rank
+// entries in increasing order).  zrow_of(j) is the fp32 z row of local token j (any address for
+// tokens past T), count_of(j) the number of its candidates and cand_of(j, i) the i-th.
+//  - up to RCAP candidates (the common case; RCAP = 0 turns this path off): the logits and
+//    experts go to the LDS arrays lv and le ([NTOK][RCAP], given by the caller), each candidate's
+//    rank under the selection order is counted against the others, ranks below k write their
+//    output slot;
+//  - up to cap: each lane keeps a top-K list, the 8 lists are merged, lane 0 writes;
+//  - more (an overflowed list): the whole workgroup sweeps all M experts for the token.
+// Either way the softmax adds exp(l - l_max) in rank order, so every path gives the same bits.
+// Must be reached by every thread of the workgroup.
+template <int RC, int K, int NTHREADS, int RCAP, typename ZRowOf, typename CountOf,
+          typename CandOf>
+__device__ __forceinline__ void finalize_tokens(ZRowOf&& zrow_of,
                                                 const uint16_t* __restrict__ R2t, int32_t T,
                                                 int32_t M, int32_t k, int64_t tok0, int32_t cap,
                                                 CountOf&& count_of, CandOf&& cand_of,
+                                                float* lv, int32_t* le,
                                                 int32_t* __restrict__ idx,
                                                 float* __restrict__ gate,
                                                 float* __restrict__ topval) {
@@ -986,6 +1026,7 @@ __device__ __forceinline__ void finalize_tokens(const float* __restrict__ z,
     __shared__ int32_t over_flag[NTOK];
     __shared__ float wv[NW][K];
     __shared__ int32_t wi[NW][K];
+    __shared__ float ex[NTOK][K];       // exp(l - l_max) by rank
     const int tid = threadIdx.x;
     const int sub = tid & 7;
     const int j = tid >> 3;
@@ -994,12 +1035,13 @@ __device__ __forceinline__ void finalize_tokens(const float* __restrict__ z,
     const int32_t n = ok ? count_of(j) : 0;
     // n >= k always holds (k experts reach theta); the test is a guard, not a path.
     const bool exact_sweep = ok && (n > cap || n < k);
+    const bool by_rank = RCAP > 0 && ok && !exact_sweep && n <= RCAP;  // same for the token's lanes
     if (sub == 0) over_flag[j] = exact_sweep;
     float v[K];
     int32_t ix[K];
     list_init<K>(v, ix);
     if (!exact_sweep && n > sub) {
-        const float* zp = z + (ok ? tok : 0) * R;
+        const float* zp = zrow_of(j);
         float zreg[R];
 #pragma unroll
         for (int i = 0; i < R; i += 4) {
@@ -1008,7 +1050,7 @@ __device__ __forceinline__ void finalize_tokens(const float* __restrict__ z,
             for (int jj = 0; jj < 4; ++jj) zreg[i + jj] = q[jj];
         }
         // Candidates sub, sub + 8, ...: FB per round, all their rows loaded before any is used.
-        constexpr int FB = RC <= 2 ? 4 : 2;
+        constexpr int FB = 2;
         for (int i0 = sub; i0 < n; i0 += 8 * FB) {
             int32_t e[FB];
             bf16x8 u[FB][2 * RC];
@@ -1023,27 +1065,61 @@ __device__ __forceinline__ void finalize_tokens(const float* __restrict__ z,
                 for (int c = 0; c < 2 * RC; ++c) u[b][c] = load_bf16x8(R2t + (int64_t)e[b] * R + 8 * c);
 #pragma unroll
             for (int b = 0; b < FB; ++b) {
-                // z . u_e in fp32, rank entries in increasing order (as exact_logit)
                 float l = 0.0f;
 #pragma unroll
                 for (int c = 0; c < 2 * RC; ++c)
 #pragma unroll
                     for (int q = 0; q < 8; ++q) l = fmaf(zreg[8 * c + q], (float)u[b][c][q], l);
-                if (i0 + 8 * b < n && better(l, e[b], v[K - 1], ix[K - 1]))
-                    list_insert<K>(v, ix, l, e[b]);
+                const int i = i0 + 8 * b;
+                if (i < n) {
+                    if (RCAP > 0 && by_rank) {
+                        lv[j * RCAP + i] = l;
+                        le[j * RCAP + i] = e[b];
+                    } else if (better(l, e[b], v[K - 1], ix[K - 1])) {
+                        list_insert<K>(v, ix, l, e[b]);
+                    }
+                }
             }
         }
     }
+    if (!by_rank) {  // list path
 #pragma unroll
-    for (int s = 1; s < 8; s <<= 1) list_merge_xor<K>(v, ix, s);
-    if (ok && sub == 0 && !exact_sweep) store_selection<K>(v, ix, k, tok, idx, gate, topval);
+        for (int s = 1; s < 8; s <<= 1) list_merge_xor<K>(v, ix, s);
+        if (ok && sub == 0 && !exact_sweep) store_selection<K>(v, ix, k, tok, idx, gate, topval);
+    }
+    if constexpr (RCAP > 0) {
+    __syncthreads();
+    if (by_rank) {
+        float lmax = -__builtin_huge_valf();  // the rank-0 logit
+        const float* lvj = lv + j * RCAP;
+        const int32_t* lej = le + j * RCAP;
+        for (int i = 0; i < n; ++i) lmax = fmaxf(lmax, lvj[i]);
+        for (int i = sub; i < n; i += 8) {
+            const float l = lvj[i];
+            const int32_t e = lej[i];
+            int rank = 0;
+            for (int i2 = 0; i2 < n; ++i2) rank += better(lvj[i2], lej[i2], l, e) ? 1 : 0;
+            if (rank < k) {
+                idx[tok * k + rank] = e;
+                if (topval) topval[tok * k + rank] = l;
+                ex[j][rank] = expf(l - lmax);
+            }
+        }
+    }
+    __syncthreads();
+    if (by_rank) {
+        float sum = 0.0f;  // in rank order, as store_selection
+        for (int i = 0; i < k; ++i) sum += ex[j][i];
+        for (int i = sub; i < k; i += 8) gate[tok * k + i] = ex[j][i] / sum;
+    }
+    }
     // Overflowed tokens (rare): the whole workgroup sweeps all experts, thread tid taking
     // experts tid, tid + NTHREADS, ...
     if (!__syncthreads_or(exact_sweep)) return;  // workgroup-uniform
     for (int jt = 0; jt < NTOK; ++jt) {
         if (!over_flag[jt]) continue;  // workgroup-uniform
         const int64_t t = tok0 + jt;
-        const float* zp = z + t * R;
+        const float* zp = zrow_of(jt);
         list_init<K>(v, ix);
         for (int32_t e = tid; e < M; e += NTHREADS) {
             const float l = exact_logit<RC>([&](int i) { return zp[i]; }, R2t + (int64_t)e * R);
@@ -1084,82 +1160,73 @@ __global__ __launch_bounds__(256) void finalize_kernel(
     int32_t k, const int32_t* __restrict__ count, const int32_t* __restrict__ cand, int32_t cap,
     int32_t* __restrict__ idx, float* __restrict__ gate, float* __restrict__ topval) {
     const int64_t tok0 = (int64_t)blockIdx.x * 32;
-    finalize_tokens<RC, K, 256>(
-        z, R2t, T, M, k, tok0, cap,
+    finalize_tokens<RC, K, 256, 0>(
+        [&](int j) __attribute__((always_inline)) {
+            return z + (tok0 + j < T ? tok0 + j : 0) * (16 * RC);
+        },
+        R2t, T, M, k, tok0, cap,
         [&](int j) __attribute__((always_inline)) { return count[tok0 + j]; },
         [&](int j, int i) __attribute__((always_inline)) { return cand[(tok0 + j) * cap + i]; },
-        idx, gate, topval);
+        nullptr, nullptr, idx, gate, topval);
 }
 
 // ------------------------------------------------------------------------------ fused route
 // One workgroup routes 64 tokens against the whole expert axis, for expert sets small enough
-// that every workgroup can read all of R2t from L2 twice: wave w sweeps tiles [Mt w / 8,
-// Mt (w + 1) / 8) for the workgroup's two token groups, with A operands loaded straight from
-// memory D tiles ahead (group norms copied to LDS first).  The screening pass, the threshold, the collect pass and the final
-// selection run in the workgroup with LDS for the exchanges, so one launch replaces the screen,
-// threshold, collect and finalize kernels (same screening bounds, same candidate guarantee, the
-// same exact evaluation: the result is bitwise identical to theirs).
+// that every workgroup can hold or re-read all of R2t: wave w sweeps tiles [Mt w / 8,
+// Mt (w + 1) / 8) for the workgroup's two token groups.  The screening pass, the threshold, the
+// collect pass and the final selection run in the workgroup with LDS for the exchanges, so one
+// launch replaces the screen, threshold, collect and finalize kernels (same screening bounds,
+// same candidate guarantee, same exact evaluation).
+//   fused_route_kernel  reads z, z_hi and the group norms written by the z pass and streams the
+//                       A operands from L2, D tiles ahead (r M <= 2^18);
+//   fused_local_kernel  also computes z for its tokens and the group norms of its tiles, and
+//                       keeps the A operands in registers for both passes (r M <= 2^17, K <= 8):
+//                       the whole routing call is one launch.  Its z sums the h axis in four
+//                       quarters (one per wave pair) added in order, so its logits may differ
+//                       from the z pass's in the last bits.
 constexpr int kFusedTokens = 64;
 constexpr int kFusedCap = 128;   // candidates per token
+constexpr int kFusedSlots = 8;   // slot entries per lane and token group in the collect pass
+constexpr int kFusedRankCap = 32;  // candidates per token selected by rank counting
 // A-operand ring depth (tiles loaded ahead), bounded by the registers at r = 64
 __host__ __device__ constexpr int fused_ring(int RC) { return RC == 2 ? 8 : (RC == 1 ? 4 : 2); }
 constexpr int kFusedMaxTiles = 512;  // expert tiles whose norms fit the LDS copy (M <= 16384)
+// Tiles per wave whose A operands stay in registers in the local kernel (128 registers at r <= 32
+// (r M <= 2^17), 64 at r = 64 (M <= 1024), next to the z pass operands).
+__host__ __device__ constexpr int fused_reg_tiles(int RC) { return RC == 4 ? 4 : 32 / RC; }
 
-// Tiles per wave whose A operands fit in 128 registers (REG variant: r M <= 2^17).
-__host__ __device__ constexpr int fused_reg_tiles(int RC) { return 32 / RC; }
+// LDS of the fused phases.
+template <int K>
+struct FusedLds {
+    float tops[kRouteWaves][kFusedTokens][K];  // per wave and token: K best bucket maxima
+    int32_t cand[kFusedTokens * kFusedCap];    // candidate lists
+    union {
+        uint32_t slots[kFusedSlots][2][kRouteThreads];  // collect pass
+        struct {                                        // final selection (rank path)
+            float lv[kFusedTokens][kFusedRankCap];
+            int32_t le[kFusedTokens][kFusedRankCap];
+        } fin;
+    };
+    float theta[kFusedTokens];
+    int32_t count[kFusedTokens];
+};
 
-template <int RC, int K, bool REG>
-__global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
-    const float* __restrict__ z, const uint16_t* __restrict__ zh, const float* __restrict__ cz,
-    const uint16_t* __restrict__ R2t, const float* __restrict__ gnorm, int32_t T, int32_t M,
-    int32_t k, int32_t* __restrict__ hist, int32_t* __restrict__ idx, float* __restrict__ gate,
-    float* __restrict__ topval) {
+// Screening pass, threshold, collect pass and final selection of a fused workgroup; run_sweep
+// (body) sweeps the wave's tiles for its two token groups (operands tg), zrow_of(j) is the fp32
+// z row of local token j.  Reached by every thread of the workgroup.
+template <int RC, int K, typename Sweep, typename ZRowOf>
+__device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroups<RC, 2>& tg,
+                                             FusedLds<K>& sh, ZRowOf&& zrow_of,
+                                             const uint16_t* __restrict__ R2t, int32_t T,
+                                             int32_t M, int32_t k, int64_t tok0,
+                                             int32_t* __restrict__ idx, float* __restrict__ gate,
+                                             float* __restrict__ topval) {
     using C = RouteCfg<RC, K>;
-    constexpr int L = C::L, TPW = 2;
-    __shared__ float tops[kRouteWaves][kFusedTokens][K];
-    __shared__ float theta_s[kFusedTokens];
-    __shared__ int32_t cnt_s[kFusedTokens];
-    __shared__ int32_t cand_s32[kFusedTokens * kFusedCap];
-    constexpr int S = 8;  // candidate slots per lane and token group during the collect pass
-    __shared__ uint16_t slots[S][TPW][kRouteThreads];
-    __shared__ __attribute__((aligned(16))) float gn[kFusedMaxTiles * 8];
+    constexpr int L = C::L, TPW = 2, S = kFusedSlots;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, half = lane >> 5;
-    const int64_t tok0 = (int64_t)blockIdx.x * kFusedTokens;
-    if (hist) {  // clear the per-expert histogram for this call
-        for (int64_t e = (int64_t)blockIdx.x * kRouteThreads + tid; e < M;
-             e += (int64_t)gridDim.x * kRouteThreads)
-            hist[e] = 0;
-    }
-    if (tid < kFusedTokens) cnt_s[tid] = 0;
-    const int64_t Mt = ((int64_t)M + 31) / 32;
-    for (int i = tid; i < (int)Mt * 8; i += kRouteThreads) gn[i] = gnorm[i];
-    __syncthreads();
-
-    TokenGroups<RC, TPW> tg;
-    tg.load(zh, cz, T, tok0, n, half);
-    const int64_t t0 = Mt * w / kRouteWaves, t1 = Mt * (w + 1) / kRouteWaves;
-    const GlobalRows<RC> src(R2t, gn, M, t0, n, half);
-    const int nt = (int)(t1 - t0);
-    const int32_t e00 = (int32_t)(t0 * 32);
-    // REG: the wave's A operands stay in registers for both passes (loaded once, here).
-    constexpr int NTW = REG ? fused_reg_tiles(RC) : 1;
-    bf16x8 areg[NTW][RC];
-    if constexpr (REG) {
-        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-            src.load_a(decltype(jj)::value < nt ? decltype(jj)::value : (nt > 0 ? nt - 1 : 0),
-                       areg[decltype(jj)::value]);
-        });
-    }
-    auto run_sweep = [&](auto&& body) __attribute__((always_inline)) {
-        if constexpr (REG)
-            sweep_regs<RC, K, TPW, NTW>(areg, gn + t0 * 8, nt, e00, M, half, tg.zhi, body);
-        else
-            sweep<RC, K, TPW, fused_ring(RC)>(src, nt, e00, M, half, tg.zhi, body);
-    };
-
     // Screening pass (as in screen_kernel): the wave's bucket maxima per token.
     {
         float bm[TPW][L];
@@ -1167,16 +1234,16 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
         for (int g = 0; g < TPW; ++g)
 #pragma unroll
             for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
-        run_sweep(
-            [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
-                __attribute__((always_inline)) {
-                constexpr int g = decltype(gg)::value;
-                constexpr int UB = 4 * decltype(u)::value;
-                (void)e0;
+        run_sweep([&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
+                      __attribute__((always_inline)) {
+                          constexpr int g = decltype(gg)::value;
+                          constexpr int UB = 4 * decltype(u)::value;
+                          (void)e0;
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    bm[g][UB + q] = fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
-            });
+                          for (int q = 0; q < 4; ++q)
+                              bm[g][UB + q] =
+                                  fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
+                      });
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
             sort_desc<L>(bm[g]);
@@ -1186,7 +1253,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
             vlist_merge<L>(bm[g], pb);
             if (half == 0) {
 #pragma unroll
-                for (int j = 0; j < K; ++j) tops[w][32 * g + n][j] = bm[g][j];
+                for (int j = 0; j < K; ++j) sh.tops[w][32 * g + n][j] = bm[g][j];
             }
         }
     }
@@ -1196,7 +1263,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
         const int jt = tid >> 3, sub = tid & 7;
         float v[K];
 #pragma unroll
-        for (int j = 0; j < K; ++j) v[j] = tops[sub][jt][j];
+        for (int j = 0; j < K; ++j) v[j] = sh.tops[sub][jt][j];
 #pragma unroll
         for (int s = 1; s < 8; s <<= 1) {
             float b[K];
@@ -1209,48 +1276,273 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
 #pragma unroll
             for (int j = 1; j < K; ++j)
                 if (j == k - 1) th = v[j];
-            theta_s[jt] = fmaxf(th - fabsf(th) * 0x1p-20f, -0x1p100f);
+            sh.theta[jt] = fmaxf(th - fabsf(th) * 0x1p-20f, -0x1p100f);
+            sh.count[jt] = 0;
         }
     }
     __syncthreads();
-    // Collect pass (as in collect_kernel): hits go to lane-private slots first, then into the
-    // token's LDS list with one reservation per lane (a lane with more than S hits overflows
-    // the token, which is then swept exactly).
+    // Collect pass (as in collect_kernel): entries go to lane-private slots first, then their
+    // experts into the token's LDS list with one reservation per lane (a lane with more than S
+    // entries overflows the token, which is then swept exactly).
     {
         int cnt[TPW];
-#pragma unroll
-        for (int g = 0; g < TPW; ++g) cnt[g] = 0;
         float th[TPW];
 #pragma unroll
-        for (int g = 0; g < TPW; ++g)  // tokens past T never qualify (+inf threshold)
-            th[g] = tg.tok_ok(g, n) ? theta_s[32 * g + n] : __builtin_huge_valf();
-        run_sweep(
-            [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
-                __attribute__((always_inline)) {
-                constexpr int g = decltype(gg)::value;
-                (void)u;
-                cnt[g] = collect_tile<S>(acc, th[g], tg.c[g], nq, e0 / 4 + half, cnt[g],
-                                         [&](int i) { return &slots[i][g][tid]; });
-            });
+        for (int g = 0; g < TPW; ++g) {
+            cnt[g] = 0;  // tokens past T never qualify (+inf threshold)
+            th[g] = tg.tok_ok(g, n) ? sh.theta[32 * g + n] : __builtin_huge_valf();
+        }
+        run_sweep([&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
+                      __attribute__((always_inline)) {
+                          constexpr int g = decltype(gg)::value;
+                          (void)u;
+                          cnt[g] = collect_tile16<S>(acc, th[g], tg.c[g], nq, e0 / 16 + half,
+                                                     cnt[g],
+                                                     [&](int i) { return &sh.slots[i][g][tid]; });
+                      });
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
             if (cnt[g] > 0) {
-                auto slot = [&](int i) { return &slots[i][g][tid]; };
                 const int tl = 32 * g + n;
-                const int ne = slot_experts<S>(cnt[g], slot, 0, M);
-                const int base = atomicAdd(&cnt_s[tl], cnt[g] > S ? kFusedCap + 1 : ne);
-                if (cnt[g] <= S && base < kFusedCap)
-                    slot_expand(cnt[g], slot, 0, M, cand_s32 + tl * kFusedCap + base,
-                                kFusedCap - base);
+                int ne = 0;
+                for (int i = 0; i < cnt[g] && i < S; ++i)
+                    ne += __builtin_popcount(entry16_bits(sh.slots[i][g][tid], M));
+                const int base = atomicAdd(&sh.count[tl], cnt[g] > S ? kFusedCap + 1 : ne);
+                if (cnt[g] <= S) {
+                    int o = base;
+                    for (int i = 0; i < cnt[g]; ++i) {
+                        const uint32_t v = sh.slots[i][g][tid];
+                        uint32_t m = entry16_bits(v, M);
+                        const int32_t e = (int32_t)(v >> 17) * 32 + 4 * (int32_t)((v >> 16) & 1);
+                        while (m) {
+                            const int b = __builtin_ctz(m);
+                            m &= m - 1;
+                            if (o < kFusedCap) sh.cand[tl * kFusedCap + o] = e + 8 * (b >> 2) + (b & 3);
+                            ++o;
+                        }
+                    }
+                }
             }
         }
     }
     __syncthreads();
-    finalize_tokens<RC, K, kRouteThreads>(
-        z, R2t, T, M, k, tok0, kFusedCap,
-        [&](int j) __attribute__((always_inline)) { return cnt_s[j]; },
-        [&](int j, int i) __attribute__((always_inline)) { return cand_s32[j * kFusedCap + i]; }, idx,
-        gate, topval);
+    finalize_tokens<RC, K, kRouteThreads, kFusedRankCap>(
+        zrow_of, R2t, T, M, k, tok0, kFusedCap,
+        [&](int j) __attribute__((always_inline)) { return sh.count[j]; },
+        [&](int j, int i) __attribute__((always_inline)) { return sh.cand[j * kFusedCap + i]; },
+        &sh.fin.lv[0][0], &sh.fin.le[0][0], idx, gate, topval);
+}
+
+template <int RC, int K>
+__global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
+    const float* __restrict__ z, const uint16_t* __restrict__ zh, const float* __restrict__ cz,
+    const uint16_t* __restrict__ R2t, const float* __restrict__ gnorm, int32_t T, int32_t M,
+    int32_t k, int32_t* __restrict__ hist, int32_t* __restrict__ idx, float* __restrict__ gate,
+    float* __restrict__ topval) {
+    constexpr int TPW = 2;
+    __shared__ FusedLds<K> sh;
+    __shared__ __attribute__((aligned(16))) float gn[kFusedMaxTiles * 8];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 31, half = lane >> 5;
+    const int64_t tok0 = (int64_t)blockIdx.x * kFusedTokens;
+    if (hist) {  // clear the per-expert histogram for this call
+        for (int64_t e = (int64_t)blockIdx.x * kRouteThreads + tid; e < M;
+             e += (int64_t)gridDim.x * kRouteThreads)
+            hist[e] = 0;
+    }
+    const int64_t Mt = ((int64_t)M + 31) / 32;
+    for (int i = tid; i < (int)Mt * 8; i += kRouteThreads) gn[i] = gnorm[i];
+    __syncthreads();
+
+    TokenGroups<RC, TPW> tg;
+    tg.load(zh, cz, T, tok0, n, half);
+    const int64_t t0 = Mt * w / kRouteWaves, t1 = Mt * (w + 1) / kRouteWaves;
+    const GlobalRows<RC> src(R2t, gn, M, t0, n, half);
+    const int nt = (int)(t1 - t0);
+    const int32_t e00 = (int32_t)(t0 * 32);
+    fused_phases<RC, K>(
+        [&](auto&& body) __attribute__((always_inline)) {
+            sweep<RC, K, TPW, fused_ring(RC)>(src, nt, e00, M, half, tg.zhi, body);
+        },
+        tg, sh,
+        [&](int j) __attribute__((always_inline)) {
+            return z + (tok0 + j < T ? tok0 + j : 0) * (16 * RC);
+        },
+        R2t, T, M, k, tok0, idx, gate, topval);
+}
+
+template <int RC, int K>
+__global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ R1t,
+    const uint16_t* __restrict__ R2t, int32_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+    int32_t* __restrict__ hist, int32_t* __restrict__ idx, float* __restrict__ gate,
+    float* __restrict__ topval) {
+    constexpr int R = 16 * RC, RT = (RC + 1) / 2, TPW = 2, NTW = fused_reg_tiles(RC);
+    constexpr int ZRED = 4 * 2 * RT * 64 * 16;  // floats: [h quarter][group][tile][lane][16]
+    constexpr int POOL = (int)sizeof(FusedLds<K>) > 4 * ZRED ? (int)sizeof(FusedLds<K>) : 4 * ZRED;
+    // The partial sums of z share their LDS with the later phases.
+    __shared__ __attribute__((aligned(16))) unsigned char pool[POOL];
+    FusedLds<K>& sh = *reinterpret_cast<FusedLds<K>*>(pool);
+    float* zred = reinterpret_cast<float*>(pool);
+    __shared__ __attribute__((aligned(16))) float zs[kFusedTokens * R];  // z rows, fp32
+    __shared__ float cs[kFusedTokens];                                   // screening scales
+    __shared__ __attribute__((aligned(16))) float gnw[kRouteWaves][NTW * 8];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 31, half = lane >> 5;
+    const int64_t tok0 = (int64_t)blockIdx.x * kFusedTokens;
+    if (hist) {  // clear the per-expert histogram for this call
+        for (int64_t e = (int64_t)blockIdx.x * kRouteThreads + tid; e < M;
+             e += (int64_t)gridDim.x * kRouteThreads)
+            hist[e] = 0;
+    }
+    // The wave's expert tiles, loaded first (they stay in registers for both passes).
+    const int64_t Mt = ((int64_t)M + 31) / 32;
+    const int64_t t0 = Mt * w / kRouteWaves, t1 = Mt * (w + 1) / kRouteWaves;
+    const int nt = (int)(t1 - t0);
+    const int32_t e00 = (int32_t)(t0 * 32);
+    const GlobalRows<RC> src(R2t, gnw[w], M, t0, n, half);
+    bf16x8 areg[NTW][RC];
+    unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+        constexpr int J = decltype(jj)::value;
+        src.load_a(J < nt ? J : (nt > 0 ? nt - 1 : 0), areg[J]);
+    });
+
+    // z = x R1 for the 64 tokens: wave w takes token group w & 1 and the h quarter w >> 1, in the
+    // MFMA layout of the z pass (rank rows permuted so that z lands in the B-operand layout).
+    {
+        const int zg = w & 1, hq = w >> 1;
+        const int S16 = h >> 4;
+        const int s0 = S16 * hq / 4, s1 = S16 * (hq + 1) / 4;
+        const int jm = n >> 3, qm = (n >> 2) & 1, im = n & 3;
+        const int prow = 16 * (jm >> 1) + 8 * qm + 4 * (jm & 1) + im;
+        const int64_t zt = tok0 + 32 * zg + n;
+        const uint16_t* xrow = x + (zt < T ? zt : T - 1) * (int64_t)h + 8 * half;
+        const uint16_t* r1row[RT];
+#pragma unroll
+        for (int pt = 0; pt < RT; ++pt) {
+            const int rr = 32 * pt + prow;
+            r1row[pt] = R1t + (int64_t)(rr < r ? rr : r - 1) * h + 8 * half;
+        }
+        f32x16 za[RT];
+#pragma unroll
+        for (int pt = 0; pt < RT; ++pt) za[pt] = zero_f32x16();
+        constexpr int ZD = 8;  // k-steps whose operands are loaded before they are used
+        for (int sb = s0; sb < s1; sb += ZD) {
+            bf16x8 xb[ZD], ab[ZD][RT];
+#pragma unroll
+            for (int i = 0; i < ZD; ++i) {
+                const int st = sb + i < s1 ? sb + i : s1 - 1;
+                xb[i] = load_bf16x8(xrow + 16 * st);
+#pragma unroll
+                for (int pt = 0; pt < RT; ++pt) ab[i][pt] = load_bf16x8(r1row[pt] + 16 * st);
+            }
+#pragma unroll
+            for (int i = 0; i < ZD; ++i)
+                if (sb + i < s1)
+#pragma unroll
+                    for (int pt = 0; pt < RT; ++pt) za[pt] = mfma_32x32x16(ab[i][pt], xb[i], za[pt]);
+        }
+#pragma unroll
+        for (int pt = 0; pt < RT; ++pt) {
+            f32x4* dst = reinterpret_cast<f32x4*>(zred + (((hq * 2 + zg) * RT + pt) * 64 + lane) * 16);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                dst[q] = f32x4{za[pt][4 * q], za[pt][4 * q + 1], za[pt][4 * q + 2], za[pt][4 * q + 3]};
+        }
+    }
+    __syncthreads();
+    if (w < 2) {
+        // The four quarters of token group w, added in order; z rows and screening scales
+        // (z_hi = bf16(z), z_lo = z - z_hi, as in the z pass) go to LDS.
+        const int zg = w;
+        const int jt = 32 * zg + n;
+        float hi2 = 0.0f, lo2 = 0.0f;
+#pragma unroll
+        for (int pt = 0; pt < RT; ++pt) {
+            f32x16 zsum;
+#pragma unroll
+            for (int hq = 0; hq < 4; ++hq) {
+                const f32x4* src4 =
+                    reinterpret_cast<const f32x4*>(zred + (((hq * 2 + zg) * RT + pt) * 64 + lane) * 16);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f32x4 v = src4[q];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        zsum[4 * q + i] = hq == 0 ? v[i] : zsum[4 * q + i] + v[i];
+                }
+            }
+#pragma unroll
+            for (int c2 = 0; c2 < 2; ++c2) {
+                const int c = 2 * pt + c2;
+                if (16 * c < r) {
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        const float v = zsum[8 * c2 + q];
+                        const float hf = (float)(__bf16)v;
+                        const float lf = v - hf;
+                        hi2 = fmaf(hf, hf, hi2);
+                        lo2 = fmaf(lf, lf, lo2);
+                        zs[jt * R + 16 * c + 8 * half + q] = v;
+                    }
+                }
+            }
+        }
+        hi2 += __shfl_xor(hi2, 32, kWave);
+        lo2 += __shfl_xor(lo2, 32, kWave);
+        if (half == 0) cs[jt] = screen_scale(lo2, hi2, r);
+    }
+    // Group norms of the wave's tiles (as group_norms), from the registers: a lane holds half
+    // of row n of each tile, the other half sits in lane n + 32.
+    unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+        constexpr int J = decltype(jj)::value;
+        if (J < nt) {  // wave-uniform
+            float ss = 0.0f;
+#pragma unroll
+            for (int c = 0; c < RC; ++c)
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const float v = (float)areg[J][c][q];
+                    ss = fmaf(v, v, ss);
+                }
+            ss += __shfl_xor(ss, 32, kWave);
+            ss = fmaxf(ss, __shfl_xor(ss, 1, kWave));
+            ss = fmaxf(ss, __shfl_xor(ss, 2, kWave));
+            const int32_t row = e00 + 32 * J + n;
+            if (half == 0 && (n & 3) == 0) {
+                const int g4 = n >> 2;
+                gnw[w][J * 8 + (g4 & 1) * 4 + (g4 >> 1)] =
+                    row + 3 < M ? sqrtf(ss) * (1.0f + 0x1p-20f) : kPhantomNorm;
+            }
+        }
+    });
+    __syncthreads();
+    TokenGroups<RC, TPW> tg;
+    tg.first = tok0;
+    tg.T = T;
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) {
+        const int jt = 32 * g + n;
+        const bool ok = tg.tok_ok(g, n);
+#pragma unroll
+        for (int c = 0; c < RC; ++c) {
+            bf16x8 v;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) v[q] = (__bf16)zs[jt * R + 16 * c + 8 * half + q];
+            tg.zhi[g][c] = ok ? v : zero_bf16x8();
+        }
+        tg.c[g] = ok ? cs[jt] : 0.0f;
+    }
+    fused_phases<RC, K>(
+        [&](auto&& body) __attribute__((always_inline)) {
+            sweep_regs<RC, K, TPW, NTW>(areg, gnw[w], nt, e00, M, half, tg.zhi, body);
+        },
+        tg, sh, [&](int j) __attribute__((always_inline)) { return zs + j * R; }, R2t, T, M, k,
+        tok0, idx, gate, topval);
 }
 
 // ------------------------------------------------------------------------------ planning
@@ -1272,6 +1564,9 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     // Library's choice on a small expert set (r M <= 2^18, i.e. R2t <= 512 KiB, read from L2 by
     // every workgroup twice): the fused route kernel.
     q.fused = m_chunks == 0 && (int64_t)r * M <= (1 << 18) && Mt <= kFusedMaxTiles;
+    // ... and when the wave's tiles fit in registers (r M <= 2^17) and K <= 8, the local kernel,
+    // which needs no z pass and no workspace.
+    q.local = q.fused && q.K <= 8 && (Mt + kRouteWaves - 1) / kRouteWaves <= fused_reg_tiles(q.RC);
     const int tokens_per_block = q.fused ? kFusedTokens : 32 * route_tpw(q.RC, q.K) * kRouteWaves;
     q.ntb = (int32_t)((T + tokens_per_block - 1) / tokens_per_block);
     const int64_t emax_tiles = (int64_t)kChunkBytes / (2 * r) / 32;
@@ -1336,7 +1631,7 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     off += route_ws * align256((size_t)T * sizeof(int32_t));
     q.off_cand = off;
     off += route_ws * align256((size_t)T * q.cap * sizeof(int32_t));
-    q.workspace_bytes = off;
+    q.workspace_bytes = q.local ? 0 : off;
     *p = q;
     return true;
 }
@@ -1370,18 +1665,7 @@ struct RouteArgs {
 template <int RC, int K>
 static void launch_route(const LowrankPlan& p, const RouteArgs& a, hipStream_t st) {
     if (p.fused) {
-        // A operands in registers when the wave's tiles fit (r M <= 2^17; K <= 8, where the
-        // bucket maxima leave room for them).
-        const int64_t Mt = ((int64_t)a.M + 31) / 32;
-        if constexpr (K <= 8) {
-            if ((Mt + kRouteWaves - 1) / kRouteWaves <= fused_reg_tiles(RC)) {
-                hipLaunchKernelGGL((fused_route_kernel<RC, K, true>), dim3((unsigned)p.ntb),
-                                   dim3(kRouteThreads), 0, st, a.z, a.zhi, a.cz, a.R2t, a.gnorm,
-                                   a.T, a.M, a.k, a.hist, a.idx, a.gate, a.topval);
-                return;
-            }
-        }
-        hipLaunchKernelGGL((fused_route_kernel<RC, K, false>), dim3((unsigned)p.ntb),
+        hipLaunchKernelGGL((fused_route_kernel<RC, K>), dim3((unsigned)p.ntb),
                            dim3(kRouteThreads), 0, st, a.z, a.zhi, a.cz, a.R2t, a.gnorm, a.T,
                            a.M, a.k, a.hist, a.idx, a.gate, a.topval);
         return;
@@ -1412,10 +1696,47 @@ static bool dispatch_route_k(const LowrankPlan& p, const RouteArgs& a, hipStream
     return false;
 }
 
+template <int RC, int K>
+static void launch_local(const LowrankPlan& p, const uint16_t* x, const uint16_t* R1t,
+                         const uint16_t* R2t, int64_t T, int32_t h, int32_t r, int32_t M,
+                         int32_t k, int32_t* hist, int32_t* idx, float* gate, float* topval,
+                         hipStream_t st) {
+    hipLaunchKernelGGL((fused_local_kernel<RC, K>), dim3((unsigned)p.ntb), dim3(kRouteThreads), 0,
+                       st, x, R1t, R2t, (int32_t)T, h, r, M, k, hist, idx, gate, topval);
+}
+
+template <int RC>
+static bool dispatch_local_k(const LowrankPlan& p, const uint16_t* x, const uint16_t* R1t,
+                             const uint16_t* R2t, int64_t T, int32_t h, int32_t r, int32_t M,
+                             int32_t k, int32_t* hist, int32_t* idx, float* gate, float* topval,
+                             hipStream_t st) {
+    switch (p.K) {
+        case 1: launch_local<RC, 1>(p, x, R1t, R2t, T, h, r, M, k, hist, idx, gate, topval, st);
+            return true;
+        case 2: launch_local<RC, 2>(p, x, R1t, R2t, T, h, r, M, k, hist, idx, gate, topval, st);
+            return true;
+        case 4: launch_local<RC, 4>(p, x, R1t, R2t, T, h, r, M, k, hist, idx, gate, topval, st);
+            return true;
+        case 8: launch_local<RC, 8>(p, x, R1t, R2t, T, h, r, M, k, hist, idx, gate, topval, st);
+            return true;
+    }
+    return false;
+}
+
 hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_t* R1t,
                           const uint16_t* R2t, int64_t T, int32_t h, int32_t r, int32_t M,
                           int32_t k, int32_t* idx, float* gate, float* topval, int32_t* counts,
                           void* workspace, hipStream_t st) {
+    if (p.local) {  // one launch, no workspace
+        bool ok = false;
+        switch (p.RC) {
+            case 1: ok = dispatch_local_k<1>(p, x, R1t, R2t, T, h, r, M, k, counts, idx, gate, topval, st); break;
+            case 2: ok = dispatch_local_k<2>(p, x, R1t, R2t, T, h, r, M, k, counts, idx, gate, topval, st); break;
+            case 4: ok = dispatch_local_k<4>(p, x, R1t, R2t, T, h, r, M, k, counts, idx, gate, topval, st); break;
+        }
+        if (!ok) return hipErrorInvalidValue;
+        return hipGetLastError();
+    }
     char* ws = static_cast<char*>(workspace);
     float* zparts = reinterpret_cast<float*>(ws + p.off_zparts);
     RouteArgs a;

@@ -123,20 +123,39 @@ def test_expert_chunking_is_bitwise_identical(chunks):
     _check(inp, 8, base[0], base[1], base[2], label="chunks")
 
 
-@pytest.mark.parametrize("shape", [(16384, 512, 32, 4096, 8), (300, 96, 64, 4100, 16),
-                                   (77, 64, 16, 1000, 5), (129, 128, 32, 33, 1)],
+@pytest.mark.parametrize("shape", [(300, 96, 32, 8000, 8), (200, 64, 16, 2000, 16),
+                                   (129, 128, 64, 3000, 4)],
                          ids=lambda s: "T%d_h%d_r%d_M%d_k%d" % s)
 def test_fused_route_matches_resident_route_bitwise(shape):
-    # m_chunks=0 picks the one-kernel fused route on these small expert sets; m_chunks=1 forces
-    # the expert-resident route (screen, threshold, collect and finalize kernels).
+    # m_chunks=0 picks the fused route kernel (fed by the z pass) on these expert sets;
+    # m_chunks=1 forces the expert-resident route (screen, threshold, collect, finalize kernels).
     T, h, r, M, k = shape
     inp = make_inputs(T, h, r, M, seed=T + 3 * M)
     fused = route_lowrank(inp, k, histogram=True, tag="fused")
     resident = route_lowrank(inp, k, histogram=True, m_chunks=1, tag="resident")
     for a, b in zip(fused, resident):
         assert np.array_equal(a, b)
+    _check(inp, k, fused[0], fused[1], fused[2], label="fused %s" % (shape,))
+
+
+@pytest.mark.parametrize("shape", [(16384, 512, 32, 4096, 8), (77, 64, 16, 1000, 5),
+                                   (129, 128, 32, 33, 1), (500, 208, 64, 1000, 8)],
+                         ids=lambda s: "T%d_h%d_r%d_M%d_k%d" % s)
+def test_local_route_matches_resident_route(shape):
+    # m_chunks=0 picks the one-launch local kernel here (z computed in the workgroup, h summed in
+    # four quarters): the same selections as the resident route, logits equal to rounding.
+    T, h, r, M, k = shape
+    inp = make_inputs(T, h, r, M, seed=T + 5 * M)
+    local = route_lowrank(inp, k, histogram=True, tag="local")
+    resident = route_lowrank(inp, k, histogram=True, m_chunks=1, tag="resident")
+    same = np.all(local[0] == resident[0], axis=1)
+    assert same.mean() >= 0.999, same.mean()
+    scale = np.abs(resident[2][same]).max() + 1.0
+    assert np.abs(local[2][same] - resident[2][same]).max() <= 1e-5 * scale
+    assert np.abs(local[1][same] - resident[1][same]).max() <= 1e-5
     rows = None if T <= 4096 else _sample_rows(T, 512, seed=5)
-    _check(inp, k, fused[0], fused[1], fused[2], rows=rows, label="fused %s" % (shape,))
+    _check(inp, k, local[0], local[1], local[2], rows=rows, label="local %s" % (shape,))
+    assert np.array_equal(local[3], oracle.histogram(local[0], M).astype(np.int32))
 
 
 def test_repeat_runs_bitwise_identical():
