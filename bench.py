@@ -47,6 +47,9 @@ SCOPE_RESIDENT = ("one routing call: the z pass, screen, threshold, collect and 
                   "kernels (+ histogram), timed together as one step")
 SCOPE_FUSED = ("one routing call: the z pass and the fused route kernel (screen, threshold, "
                "collect and finalize in one launch) (+ histogram), timed together as one step")
+SCOPE_LOCAL = ("one routing call: one launch of the local fused kernel (z pass, group norms, "
+               "screen, threshold, collect and finalize) (+ histogram)")
+SCOPES = {"expert-resident": SCOPE_RESIDENT, "fused": SCOPE_FUSED, "fused-local": SCOPE_LOCAL}
 
 
 def roofline(w, seconds, scope):
@@ -174,7 +177,10 @@ def main():
 
     sec = timed_graph(step, args.steps, args.warmup)
     plan_chunks = router.lowrank_plan(w.T, w.h, w.r, w.M, w.k)
-    route = "fused" if plan_chunks == 0 else "expert-resident"
+    route = "expert-resident"
+    if plan_chunks == 0:  # fused; the local variant needs no workspace
+        local = router.lowrank_workspace_size(w.T, w.h, w.r, w.M, w.k) == 0
+        route = "fused-local" if local else "fused"
 
     result = {
         "metric": METRIC,
@@ -192,7 +198,7 @@ def main():
         "config": {"workload": w.name, "T": w.T, "h": w.h, "r": w.r, "M": w.M, "k": w.k,
                    "histogram": w.histogram, "route": route, "expert_chunks": plan_chunks,
                    "rotating_batches": nbuf, "launch": "hip graph of the timed steps"},
-        "roofline": roofline(w, sec, SCOPE_FUSED if route == "fused" else SCOPE_RESIDENT),
+        "roofline": roofline(w, sec, SCOPES[route]),
     }
 
     if not args.no_fullrank:

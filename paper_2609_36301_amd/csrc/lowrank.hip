@@ -1,17 +1,18 @@
 // Low-rank router kernels for gfx950: softmax(TopK(x R1 R2)) without materialising the
 // T x M logits (Appendix "Pseudocode", inference algorithm; MoRE layer in "Preliminaries").
 //
-// Pipeline of one call:
-//   zpass    z = x R1 (fp32 accumulate) for 128-token blocks; the h axis may be split over
-//            several workgroups (hsplit > 1), each writing a partial z;
-//   zreduce  sums the partials in a fixed order (only when hsplit > 1);
-//   route    for a block of 32*NW tokens and a chunk of the expert axis: logits
-//            z R2 tile by tile on the matrix cores (expert rows streamed through LDS),
-//            a screening sweep that fixes a per-token candidate threshold, an exact sweep
-//            that collects the candidates, and a per-token top-K of them; the block
-//            either writes the final (idx, gate, topval) or, when the expert axis is
-//            split into chunks, a partial top-K list per token;
-//   merge    (chunks > 1) merges the chunk lists of each token and writes the result.
+// Routes of one call (chosen per shape by lowrank_make_plan):
+//   expert-resident  zpass (z = x R1, fp32, and the group norms of R2t's rows) [+ zreduce when
+//                    the h axis is split over workgroups for small T], then screen, threshold,
+//                    collect and finalize kernels; screen and collect workgroups hold one chunk
+//                    of the expert axis in LDS;
+//   fused            zpass, then one fused_route_kernel: a workgroup of 64 tokens sweeps the
+//                    whole expert axis (operands streamed from L2) through the same four steps;
+//   local            one fused_local_kernel: the fused workgroup also computes z and the group
+//                    norms, and keeps its expert rows in registers.
+// The steps: screening bounds on z_hi = bf16(z) give a per-token threshold that k experts
+// provably reach, the candidates above it are collected, and their logits are evaluated exactly
+// in fp32 for the final top k (see the route section).
 //
 // MFMA layout.  Every contraction uses v_mfma_f32_32x32x16_bf16 with experts (or rank
 // rows) on the 32 A rows and tokens on the 32 B columns.  A lane therefore owns one token
