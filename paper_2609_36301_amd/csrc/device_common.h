@@ -11,6 +11,7 @@
 namespace more {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -147,15 +148,54 @@ __device__ __forceinline__ void list_merge(float (&av)[K], int32_t (&ai)[K], con
     }
 }
 
-// Merge with the list held by lane (lane ^ mask) of the same wave.
-template <int K>
-__device__ __forceinline__ void list_merge_xor(float (&v)[K], int32_t (&ix)[K], int mask) {
+// ---------------------------------------------------------------- cross-lane moves
+// The value of x held by lane (lane ^ M).  M = 1 and 2 are DPP quad permutations, M = 4 a
+// half-row mirror followed by a quad reversal (lane i of an 8-lane group reads 7 - (i ^ 3) =
+// i ^ 4); these stay in the VALU instead of going through the LDS crossbar of a general
+// shuffle.  Other M use __shfl_xor.
+template <int M, typename T>
+__device__ __forceinline__ T lane_xor(T x) {
+    static_assert(sizeof(T) == 4, "32-bit values only");
+    const int v = __builtin_bit_cast(int, x);
+    int r;
+    if constexpr (M == 1) {
+        r = __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);  // quad_perm [1,0,3,2]
+    } else if constexpr (M == 2) {
+        r = __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);  // quad_perm [2,3,0,1]
+    } else if constexpr (M == 4) {
+        const int h = __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);  // row_half_mirror
+        r = __builtin_amdgcn_mov_dpp(h, 0x1B, 0xF, 0xF, false);             // quad_perm [3,2,1,0]
+    } else {
+        r = __shfl_xor(v, M, kWave);
+    }
+    return __builtin_bit_cast(T, r);
+}
+
+// The values of x in lane l and in lane l ^ 32, in some order (both lanes of a pair get the
+// same two values): one gfx950 permlane32 swap, for symmetric combinations (sums, merges).
+__device__ __forceinline__ void lane_pair32(float x, float& a, float& b) {
+    const unsigned v = __builtin_bit_cast(unsigned, x);
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    a = __builtin_bit_cast(float, (unsigned)r[0]);
+    b = __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
+// x plus its value in lane l ^ 32.
+__device__ __forceinline__ float sum_pair32(float x) {
+    float a, b;
+    lane_pair32(x, a, b);
+    return a + b;
+}
+
+// Merge with the list held by lane (lane ^ M) of the same wave.
+template <int M, int K>
+__device__ __forceinline__ void list_merge_xor(float (&v)[K], int32_t (&ix)[K]) {
     float pv[K];
     int32_t pi[K];
 #pragma unroll
     for (int j = 0; j < K; ++j) {
-        pv[j] = __shfl_xor(v[j], mask, kWave);
-        pi[j] = __shfl_xor(ix[j], mask, kWave);
+        pv[j] = lane_xor<M>(v[j]);
+        pi[j] = lane_xor<M>(ix[j]);
     }
     list_merge<K>(v, ix, pv, pi);
 }

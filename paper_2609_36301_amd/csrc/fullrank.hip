@@ -47,7 +47,12 @@ __global__ __launch_bounds__(256) void rows_topk_kernel(const void* __restrict__
             if (x > v[K - 1]) list_insert_newer<K>(v, ix, x, e);
         }
     }
-    for (int s = 1; s < 64; s <<= 1) list_merge_xor<K>(v, ix, s);
+    list_merge_xor<1, K>(v, ix);
+    list_merge_xor<2, K>(v, ix);
+    list_merge_xor<4, K>(v, ix);
+    list_merge_xor<8, K>(v, ix);
+    list_merge_xor<16, K>(v, ix);
+    list_merge_xor<32, K>(v, ix);
     if (lane == 0) store_selection<K>(v, ix, k, row, idx, gate, topval);
 }
 

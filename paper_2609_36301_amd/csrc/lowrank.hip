@@ -809,9 +809,9 @@ __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
             sort_desc<L>(bm[g]);
-            float pb[L];
+            float pb[L];  // the two lanes' lists (merging is symmetric)
 #pragma unroll
-            for (int b = 0; b < L; ++b) pb[b] = __shfl_xor(bm[g][b], 32, kWave);
+            for (int b = 0; b < L; ++b) lane_pair32(bm[g][b], bm[g][b], pb[b]);
             vlist_merge<L>(bm[g], pb);
             if (half == 0 && tg.tok_ok(g, n)) {
                 float* o = top + ((int64_t)sp.chunk * T + tg.tok(g, n)) * K;
@@ -1084,8 +1084,9 @@ __device__ __forceinline__ void finalize_tokens(ZRowOf&& zrow_of,
         }
     }
     if (!by_rank) {  // list path
-#pragma unroll
-        for (int s = 1; s < 8; s <<= 1) list_merge_xor<K>(v, ix, s);
+        list_merge_xor<1, K>(v, ix);
+        list_merge_xor<2, K>(v, ix);
+        list_merge_xor<4, K>(v, ix);
         if (ok && sub == 0 && !exact_sweep) store_selection<K>(v, ix, k, tok, idx, gate, topval);
     }
     if constexpr (RCAP > 0) {
@@ -1126,8 +1127,12 @@ __device__ __forceinline__ void finalize_tokens(ZRowOf&& zrow_of,
             const float l = exact_logit<RC>([&](int i) { return zp[i]; }, R2t + (int64_t)e * R);
             if (better(l, e, v[K - 1], ix[K - 1])) list_insert<K>(v, ix, l, e);
         }
-#pragma unroll
-        for (int s = 1; s < 64; s <<= 1) list_merge_xor<K>(v, ix, s);
+        list_merge_xor<1, K>(v, ix);
+        list_merge_xor<2, K>(v, ix);
+        list_merge_xor<4, K>(v, ix);
+        list_merge_xor<8, K>(v, ix);
+        list_merge_xor<16, K>(v, ix);
+        list_merge_xor<32, K>(v, ix);
         if ((tid & 63) == 0) {
 #pragma unroll
             for (int q = 0; q < K; ++q) {
@@ -1248,9 +1253,9 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
             sort_desc<L>(bm[g]);
-            float pb[L];
+            float pb[L];  // the two lanes' lists (merging is symmetric)
 #pragma unroll
-            for (int b = 0; b < L; ++b) pb[b] = __shfl_xor(bm[g][b], 32, kWave);
+            for (int b = 0; b < L; ++b) lane_pair32(bm[g][b], bm[g][b], pb[b]);
             vlist_merge<L>(bm[g], pb);
             if (half == 0) {
 #pragma unroll
@@ -1265,13 +1270,12 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
         float v[K];
 #pragma unroll
         for (int j = 0; j < K; ++j) v[j] = sh.tops[sub][jt][j];
-#pragma unroll
-        for (int s = 1; s < 8; s <<= 1) {
+        unroll<3>([&](auto ss) __attribute__((always_inline)) {
             float b[K];
 #pragma unroll
-            for (int j = 0; j < K; ++j) b[j] = __shfl_xor(v[j], s, kWave);
+            for (int j = 0; j < K; ++j) b[j] = lane_xor<(1 << decltype(ss)::value)>(v[j]);
             vlist_merge<K>(v, b);
-        }
+        });
         if (sub == 0) {
             float th = v[0];
 #pragma unroll
@@ -1493,34 +1497,47 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
                 }
             }
         }
-        hi2 += __shfl_xor(hi2, 32, kWave);
-        lo2 += __shfl_xor(lo2, 32, kWave);
+        hi2 = sum_pair32(hi2);
+        lo2 = sum_pair32(lo2);
         if (half == 0) cs[jt] = screen_scale(lo2, hi2, r);
     }
     // Group norms of the wave's tiles (as group_norms), from the registers: a lane holds half
-    // of row n of each tile, the other half sits in lane n + 32.
-    unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-        constexpr int J = decltype(jj)::value;
-        if (J < nt) {  // wave-uniform
+    // of row n of each tile, the other half sits in lane n + 32.  The squared sums use bf16 dot
+    // products; their rounding (a relative 2^-18 at most) is covered by the 2^-10 slack of c.
+    // All tiles' sums are formed before the cross-lane steps, which then overlap.
+    {
+        float ssn[NTW];
+        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+            constexpr int J = decltype(jj)::value;
             float ss = 0.0f;
 #pragma unroll
             for (int c = 0; c < RC; ++c)
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
-                    const float v = (float)areg[J][c][q];
-                    ss = fmaf(v, v, ss);
+                for (int q = 0; q < 8; q += 2) {
+                    const bf16x2 p = {areg[J][c][q], areg[J][c][q + 1]};
+                    ss = __builtin_amdgcn_fdot2_f32_bf16(p, p, ss, false);
                 }
-            ss += __shfl_xor(ss, 32, kWave);
-            ss = fmaxf(ss, __shfl_xor(ss, 1, kWave));
-            ss = fmaxf(ss, __shfl_xor(ss, 2, kWave));
+            ssn[J] = ss;
+        });
+        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+            constexpr int J = decltype(jj)::value;
+            ssn[J] = sum_pair32(ssn[J]);  // the whole row
+        });
+        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+            constexpr int J = decltype(jj)::value;
+            ssn[J] = fmaxf(ssn[J], lane_xor<1>(ssn[J]));  // the group's 4 rows
+            ssn[J] = fmaxf(ssn[J], lane_xor<2>(ssn[J]));
+        });
+        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+            constexpr int J = decltype(jj)::value;
             const int32_t row = e00 + 32 * J + n;
-            if (half == 0 && (n & 3) == 0) {
+            if (J < nt && half == 0 && (n & 3) == 0) {
                 const int g4 = n >> 2;
                 gnw[w][J * 8 + (g4 & 1) * 4 + (g4 >> 1)] =
-                    row + 3 < M ? sqrtf(ss) * (1.0f + 0x1p-20f) : kPhantomNorm;
+                    row + 3 < M ? sqrtf(ssn[J]) * (1.0f + 0x1p-20f) : kPhantomNorm;
             }
-        }
-    });
+        });
+    }
     __syncthreads();
     TokenGroups<RC, TPW> tg;
     tg.first = tok0;
