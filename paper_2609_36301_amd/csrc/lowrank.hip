@@ -612,24 +612,26 @@ __device__ __forceinline__ void sweep(const Src& src, int nt, int32_t e00, int32
 }
 
 // The same sweep over tiles whose A operands are held in registers (a[t] for tile t < nt <=
-// NTW, loaded by the caller) and whose norms sit in LDS (gn + 8 t + 4 half).  Tiles are fully
-// unrolled, so register indices are compile-time constants.
-template <int RC, int K, int TPW, int NTW, typename Body>
+// NTW, loaded by the caller).  The accumulator of token group g starts from cin[g] (the MFMA
+// adds it for free); with NQ the norms come from LDS (gn + 8 t + 4 half), otherwise nq is
+// zero.  Tiles are fully unrolled, so register indices are compile-time constants.
+template <int RC, int K, int TPW, int NTW, bool NQ, typename Body>
 __device__ __forceinline__ void sweep_regs(const bf16x8 (&a)[NTW][RC], const float* gn, int nt,
                                            int32_t e00, int32_t M, int half,
-                                           const bf16x8 (&zhi)[TPW][RC], Body&& body) {
+                                           const bf16x8 (&zhi)[TPW][RC],
+                                           const f32x16 (&cin)[TPW], Body&& body) {
     using C = RouteCfg<RC, K>;
     constexpr int H = TPW / 2;
     constexpr int U = C::U;
     f32x16 acc[TPW];
-    f32x4 nq[2];
+    f32x4 nq[2] = {f32x4{0.0f, 0.0f, 0.0f, 0.0f}, f32x4{0.0f, 0.0f, 0.0f, 0.0f}};
     auto mfmas = [&](auto jj, auto hh) __attribute__((always_inline)) {
         constexpr int J = decltype(jj)::value;
         constexpr int G0 = decltype(hh)::value * H;
 #pragma unroll
-        for (int g = G0; g < G0 + H; ++g) acc[g] = zero_f32x16();
+        for (int g = G0; g < G0 + H; ++g) acc[g] = mfma_32x32x16(a[J][0], zhi[g][0], cin[g]);
 #pragma unroll
-        for (int c = 0; c < RC; ++c)
+        for (int c = 1; c < RC; ++c)
 #pragma unroll
             for (int g = G0; g < G0 + H; ++g) acc[g] = mfma_32x32x16(a[J][c], zhi[g][c], acc[g]);
     };
@@ -647,7 +649,7 @@ __device__ __forceinline__ void sweep_regs(const bf16x8 (&a)[NTW][RC], const flo
     unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
         constexpr int J = decltype(jj)::value;
         if (J < nt) {  // wave-uniform
-            nq[J & 1] = *reinterpret_cast<const f32x4*>(gn + J * 8 + 4 * half);
+            if constexpr (NQ) nq[J & 1] = *reinterpret_cast<const f32x4*>(gn + J * 8 + 4 * half);
             mfmas(jj, I0{});
             if constexpr (J > 0) finish(std::integral_constant<int, J - 1>{}, I1{});
             mfmas(jj, I1{});
@@ -704,6 +706,30 @@ __device__ __forceinline__ int collect_tile16(const f32x16& acc, float th, float
 #pragma unroll
         for (int i = 0; i < 4; ++i) m |= acc[4 * q + i] >= tq ? (1u << (4 * q + i)) : 0u;
     }
+    if (m) {
+        *slot(cnt < S ? cnt : S - 1) = ((uint32_t)code << 16) | m;
+        ++cnt;
+    }
+    return cnt;
+}
+
+// The same entry from an accumulator that already holds s_e + b, where b = c N_w - theta plus a
+// rounding guard was fed to the MFMA as its initial value (N_w bounds every row norm of the
+// wave): an element passes iff its sign bit is clear, and v_alignbit shifts the 16 sign bits
+// into a mask, one instruction per element.
+template <int S, typename Slot>
+__device__ __forceinline__ int collect_tile_sign(const f32x16& acc, int32_t code, int cnt,
+                                                 Slot&& slot) {
+    // (Each element is copied to a scalar first: a bit cast applied directly to a vector element
+    // reads element 0 with this compiler.)
+    const float a15 = acc[15];
+    uint32_t m = __builtin_bit_cast(uint32_t, a15) >> 31;
+#pragma unroll
+    for (int i = 14; i >= 0; --i) {
+        const float ai = acc[i];
+        m = __builtin_amdgcn_alignbit(m, __builtin_bit_cast(uint32_t, ai), 31);
+    }
+    m ^= 0xFFFFu;  // element i (bit i) passes iff acc[i] >= +0
     if (m) {
         *slot(cnt < S ? cnt : S - 1) = ((uint32_t)code << 16) | m;
         ++cnt;
@@ -1217,18 +1243,30 @@ struct FusedLds {
     int32_t count[kFusedTokens];
 };
 
-// Screening pass, threshold, collect pass and final selection of a fused workgroup; run_sweep
-// (body) sweeps the wave's tiles for its two token groups (operands tg), zrow_of(j) is the fp32
-// z row of local token j.  Reached by every thread of the workgroup.
-template <int RC, int K, typename Sweep, typename ZRowOf>
+// Screening pass, threshold, collect pass and final selection of a fused workgroup;
+// run_sweep(cin, body) sweeps the wave's tiles for its two token groups (operands tg, initial
+// accumulators cin), zrow_of(j) is the fp32 z row of local token j.  Reached by every thread of
+// the workgroup.
+//
+// Norm bounds.  With WN the wave uses one bound nw >= every row norm of its tiles instead of
+// the per-group norms (looser by c (nw - N_g), a few 1e-3 of a logit at unit-variance rows):
+//  - screen keeps bucket maxima of s itself (two v_max3 per 4-expert group) and subtracts c nw
+//    once at the end; rows past M (copies of row M - 1) are set to -inf first, in the one tile
+//    that has them, so that no bucket maximum is attained by a phantom row;
+//  - collect starts each accumulator at b = c nw - theta + guard, so the test s_e + c nw >=
+//    theta becomes the sign of the MFMA result (collect_tile_sign).  The guard (r + 2) 2^-23
+//    (|theta| + c nw) covers the rounding of b and the accumulation error that |b| adds to the
+//    MFMA sum (r + 1 terms, at most r 2^-24 relative each); the products' own accumulation
+//    error is inside c.  So every expert with l_e >= theta gets s_e + b >= +0.
+template <int RC, int K, bool WN, typename Sweep, typename ZRowOf>
 __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroups<RC, 2>& tg,
-                                             FusedLds<K>& sh, ZRowOf&& zrow_of,
+                                             float nw, FusedLds<K>& sh, ZRowOf&& zrow_of,
                                              const uint16_t* __restrict__ R2t, int32_t T,
                                              int32_t M, int32_t k, int64_t tok0,
                                              int32_t* __restrict__ idx, float* __restrict__ gate,
                                              float* __restrict__ topval) {
     using C = RouteCfg<RC, K>;
-    constexpr int L = C::L, TPW = 2, S = kFusedSlots;
+    constexpr int L = C::L, TPW = 2, S = kFusedSlots, R = 16 * RC;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1236,22 +1274,42 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
     // Screening pass (as in screen_kernel): the wave's bucket maxima per token.
     {
         float bm[TPW][L];
-#pragma unroll
-        for (int g = 0; g < TPW; ++g)
-#pragma unroll
-            for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
-        run_sweep([&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
-                      __attribute__((always_inline)) {
-                          constexpr int g = decltype(gg)::value;
-                          constexpr int UB = 4 * decltype(u)::value;
-                          (void)e0;
-#pragma unroll
-                          for (int q = 0; q < 4; ++q)
-                              bm[g][UB + q] =
-                                  fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
-                      });
+        f32x16 cz[TPW];
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
+            cz[g] = zero_f32x16();
+#pragma unroll
+            for (int b = 0; b < L; ++b) bm[g][b] = -__builtin_huge_valf();
+        }
+        run_sweep(cz, [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
+                          __attribute__((always_inline)) {
+                              constexpr int g = decltype(gg)::value;
+                              constexpr int UB = 4 * decltype(u)::value;
+                              if constexpr (WN) {
+                                  if (e0 + 32 > M) {  // wave-uniform: the tile reaching past M
+#pragma unroll
+                                      for (int i = 0; i < 16; ++i)
+                                          if (e0 + acc_row(i, half) >= M)
+                                              acc[i] = -__builtin_huge_valf();
+                                  }
+#pragma unroll
+                                  for (int q = 0; q < 4; ++q)
+                                      bm[g][UB + q] = fmaxf(fmaxf(fmaxf(bm[g][UB + q], acc[4 * q]),
+                                                                  acc[4 * q + 1]),
+                                                            fmaxf(acc[4 * q + 2], acc[4 * q + 3]));
+                              } else {
+#pragma unroll
+                                  for (int q = 0; q < 4; ++q)
+                                      bm[g][UB + q] =
+                                          fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
+                              }
+                          });
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            if constexpr (WN) {
+#pragma unroll
+                for (int b = 0; b < L; ++b) bm[g][b] = fmaf(-tg.c[g], nw, bm[g][b]);
+            }
             sort_desc<L>(bm[g]);
             float pb[L];  // the two lanes' lists (merging is symmetric)
 #pragma unroll
@@ -1292,19 +1350,33 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
     {
         int cnt[TPW];
         float th[TPW];
+        f32x16 cb[TPW];
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
-            cnt[g] = 0;  // tokens past T never qualify (+inf threshold)
-            th[g] = tg.tok_ok(g, n) ? sh.theta[32 * g + n] : __builtin_huge_valf();
+            cnt[g] = 0;  // tokens past T never qualify (+inf threshold, -inf start)
+            const bool ok = tg.tok_ok(g, n);
+            th[g] = ok ? sh.theta[32 * g + n] : __builtin_huge_valf();
+            float b = 0.0f;
+            if constexpr (WN) {
+                const float cn = tg.c[g] * nw;
+                b = fmaf(tg.c[g], nw, -th[g]) +
+                    (float)(R + 2) * 0x1p-23f * (fabsf(th[g]) + cn);
+                b = ok ? b : -__builtin_huge_valf();
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) cb[g][i] = b;
         }
-        run_sweep([&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
-                      __attribute__((always_inline)) {
-                          constexpr int g = decltype(gg)::value;
-                          (void)u;
-                          cnt[g] = collect_tile16<S>(acc, th[g], tg.c[g], nq, e0 / 16 + half,
-                                                     cnt[g],
-                                                     [&](int i) { return &sh.slots[i][g][tid]; });
-                      });
+        run_sweep(cb, [&](auto gg, f32x16& acc, int32_t e0, auto u, const f32x4& nq)
+                          __attribute__((always_inline)) {
+                              constexpr int g = decltype(gg)::value;
+                              (void)u;
+                              auto slot = [&](int i) { return &sh.slots[i][g][tid]; };
+                              if constexpr (WN)
+                                  cnt[g] = collect_tile_sign<S>(acc, e0 / 16 + half, cnt[g], slot);
+                              else
+                                  cnt[g] = collect_tile16<S>(acc, th[g], tg.c[g], nq,
+                                                             e0 / 16 + half, cnt[g], slot);
+                          });
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
             if (cnt[g] > 0) {
@@ -1367,11 +1439,11 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
     const GlobalRows<RC> src(R2t, gn, M, t0, n, half);
     const int nt = (int)(t1 - t0);
     const int32_t e00 = (int32_t)(t0 * 32);
-    fused_phases<RC, K>(
-        [&](auto&& body) __attribute__((always_inline)) {
+    fused_phases<RC, K, false>(
+        [&](const f32x16(&)[TPW], auto&& body) __attribute__((always_inline)) {
             sweep<RC, K, TPW, fused_ring(RC)>(src, nt, e00, M, half, tg.zhi, body);
         },
-        tg, sh,
+        tg, 0.0f, sh,
         [&](int j) __attribute__((always_inline)) {
             return z + (tok0 + j < T ? tok0 + j : 0) * (16 * RC);
         },
@@ -1393,7 +1465,6 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     float* zred = reinterpret_cast<float*>(pool);
     __shared__ __attribute__((aligned(16))) float zs[kFusedTokens * R];  // z rows, fp32
     __shared__ float cs[kFusedTokens];                                   // screening scales
-    __shared__ __attribute__((aligned(16))) float gnw[kRouteWaves][NTW * 8];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1409,7 +1480,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     const int64_t t0 = Mt * w / kRouteWaves, t1 = Mt * (w + 1) / kRouteWaves;
     const int nt = (int)(t1 - t0);
     const int32_t e00 = (int32_t)(t0 * 32);
-    const GlobalRows<RC> src(R2t, gnw[w], M, t0, n, half);
+    const GlobalRows<RC> src(R2t, nullptr, M, t0, n, half);  // A operands only
     bf16x8 areg[NTW][RC];
     unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
         constexpr int J = decltype(jj)::value;
@@ -1501,10 +1572,12 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
         lo2 = sum_pair32(lo2);
         if (half == 0) cs[jt] = screen_scale(lo2, hi2, r);
     }
-    // Group norms of the wave's tiles (as group_norms), from the registers: a lane holds half
-    // of row n of each tile, the other half sits in lane n + 32.  The squared sums use bf16 dot
-    // products; their rounding (a relative 2^-18 at most) is covered by the 2^-10 slack of c.
-    // All tiles' sums are formed before the cross-lane steps, which then overlap.
+    // The wave's norm bound nw >= the norm of every row of its tiles, from the registers: a lane
+    // holds half of row n of each tile, the other half sits in lane n + 32.  The squared sums use
+    // bf16 dot products; their rounding (a relative 2^-18 at most) is covered by the 2^-20 and
+    // 2^-10 slacks.  Tiles J >= nt hold copies of tile nt - 1, and rows past M copies of row
+    // M - 1, so they do not raise the bound.
+    float nw;
     {
         float ssn[NTW];
         unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
@@ -1519,24 +1592,17 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
                 }
             ssn[J] = ss;
         });
+        float mx = 0.0f;
         unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-            constexpr int J = decltype(jj)::value;
-            ssn[J] = sum_pair32(ssn[J]);  // the whole row
+            mx = fmaxf(mx, sum_pair32(ssn[decltype(jj)::value]));  // whole rows
         });
-        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-            constexpr int J = decltype(jj)::value;
-            ssn[J] = fmaxf(ssn[J], lane_xor<1>(ssn[J]));  // the group's 4 rows
-            ssn[J] = fmaxf(ssn[J], lane_xor<2>(ssn[J]));
-        });
-        unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-            constexpr int J = decltype(jj)::value;
-            const int32_t row = e00 + 32 * J + n;
-            if (J < nt && half == 0 && (n & 3) == 0) {
-                const int g4 = n >> 2;
-                gnw[w][J * 8 + (g4 & 1) * 4 + (g4 >> 1)] =
-                    row + 3 < M ? sqrtf(ssn[J]) * (1.0f + 0x1p-20f) : kPhantomNorm;
-            }
-        });
+        mx = fmaxf(mx, lane_xor<1>(mx));
+        mx = fmaxf(mx, lane_xor<2>(mx));
+        mx = fmaxf(mx, lane_xor<4>(mx));
+        mx = fmaxf(mx, lane_xor<8>(mx));
+        mx = fmaxf(mx, lane_xor<16>(mx));
+        nw = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                           __builtin_bit_cast(int, sqrtf(mx) * (1.0f + 0x1p-20f))));
     }
     __syncthreads();
     TokenGroups<RC, TPW> tg;
@@ -1555,11 +1621,11 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
         }
         tg.c[g] = ok ? cs[jt] : 0.0f;
     }
-    fused_phases<RC, K>(
-        [&](auto&& body) __attribute__((always_inline)) {
-            sweep_regs<RC, K, TPW, NTW>(areg, gnw[w], nt, e00, M, half, tg.zhi, body);
+    fused_phases<RC, K, true>(
+        [&](const f32x16(&cin)[TPW], auto&& body) __attribute__((always_inline)) {
+            sweep_regs<RC, K, TPW, NTW, false>(areg, nullptr, nt, e00, M, half, tg.zhi, cin, body);
         },
-        tg, sh, [&](int j) __attribute__((always_inline)) { return zs + j * R; }, R2t, T, M, k,
+        tg, nw, sh, [&](int j) __attribute__((always_inline)) { return zs + j * R; }, R2t, T, M, k,
         tok0, idx, gate, topval);
 }
 
