@@ -52,20 +52,69 @@ SCOPE_LOCAL = ("one routing call: one launch of the local fused kernel (z pass, 
 SCOPES = {"expert-resident": SCOPE_RESIDENT, "fused": SCOPE_FUSED, "fused-local": SCOPE_LOCAL}
 
 
+KERNEL_SOURCES = ("lowrank.hip", "lowrank.h", "device_common.h", "histogram.hip")
+
+
+def kernel_source_digest():
+    """sha256 over the sources of the routing kernels (a traffic record is valid only for them)."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_36301_amd", "csrc", name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(w):
+    """HBM bytes per routing call from the committed rocprofv3 counter summary of this workload.
+
+    The summary (profiles/route_<workload>_traffic.md) holds one line `traffic-record: {json}`
+    with FETCH_SIZE and WRITE_SIZE per dispatch (KiB, summed over the call's kernels) and the
+    scale factors that map each counter to true bytes on a plain copy kernel of known size.
+    Returns None when there is no record or when the kernel sources changed since it was taken.
+    """
+    path = os.path.join(ROOT, "profiles", "route_%s_traffic.md" % w.name)
+    if not os.path.exists(path):
+        return None
+    rec = None
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic-record:"):
+                rec = json.loads(line.split(":", 1)[1])
+    if not rec or rec.get("source_sha256") != kernel_source_digest():
+        return None
+    return int(round(1024 * (rec["fetch_kib_per_call"] * rec["fetch_scale"] +
+                             rec["write_kib_per_call"] * rec["write_scale"])))
+
+
 def roofline(w, seconds, scope):
     """Position of one routing call against max(flops / MFMA peak, bytes / HBM peak)."""
     nbytes, flops = algorithmic(w)
     t_hbm = nbytes / (PEAK_HBM_GBS * 1e9)
     t_mfma = flops / (PEAK_BF16_TFLOPS * 1e12)
+    traffic = measured_traffic(w)
     if t_hbm >= t_mfma:
         achieved = nbytes / seconds / 1e9
         return {"bound": "hbm", "achieved": round(achieved, 2), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": traffic,
                 "kernel": scope, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
     achieved = flops / seconds / 1e12
     return {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
-            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
             "kernel": scope, "algorithmic_bytes": nbytes, "algorithmic_flops": flops}
+
+
+def copy_calibration(nbytes):
+    """Runs a plain fp32 copy kernel (out = in * 1) over nbytes, for the counter scale factors."""
+    import torch
+    n = nbytes // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_kernel_bytes_read": 4 * n, "copy_kernel_bytes_written": 4 * n}),
+          flush=True)
 
 
 def timed(fn, steps, warmup, stream):
@@ -137,12 +186,18 @@ def main():
     ap.add_argument("--workload", default="teaser_prefill")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-fullrank", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain copy kernel of BYTES (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the router runs data-parallel over tokens, so "
               "each GPU routes its own token shard with no communication; --gpus %d is not "
               "supported" % args.gpus, file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
 
     import torch
     from paper_2609_36301_amd import router

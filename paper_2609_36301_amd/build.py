@@ -61,6 +61,13 @@ def build(verbose: bool = True) -> str:
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed: %s\n%s\n%s" % (" ".join(cmd), r.stdout, r.stderr))
+    # A kernel whose host stub was not emitted links but leaves an undefined symbol: load the
+    # library once (no GPU needed) so that the build fails here rather than at first use.
+    import ctypes
+    try:
+        ctypes.CDLL(tmp)
+    except OSError as e:
+        raise RuntimeError("built library does not load: %s" % e)
     os.replace(tmp, LIB)
     if verbose:
         print("built", LIB)

@@ -611,13 +611,14 @@ __device__ __forceinline__ void sweep(const Src& src, int nt, int32_t e00, int32
     });
 }
 
-// The same sweep over tiles whose A operands are held in registers (a[t] for tile t < nt <=
-// NTW, loaded by the caller).  The accumulator of token group g starts from cin[g] (the MFMA
-// adds it for free); with NQ the norms come from LDS (gn + 8 t + 4 half), otherwise nq is
-// zero.  Tiles are fully unrolled, so register indices are compile-time constants.
+// The same sweep over tiles whose A operands are held in registers (slot J < nt <= NTW holds
+// tile (J + rot) mod nt, loaded by the caller).  The accumulator of token group g starts from
+// cin[g] (the MFMA adds it for free); with NQ the norms come from LDS (gn + 8 t + 4 half),
+// otherwise nq is zero.  Slots are fully unrolled, so register indices are compile-time
+// constants; the bucket of slot J is J mod U.
 template <int RC, int K, int TPW, int NTW, bool NQ, typename Body>
 __device__ __forceinline__ void sweep_regs(const bf16x8 (&a)[NTW][RC], const float* gn, int nt,
-                                           int32_t e00, int32_t M, int half,
+                                           int rot, int32_t e00, int32_t M, int half,
                                            const bf16x8 (&zhi)[TPW][RC],
                                            const f32x16 (&cin)[TPW], Body&& body) {
     using C = RouteCfg<RC, K>;
@@ -640,7 +641,8 @@ __device__ __forceinline__ void sweep_regs(const bf16x8 (&a)[NTW][RC], const flo
         constexpr int G0 = decltype(hh)::value * H;
         unroll<H>([&](auto gg) __attribute__((always_inline)) {
             constexpr int G = G0 + decltype(gg)::value;
-            body(std::integral_constant<int, G>{}, acc[G], e00 + J * 32,
+            const int tj = J + rot < nt ? J + rot : J + rot - nt;  // the slot's tile
+            body(std::integral_constant<int, G>{}, acc[G], e00 + tj * 32,
                  std::integral_constant<int, J % U>{}, nq[J & 1]);
         });
     };
@@ -649,7 +651,10 @@ __device__ __forceinline__ void sweep_regs(const bf16x8 (&a)[NTW][RC], const flo
     unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
         constexpr int J = decltype(jj)::value;
         if (J < nt) {  // wave-uniform
-            if constexpr (NQ) nq[J & 1] = *reinterpret_cast<const f32x4*>(gn + J * 8 + 4 * half);
+            if constexpr (NQ) {
+                const int tj = J + rot < nt ? J + rot : J + rot - nt;
+                nq[J & 1] = *reinterpret_cast<const f32x4*>(gn + tj * 8 + 4 * half);
+            }
             mfmas(jj, I0{});
             if constexpr (J > 0) finish(std::integral_constant<int, J - 1>{}, I1{});
             mfmas(jj, I1{});
@@ -1223,6 +1228,19 @@ constexpr int kFusedRankCap = 32;  // candidates per token selected by rank coun
 // A-operand ring depth (tiles loaded ahead), bounded by the registers at r = 64
 __host__ __device__ constexpr int fused_ring(int RC) { return RC == 2 ? 8 : (RC == 1 ? 4 : 2); }
 constexpr int kFusedMaxTiles = 512;  // expert tiles whose norms fit the LDS copy (M <= 16384)
+// h values per LDS-staged chunk of the local kernel's z pass: (64 + r) rows of this many bf16
+// stay within 96 KiB.
+__host__ __device__ constexpr int local_zchunk(int RC) { return RC <= 2 ? 512 : 256; }
+// s_waitcnt immediate that waits until at most n vector memory operations are outstanding
+// (n < 64; expcnt and lgkmcnt not waited for).
+__host__ __device__ constexpr int vmcnt_imm(int n) {
+    return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8);
+}
+// Direct-to-LDS load of 16 bytes per lane: lane l of the wave writes lds + 16 l (lds must be
+// wave-uniform).  Completion is counted by vmcnt.
+__device__ __forceinline__ void lds_dma16(const void* g, void* lds) {
+    __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+}
 // Tiles per wave whose A operands stay in registers in the local kernel (128 registers at r <= 32
 // (r M <= 2^17), 64 at r = 64 (M <= 1024), next to the z pass operands).
 __host__ __device__ constexpr int fused_reg_tiles(int RC) { return RC == 4 ? 4 : 32 / RC; }
@@ -1458,7 +1476,10 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     float* __restrict__ topval) {
     constexpr int R = 16 * RC, RT = (RC + 1) / 2, TPW = 2, NTW = fused_reg_tiles(RC);
     constexpr int ZRED = 4 * 2 * RT * 64 * 16;  // floats: [h quarter][group][tile][lane][16]
-    constexpr int POOL = (int)sizeof(FusedLds<K>) > 4 * ZRED ? (int)sizeof(FusedLds<K>) : 4 * ZRED;
+    constexpr int ZHC = local_zchunk(RC);       // h per staged chunk
+    constexpr int STAGE = (kFusedTokens + R) * ZHC * 2;  // bytes: x rows, then R1t rows
+    constexpr int POOL0 = (int)sizeof(FusedLds<K>) > 4 * ZRED ? (int)sizeof(FusedLds<K>) : 4 * ZRED;
+    constexpr int POOL = POOL0 > STAGE ? POOL0 : STAGE;
     // The partial sums of z share their LDS with the later phases.
     __shared__ __attribute__((aligned(16))) unsigned char pool[POOL];
     FusedLds<K>& sh = *reinterpret_cast<FusedLds<K>*>(pool);
@@ -1475,52 +1496,104 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
              e += (int64_t)gridDim.x * kRouteThreads)
             hist[e] = 0;
     }
-    // The wave's expert tiles, loaded first (they stay in registers for both passes).
+    // The wave's expert tiles (they stay in registers for both passes).  Register slot J < nt
+    // holds tile (J + rot) mod nt of the wave's slice: the rotation by workgroup spreads the
+    // 32 CUs of an XCD that read the same R2t rows at once over the L2 channels.
     const int64_t Mt = ((int64_t)M + 31) / 32;
     const int64_t t0 = Mt * w / kRouteWaves, t1 = Mt * (w + 1) / kRouteWaves;
     const int nt = (int)(t1 - t0);
+    const int rot = nt > 0 ? (int)(blockIdx.x % (unsigned)nt) : 0;
     const int32_t e00 = (int32_t)(t0 * 32);
     const GlobalRows<RC> src(R2t, nullptr, M, t0, n, half);  // A operands only
     bf16x8 areg[NTW][RC];
-    unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-        constexpr int J = decltype(jj)::value;
-        src.load_a(J < nt ? J : (nt > 0 ? nt - 1 : 0), areg[J]);
-    });
 
-    // z = x R1 for the 64 tokens: wave w takes token group w & 1 and the h quarter w >> 1, in the
-    // MFMA layout of the z pass (rank rows permuted so that z lands in the B-operand layout).
+    // z = x R1 for the 64 tokens: wave w takes token group w & 1 and the h quarter w >> 1 of each
+    // staged chunk, in the MFMA layout of the z pass (rank rows permuted so that z lands in the
+    // B-operand layout).  The x rows and R1t rows of a chunk of ZHC h values are staged in LDS
+    // by direct-to-LDS loads, each instruction a contiguous 1 KiB of LDS filled from whole
+    // 128-byte lines (a B-operand load straight from memory touches 32 rows for 32 bytes each).
+    // In LDS, 16-byte segment s of row t sits at position s ^ (t & swm), so that the 32 rows of
+    // an operand read hit distinct banks.  The expert tiles are issued after the first chunk's
+    // loads; the chunk barrier then waits for the staged loads only (loads complete in order).
     {
         const int zg = w & 1, hq = w >> 1;
-        const int S16 = h >> 4;
-        const int s0 = S16 * hq / 4, s1 = S16 * (hq + 1) / 4;
         const int jm = n >> 3, qm = (n >> 2) & 1, im = n & 3;
         const int prow = 16 * (jm >> 1) + 8 * qm + 4 * (jm & 1) + im;
-        const int64_t zt = tok0 + 32 * zg + n;
-        const uint16_t* xrow = x + (zt < T ? zt : T - 1) * (int64_t)h + 8 * half;
-        const uint16_t* r1row[RT];
-#pragma unroll
-        for (int pt = 0; pt < RT; ++pt) {
-            const int rr = 32 * pt + prow;
-            r1row[pt] = R1t + (int64_t)(rr < r ? rr : r - 1) * h + 8 * half;
-        }
         f32x16 za[RT];
 #pragma unroll
         for (int pt = 0; pt < RT; ++pt) za[pt] = zero_f32x16();
-        constexpr int ZD = 8;  // k-steps whose operands are loaded before they are used
-        for (int sb = s0; sb < s1; sb += ZD) {
-            bf16x8 xb[ZD], ab[ZD][RT];
-#pragma unroll
-            for (int i = 0; i < ZD; ++i) {
-                const int st = sb + i < s1 ? sb + i : s1 - 1;
-                xb[i] = load_bf16x8(xrow + 16 * st);
-#pragma unroll
-                for (int pt = 0; pt < RT; ++pt) ab[i][pt] = load_bf16x8(r1row[pt] + 16 * st);
+        for (int h0 = 0; h0 < h; h0 += ZHC) {
+            const int hc = h - h0 < ZHC ? h - h0 : ZHC;  // multiple of 32
+            const int segs = hc >> 3;                     // 16-byte segments per row
+            const int swm = ((segs & -segs) < 32 ? (segs & -segs) : 32) - 1;
+            const int ns = (kFusedTokens + r) * segs;
+            // staging: LDS slot q = 512 i + 64 w + lane = row * segs + p
+            int row = tid / segs, p = tid - row * segs;
+            const int drow = kRouteThreads / segs, dp = kRouteThreads - drow * segs;
+            for (int q0 = 0; q0 < ns; q0 += kRouteThreads) {
+                if (q0 + tid < ns) {
+                    const int sg = p ^ (row & swm);
+                    const uint16_t* gp;
+                    if (row < kFusedTokens) {
+                        const int64_t t = tok0 + row < T ? tok0 + row : T - 1;
+                        gp = x + t * h + h0 + 8 * sg;
+                    } else {
+                        gp = R1t + (int64_t)(row - kFusedTokens) * h + h0 + 8 * sg;
+                    }
+                    lds_dma16(gp, pool + 16 * (q0 + 64 * w));
+                }
+                row += drow;
+                p += dp;
+                if (p >= segs) {
+                    p -= segs;
+                    ++row;
+                }
             }
+            if (h0 == 0) {
+                // Slot J < nt loads tile (J + rot) mod nt, slots past nt copies of tile nt - 1.
+                __builtin_amdgcn_sched_barrier(0);
+                unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
+                    constexpr int J = decltype(jj)::value;
+                    int tj = J < nt ? J + rot : nt - 1;
+                    tj = tj < nt ? tj : tj - nt;
+                    src.load_a(tj > 0 ? tj : 0, areg[J]);
+                });
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(NTW * RC));
+            } else {
+                __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+            }
+            __builtin_amdgcn_s_barrier();
+            const int S = hc >> 4;
+            const int s0 = S * hq / 4, s1 = S * (hq + 1) / 4;
+            const unsigned char* xr = pool + (32 * zg + n) * segs * 16;
+            const int xsw = (32 * zg + n) & swm;
+            const unsigned char* ar[RT];
+            int asw[RT];
 #pragma unroll
-            for (int i = 0; i < ZD; ++i)
-                if (sb + i < s1)
+            for (int pt = 0; pt < RT; ++pt) {
+                const int rr = 32 * pt + prow < r ? 32 * pt + prow : r - 1;
+                ar[pt] = pool + (kFusedTokens + rr) * segs * 16;
+                asw[pt] = (kFusedTokens + rr) & swm;
+            }
+            constexpr int ZD = 4;  // k-steps whose operands are read before they are used
+            for (int sb = s0; sb < s1; sb += ZD) {
+                bf16x8 xb[ZD], ab[ZD][RT];
 #pragma unroll
-                    for (int pt = 0; pt < RT; ++pt) za[pt] = mfma_32x32x16(ab[i][pt], xb[i], za[pt]);
+                for (int i = 0; i < ZD; ++i) {
+                    const int sg = 2 * (sb + i < s1 ? sb + i : s1 - 1) + half;
+                    xb[i] = *reinterpret_cast<const bf16x8*>(xr + 16 * (sg ^ xsw));
+#pragma unroll
+                    for (int pt = 0; pt < RT; ++pt)
+                        ab[i][pt] = *reinterpret_cast<const bf16x8*>(ar[pt] + 16 * (sg ^ asw[pt]));
+                }
+#pragma unroll
+                for (int i = 0; i < ZD; ++i)
+                    if (sb + i < s1)
+#pragma unroll
+                        for (int pt = 0; pt < RT; ++pt) za[pt] = mfma_32x32x16(ab[i][pt], xb[i], za[pt]);
+            }
+            __syncthreads();  // the chunk is consumed (the next one, or zred, reuses the LDS)
         }
 #pragma unroll
         for (int pt = 0; pt < RT; ++pt) {
@@ -1575,7 +1648,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     // The wave's norm bound nw >= the norm of every row of its tiles, from the registers: a lane
     // holds half of row n of each tile, the other half sits in lane n + 32.  The squared sums use
     // bf16 dot products; their rounding (a relative 2^-18 at most) is covered by the 2^-20 and
-    // 2^-10 slacks.  Tiles J >= nt hold copies of tile nt - 1, and rows past M copies of row
+    // 2^-10 slacks.  Slots past nt hold copies of tile nt - 1, and rows past M copies of row
     // M - 1, so they do not raise the bound.
     float nw;
     {
@@ -1623,7 +1696,8 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     }
     fused_phases<RC, K, true>(
         [&](const f32x16(&cin)[TPW], auto&& body) __attribute__((always_inline)) {
-            sweep_regs<RC, K, TPW, NTW, false>(areg, nullptr, nt, e00, M, half, tg.zhi, cin, body);
+            sweep_regs<RC, K, TPW, NTW, false>(areg, nullptr, nt, rot, e00, M, half, tg.zhi, cin,
+                                               body);
         },
         tg, nw, sh, [&](int j) __attribute__((always_inline)) { return zs + j * R; }, R2t, T, M, k,
         tok0, idx, gate, topval);
