@@ -1241,6 +1241,17 @@ __host__ __device__ constexpr int vmcnt_imm(int n) {
 __device__ __forceinline__ void lds_dma16(const void* g, void* lds) {
     __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
 }
+// Workgroup barrier for LDS data: waits for the wave's own LDS operations and, with vmcnt_left
+// < 64, until at most that many vector memory operations are outstanding (direct-to-LDS loads
+// complete in order with the others).  Unlike __syncthreads it does not drain the remaining
+// global loads.  The empty asm statements keep the compiler from moving memory accesses across.
+template <int VM = 63>
+__device__ __forceinline__ void lds_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(VM) & ~(15 << 8));  // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 // Tiles per wave whose A operands stay in registers in the local kernel (128 registers at r <= 32
 // (r M <= 2^17), 64 at r = 64 (M <= 1024), next to the z pass operands).
 __host__ __device__ constexpr int fused_reg_tiles(int RC) { return RC == 4 ? 4 : 32 / RC; }
@@ -1276,9 +1287,10 @@ struct FusedLds {
 //    (|theta| + c nw) covers the rounding of b and the accumulation error that |b| adds to the
 //    MFMA sum (r + 1 terms, at most r 2^-24 relative each); the products' own accumulation
 //    error is inside c.  So every expert with l_e >= theta gets s_e + b >= +0.
-template <int RC, int K, bool WN, typename Sweep, typename ZRowOf>
+template <int RC, int K, bool WN, typename Sweep, typename WaveNorm, typename ZRowOf>
 __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroups<RC, 2>& tg,
-                                             float nw, FusedLds<K>& sh, ZRowOf&& zrow_of,
+                                             WaveNorm&& wave_norm, FusedLds<K>& sh,
+                                             ZRowOf&& zrow_of,
                                              const uint16_t* __restrict__ R2t, int32_t T,
                                              int32_t M, int32_t k, int64_t tok0,
                                              int32_t* __restrict__ idx, float* __restrict__ gate,
@@ -1289,6 +1301,7 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, half = lane >> 5;
+    float nw = 0.0f;  // the wave's norm bound (WN), taken after the screening sweep
     // Screening pass (as in screen_kernel): the wave's bucket maxima per token.
     {
         float bm[TPW][L];
@@ -1322,6 +1335,7 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
                                           fmaxf(bm[g][UB + q], max4(acc, q) - tg.c[g] * nq[q]);
                               }
                           });
+        if constexpr (WN) nw = wave_norm();
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
             if constexpr (WN) {
@@ -1461,7 +1475,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_route_kernel(
         [&](const f32x16(&)[TPW], auto&& body) __attribute__((always_inline)) {
             sweep<RC, K, TPW, fused_ring(RC)>(src, nt, e00, M, half, tg.zhi, body);
         },
-        tg, 0.0f, sh,
+        tg, [] { return 0.0f; }, sh,
         [&](int j) __attribute__((always_inline)) {
             return z + (tok0 + j < T ? tok0 + j : 0) * (16 * RC);
         },
@@ -1506,6 +1520,17 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     const int32_t e00 = (int32_t)(t0 * 32);
     const GlobalRows<RC> src(R2t, nullptr, M, t0, n, half);  // A operands only
     bf16x8 areg[NTW][RC];
+    // Slot J < nt loads tile (J + rot) mod nt, slots past nt copies of tile nt - 1.  The first
+    // half of the slots is loaded during the z pass, the second half right before the screening
+    // sweep, whose first tiles then run while those loads complete.
+    auto load_tiles = [&](auto part) __attribute__((always_inline)) {
+        unroll<NTW / 2>([&](auto jj) __attribute__((always_inline)) {
+            constexpr int J = decltype(jj)::value + decltype(part)::value * (NTW / 2);
+            int tj = J < nt ? J + rot : nt - 1;
+            tj = tj < nt ? tj : tj - nt;
+            src.load_a(tj > 0 ? tj : 0, areg[J]);
+        });
+    };
 
     // z = x R1 for the 64 tokens: wave w takes token group w & 1 and the h quarter w >> 1 of each
     // staged chunk, in the MFMA layout of the z pass (rank rows permuted so that z lands in the
@@ -1550,20 +1575,13 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
                 }
             }
             if (h0 == 0) {
-                // Slot J < nt loads tile (J + rot) mod nt, slots past nt copies of tile nt - 1.
                 __builtin_amdgcn_sched_barrier(0);
-                unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-                    constexpr int J = decltype(jj)::value;
-                    int tj = J < nt ? J + rot : nt - 1;
-                    tj = tj < nt ? tj : tj - nt;
-                    src.load_a(tj > 0 ? tj : 0, areg[J]);
-                });
+                load_tiles(std::integral_constant<int, 0>{});
                 __builtin_amdgcn_sched_barrier(0);
-                __builtin_amdgcn_s_waitcnt(vmcnt_imm(NTW * RC));
+                lds_barrier<NTW / 2 * RC>();
             } else {
-                __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+                lds_barrier<0>();
             }
-            __builtin_amdgcn_s_barrier();
             const int S = hc >> 4;
             const int s0 = S * hq / 4, s1 = S * (hq + 1) / 4;
             const unsigned char* xr = pool + (32 * zg + n) * segs * 16;
@@ -1593,7 +1611,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
 #pragma unroll
                         for (int pt = 0; pt < RT; ++pt) za[pt] = mfma_32x32x16(ab[i][pt], xb[i], za[pt]);
             }
-            __syncthreads();  // the chunk is consumed (the next one, or zred, reuses the LDS)
+            lds_barrier();  // the chunk is consumed (the next one, or zred, reuses the LDS)
         }
 #pragma unroll
         for (int pt = 0; pt < RT; ++pt) {
@@ -1603,7 +1621,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
                 dst[q] = f32x4{za[pt][4 * q], za[pt][4 * q + 1], za[pt][4 * q + 2], za[pt][4 * q + 3]};
         }
     }
-    __syncthreads();
+    lds_barrier();  // (the expert tiles may still be in flight)
     if (w < 2) {
         // The four quarters of token group w, added in order; z rows and screening scales
         // (z_hi = bf16(z), z_lo = z - z_hi, as in the z pass) go to LDS.
@@ -1649,9 +1667,9 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     // holds half of row n of each tile, the other half sits in lane n + 32.  The squared sums use
     // bf16 dot products; their rounding (a relative 2^-18 at most) is covered by the 2^-20 and
     // 2^-10 slacks.  Slots past nt hold copies of tile nt - 1, and rows past M copies of row
-    // M - 1, so they do not raise the bound.
-    float nw;
-    {
+    // M - 1, so they do not raise the bound.  It is evaluated after the screening sweep, whose
+    // first tiles then need not wait for the last tiles' loads.
+    auto wave_norm = [&]() __attribute__((always_inline)) {
         float ssn[NTW];
         unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
             constexpr int J = decltype(jj)::value;
@@ -1674,10 +1692,12 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
         mx = fmaxf(mx, lane_xor<4>(mx));
         mx = fmaxf(mx, lane_xor<8>(mx));
         mx = fmaxf(mx, lane_xor<16>(mx));
-        nw = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
-                                           __builtin_bit_cast(int, sqrtf(mx) * (1.0f + 0x1p-20f))));
-    }
-    __syncthreads();
+        return __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
+                                             __builtin_bit_cast(int, sqrtf(mx) * (1.0f + 0x1p-20f))));
+    };
+    lds_barrier();
+    load_tiles(std::integral_constant<int, 1>{});
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(NTW / 2 * RC));  // the first half is in registers
     TokenGroups<RC, TPW> tg;
     tg.first = tok0;
     tg.T = T;
@@ -1699,8 +1719,8 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
             sweep_regs<RC, K, TPW, NTW, false>(areg, nullptr, nt, rot, e00, M, half, tg.zhi, cin,
                                                body);
         },
-        tg, nw, sh, [&](int j) __attribute__((always_inline)) { return zs + j * R; }, R2t, T, M, k,
-        tok0, idx, gate, topval);
+        tg, wave_norm, sh, [&](int j) __attribute__((always_inline)) { return zs + j * R; }, R2t, T,
+        M, k, tok0, idx, gate, topval);
 }
 
 // ------------------------------------------------------------------------------ planning
