@@ -139,7 +139,10 @@ def test_fused_route_matches_resident_route_bitwise(shape):
 
 
 @pytest.mark.parametrize("shape", [(16384, 512, 32, 4096, 8), (77, 64, 16, 1000, 5),
-                                   (129, 128, 32, 33, 1), (500, 208, 64, 1000, 8)],
+                                   (129, 128, 32, 33, 1), (500, 208, 64, 1000, 8),
+                                   # h staged in LDS over several chunks, the last one partial
+                                   (96, 1280, 16, 700, 6), (70, 1088, 64, 500, 8),
+                                   (130, 2080, 32, 3000, 4)],
                          ids=lambda s: "T%d_h%d_r%d_M%d_k%d" % s)
 def test_local_route_matches_resident_route(shape):
     # m_chunks=0 picks the one-launch local kernel here (z computed in the workgroup, h summed in
