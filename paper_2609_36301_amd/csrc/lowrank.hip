@@ -1121,29 +1121,71 @@ __device__ __forceinline__ void finalize_tokens(ZRowOf&& zrow_of,
         if (ok && sub == 0 && !exact_sweep) store_selection<K>(v, ix, k, tok, idx, gate, topval);
     }
     if constexpr (RCAP > 0) {
+    static_assert(RCAP % 8 == 0, "rank path: chunks of 8 entries");
     __syncthreads();
+    // The token's entries are read in chunks of 8 (two 16-byte LDS reads per array); chunks
+    // at or past the wave's largest candidate count are skipped (wave-uniform), entries past
+    // the token's own count are masked to -inf, which no candidate ranks below.
+    int nmx = by_rank ? n : 0;  // the 8 lanes of a token share n
+    nmx = max(nmx, lane_xor<8>(nmx));
+    nmx = max(nmx, lane_xor<16>(nmx));
+    nmx = max(nmx, lane_xor<32>(nmx));
+    const int nch = __builtin_amdgcn_readfirstlane((nmx + 7) >> 3);
+    float L[RCAP];
+    int32_t E[RCAP];
+    float lmax = -__builtin_huge_valf();  // the rank-0 logit
+    const float* lvj = lv + j * RCAP;
+    const int32_t* lej = le + j * RCAP;
+#pragma unroll
+    for (int c = 0; c < RCAP / 8; ++c) {
+        if (c < nch) {
+#pragma unroll
+            for (int h4 = 0; h4 < 2; ++h4) {
+                const f32x4 a = *reinterpret_cast<const f32x4*>(lvj + 8 * c + 4 * h4);
+                const i32x4 b = *reinterpret_cast<const i32x4*>(lej + 8 * c + 4 * h4);
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const int i = 8 * c + 4 * h4 + t;
+                    L[i] = i < n ? a[t] : -__builtin_huge_valf();
+                    E[i] = b[t];
+                    lmax = fmaxf(lmax, L[i]);
+                }
+            }
+        }
+    }
     if (by_rank) {
-        float lmax = -__builtin_huge_valf();  // the rank-0 logit
-        const float* lvj = lv + j * RCAP;
-        const int32_t* lej = le + j * RCAP;
-        for (int i = 0; i < n; ++i) lmax = fmaxf(lmax, lvj[i]);
-        for (int i = sub; i < n; i += 8) {
-            const float l = lvj[i];
-            const int32_t e = lej[i];
-            int rank = 0;
-            for (int i2 = 0; i2 < n; ++i2) rank += better(lvj[i2], lej[i2], l, e) ? 1 : 0;
-            if (rank < k) {
-                idx[tok * k + rank] = e;
-                if (topval) topval[tok * k + rank] = l;
-                ex[j][rank] = expf(l - lmax);
+#pragma unroll
+        for (int m = 0; m < RCAP / 8; ++m) {
+            const int i = sub + 8 * m;
+            if (m < nch && i < n) {
+                const float l = lvj[i];
+                const int32_t e = lej[i];
+                int rank = 0;
+#pragma unroll
+                for (int c = 0; c < RCAP / 8; ++c) {
+                    if (c < nch) {
+#pragma unroll
+                        for (int t = 0; t < 8; ++t)
+                            rank += better(L[8 * c + t], E[8 * c + t], l, e) ? 1 : 0;
+                    }
+                }
+                if (rank < k) {
+                    idx[tok * k + rank] = e;
+                    if (topval) topval[tok * k + rank] = l;
+                    ex[j][rank] = expf(l - lmax);
+                }
             }
         }
     }
     __syncthreads();
     if (by_rank) {
         float sum = 0.0f;  // in rank order, as store_selection
-        for (int i = 0; i < k; ++i) sum += ex[j][i];
-        for (int i = sub; i < k; i += 8) gate[tok * k + i] = ex[j][i] / sum;
+#pragma unroll
+        for (int i = 0; i < K; ++i)
+            if (i < k) sum += ex[j][i];
+#pragma unroll
+        for (int i = sub; i < K; i += 8)
+            if (i < k) gate[tok * k + i] = ex[j][i] / sum;
     }
     }
     // Overflowed tokens (rare): the whole workgroup sweeps all experts, thread tid taking
