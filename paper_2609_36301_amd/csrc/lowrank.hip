@@ -742,17 +742,29 @@ __device__ __forceinline__ int collect_tile_sign(const f32x16& acc, int32_t code
     return cnt;
 }
 
-// Experts of a 32-bit entry that exist (< M), as a 16-bit mask.
-__device__ __forceinline__ uint32_t entry16_bits(uint32_t v, int32_t M) {
-    const int32_t tile = (int32_t)(v >> 17), half = (int32_t)(v >> 16) & 1;
-    uint32_t m = v & 0xFFFFu;
-    if (tile * 32 + 32 > M) {  // last tile only
+// Masks of the accumulator elements of lane half 0 and 1 that hold experts < M in the last
+// tile (all ones when M is a multiple of 32): element b is row 8 (b >> 2) + 4 half + (b & 3).
+struct LastTileMask {
+    int32_t last;     // index of the last tile
+    uint32_t m[2];
+    __device__ __forceinline__ explicit LastTileMask(int32_t M) : last((M - 1) >> 5) {
+        const int32_t rows = M - 32 * last;  // 1 .. 32
 #pragma unroll
-        for (int b = 0; b < 16; ++b)
-            if (tile * 32 + 8 * (b >> 2) + 4 * half + (b & 3) >= M) m &= ~(1u << b);
+        for (int hf = 0; hf < 2; ++hf) {
+            uint32_t mm = 0;
+#pragma unroll
+            for (int b = 0; b < 16; ++b)
+                mm |= (8 * (b >> 2) + 4 * hf + (b & 3) < rows ? 1u : 0u) << b;
+            m[hf] = mm;
+        }
     }
-    return m;
-}
+    // Experts of a 32-bit entry that exist (< M), as a 16-bit mask.
+    __device__ __forceinline__ uint32_t bits(uint32_t v) const {
+        const int32_t tile = (int32_t)(v >> 17);
+        const uint32_t hm = (v >> 16) & 1u ? m[1] : m[0];
+        return v & (tile == last ? hm : 0xFFFFu);
+    }
+};
 
 // Number of experts in the first min(cnt, S) slot entries of a lane.
 template <int S, typename Slot>
@@ -1366,10 +1378,12 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
                                               acc[i] = -__builtin_huge_valf();
                                   }
 #pragma unroll
-                                  for (int q = 0; q < 4; ++q)
-                                      bm[g][UB + q] = fmaxf(fmaxf(fmaxf(bm[g][UB + q], acc[4 * q]),
-                                                                  acc[4 * q + 1]),
-                                                            fmaxf(acc[4 * q + 2], acc[4 * q + 3]));
+                                  for (int q = 0; q < 4; ++q) {  // two v_max3
+                                      const float t = fmaxf(fmaxf(bm[g][UB + q], acc[4 * q]),
+                                                            acc[4 * q + 1]);
+                                      bm[g][UB + q] =
+                                          fmaxf(fmaxf(t, acc[4 * q + 2]), acc[4 * q + 3]);
+                                  }
                               } else {
 #pragma unroll
                                   for (int q = 0; q < 4; ++q)
@@ -1451,26 +1465,39 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
                                   cnt[g] = collect_tile16<S>(acc, th[g], tg.c[g], nq,
                                                              e0 / 16 + half, cnt[g], slot);
                           });
+        // Expansion.  The lane's entries of both token groups are read at once (independent LDS
+        // reads), counted, reserved with one LDS atomic per group, then expanded.
+        const LastTileMask ltm(M);
+        uint32_t ent[TPW][S];
+#pragma unroll
+        for (int g = 0; g < TPW; ++g)
+#pragma unroll
+            for (int i = 0; i < S; ++i) ent[g][i] = i < cnt[g] ? sh.slots[i][g][tid] : 0u;
+        int base[TPW];
 #pragma unroll
         for (int g = 0; g < TPW; ++g) {
-            if (cnt[g] > 0) {
+            int ne = 0;
+#pragma unroll
+            for (int i = 0; i < S; ++i) ne += __builtin_popcount(ltm.bits(ent[g][i]));
+            base[g] = 0;
+            if (cnt[g] > 0)
+                base[g] = atomicAdd(&sh.count[32 * g + n], cnt[g] > S ? kFusedCap + 1 : ne);
+        }
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            if (cnt[g] > 0 && cnt[g] <= S) {
                 const int tl = 32 * g + n;
-                int ne = 0;
-                for (int i = 0; i < cnt[g] && i < S; ++i)
-                    ne += __builtin_popcount(entry16_bits(sh.slots[i][g][tid], M));
-                const int base = atomicAdd(&sh.count[tl], cnt[g] > S ? kFusedCap + 1 : ne);
-                if (cnt[g] <= S) {
-                    int o = base;
-                    for (int i = 0; i < cnt[g]; ++i) {
-                        const uint32_t v = sh.slots[i][g][tid];
-                        uint32_t m = entry16_bits(v, M);
-                        const int32_t e = (int32_t)(v >> 17) * 32 + 4 * (int32_t)((v >> 16) & 1);
-                        while (m) {
-                            const int b = __builtin_ctz(m);
-                            m &= m - 1;
-                            if (o < kFusedCap) sh.cand[tl * kFusedCap + o] = e + 8 * (b >> 2) + (b & 3);
-                            ++o;
-                        }
+                int o = base[g];
+#pragma unroll
+                for (int i = 0; i < S; ++i) {
+                    const uint32_t v = ent[g][i];
+                    uint32_t m = ltm.bits(v);  // 0 for i >= cnt
+                    const int32_t e = (int32_t)(v >> 17) * 32 + 4 * (int32_t)((v >> 16) & 1);
+                    while (m) {
+                        const int bt = __builtin_ctz(m);
+                        m &= m - 1;
+                        if (o < kFusedCap) sh.cand[tl * kFusedCap + o] = e + 8 * (bt >> 2) + (bt & 3);
+                        ++o;
                     }
                 }
             }
