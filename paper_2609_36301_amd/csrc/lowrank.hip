@@ -1568,7 +1568,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     FusedLds<K>& sh = *reinterpret_cast<FusedLds<K>*>(pool);
     float* zred = reinterpret_cast<float*>(pool);
     __shared__ __attribute__((aligned(16))) float zs[kFusedTokens * R];  // z rows, fp32
-    __shared__ float cs[kFusedTokens];                                   // screening scales
+    __shared__ float csp[kFusedTokens][4][2];  // shares of the squared norms of z_lo, z_hi
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1621,19 +1621,21 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
             const int segs = hc >> 3;                     // 16-byte segments per row
             const int swm = ((segs & -segs) < 32 ? (segs & -segs) : 32) - 1;
             const int ns = (kFusedTokens + r) * segs;
-            // staging: LDS slot q = 512 i + 64 w + lane = row * segs + p
+            // staging: LDS slot q = 512 i + 64 w + lane = row * segs + p; rows [0, 64) are x rows
+            // tok0 + row (clamped to T - 1), rows [64, 64 + r) R1t rows.  Row offsets times h fit
+            // a 24-bit multiply (h < 2^24, checked by the plan).
             int row = tid / segs, p = tid - row * segs;
             const int drow = kRouteThreads / segs, dp = kRouteThreads - drow * segs;
+            const int xlast = (int)(T - 1 - tok0 < kFusedTokens ? T - 1 - tok0 : kFusedTokens - 1);
+            const uint16_t* xb = x + tok0 * h + h0;
+            const uint16_t* rb = R1t + h0;
             for (int q0 = 0; q0 < ns; q0 += kRouteThreads) {
                 if (q0 + tid < ns) {
                     const int sg = p ^ (row & swm);
-                    const uint16_t* gp;
-                    if (row < kFusedTokens) {
-                        const int64_t t = tok0 + row < T ? tok0 + row : T - 1;
-                        gp = x + t * h + h0 + 8 * sg;
-                    } else {
-                        gp = R1t + (int64_t)(row - kFusedTokens) * h + h0 + 8 * sg;
-                    }
+                    const bool isx = row < kFusedTokens;
+                    const int roff = isx ? (row < xlast ? row : xlast) : row - kFusedTokens;
+                    const uint16_t* gp =
+                        (isx ? xb : rb) + __umul24((unsigned)roff, (unsigned)h) + 8 * sg;
                     lds_dma16(gp, pool + 16 * (q0 + 64 * w));
                 }
                 row += drow;
@@ -1691,46 +1693,43 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
         }
     }
     lds_barrier();  // (the expert tiles may still be in flight)
-    if (w < 2) {
-        // The four quarters of token group w, added in order; z rows and screening scales
-        // (z_hi = bf16(z), z_lo = z - z_hi, as in the z pass) go to LDS.
-        const int zg = w;
+    {
+        // The four h quarters of token group w & 1 added in order, by all 8 waves: wave w takes
+        // accumulator elements 4 (w >> 1) .. 4 (w >> 1) + 3 of each tile.  z rows go to LDS, and
+        // each wave's share of the token's squared norms of z_hi = bf16(z) and z_lo = z - z_hi
+        // (as in the z pass) to csp; the screening scale adds the four shares in order.
+        const int zg = w & 1, part = w >> 1;
         const int jt = 32 * zg + n;
+        const int c2 = part >> 1, q0 = 4 * (part & 1);
         float hi2 = 0.0f, lo2 = 0.0f;
 #pragma unroll
         for (int pt = 0; pt < RT; ++pt) {
-            f32x16 zsum;
+            const int c = 2 * pt + c2;
+            f32x4 zsum;
 #pragma unroll
             for (int hq = 0; hq < 4; ++hq) {
-                const f32x4* src4 =
-                    reinterpret_cast<const f32x4*>(zred + (((hq * 2 + zg) * RT + pt) * 64 + lane) * 16);
+                const f32x4 v = *reinterpret_cast<const f32x4*>(
+                    zred + (((hq * 2 + zg) * RT + pt) * 64 + lane) * 16 + 4 * part);
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const f32x4 v = src4[q];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        zsum[4 * q + i] = hq == 0 ? v[i] : zsum[4 * q + i] + v[i];
-                }
+                for (int i = 0; i < 4; ++i) zsum[i] = hq == 0 ? v[i] : zsum[i] + v[i];
             }
+            if (16 * c < r) {  // wave-uniform
 #pragma unroll
-            for (int c2 = 0; c2 < 2; ++c2) {
-                const int c = 2 * pt + c2;
-                if (16 * c < r) {
-#pragma unroll
-                    for (int q = 0; q < 8; ++q) {
-                        const float v = zsum[8 * c2 + q];
-                        const float hf = (float)(__bf16)v;
-                        const float lf = v - hf;
-                        hi2 = fmaf(hf, hf, hi2);
-                        lo2 = fmaf(lf, lf, lo2);
-                        zs[jt * R + 16 * c + 8 * half + q] = v;
-                    }
+                for (int i = 0; i < 4; ++i) {
+                    const float hf = (float)(__bf16)zsum[i];
+                    const float lf = zsum[i] - hf;
+                    hi2 = fmaf(hf, hf, hi2);
+                    lo2 = fmaf(lf, lf, lo2);
                 }
+                *reinterpret_cast<f32x4*>(&zs[jt * R + 16 * c + 8 * half + q0]) = zsum;
             }
         }
         hi2 = sum_pair32(hi2);
         lo2 = sum_pair32(lo2);
-        if (half == 0) cs[jt] = screen_scale(lo2, hi2, r);
+        if (half == 0) {
+            csp[jt][part][0] = lo2;
+            csp[jt][part][1] = hi2;
+        }
     }
     // The wave's norm bound nw >= the norm of every row of its tiles, from the registers: a lane
     // holds half of row n of each tile, the other half sits in lane n + 32.  The squared sums use
@@ -1781,7 +1780,9 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
             for (int q = 0; q < 8; ++q) v[q] = (__bf16)zs[jt * R + 16 * c + 8 * half + q];
             tg.zhi[g][c] = ok ? v : zero_bf16x8();
         }
-        tg.c[g] = ok ? cs[jt] : 0.0f;
+        const float lo2 = ((csp[jt][0][0] + csp[jt][1][0]) + csp[jt][2][0]) + csp[jt][3][0];
+        const float hi2 = ((csp[jt][0][1] + csp[jt][1][1]) + csp[jt][2][1]) + csp[jt][3][1];
+        tg.c[g] = ok ? screen_scale(lo2, hi2, r) : 0.0f;
     }
     fused_phases<RC, K, true>(
         [&](const f32x16(&cin)[TPW], auto&& body) __attribute__((always_inline)) {
@@ -1813,7 +1814,8 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     q.fused = m_chunks == 0 && (int64_t)r * M <= (1 << 18) && Mt <= kFusedMaxTiles;
     // ... and when the wave's tiles fit in registers (r M <= 2^17) and K <= 8, the local kernel,
     // which needs no z pass and no workspace.
-    q.local = q.fused && q.K <= 8 && (Mt + kRouteWaves - 1) / kRouteWaves <= fused_reg_tiles(q.RC);
+    q.local = q.fused && q.K <= 8 && (Mt + kRouteWaves - 1) / kRouteWaves <= fused_reg_tiles(q.RC) &&
+              h < (1 << 24);
     const int tokens_per_block = q.fused ? kFusedTokens : 32 * route_tpw(q.RC, q.K) * kRouteWaves;
     q.ntb = (int32_t)((T + tokens_per_block - 1) / tokens_per_block);
     const int64_t emax_tiles = (int64_t)kChunkBytes / (2 * r) / 32;
