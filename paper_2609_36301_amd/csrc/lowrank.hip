@@ -1751,10 +1751,13 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
                 }
             ssn[J] = ss;
         });
+        // Row n of tile J has squared norm a_J + b_J (this lane's half and lane n + 32's), at most
+        // max_J a_J + max_J b_J: one pair sum after the per-lane maximum.
         float mx = 0.0f;
         unroll<NTW>([&](auto jj) __attribute__((always_inline)) {
-            mx = fmaxf(mx, sum_pair32(ssn[decltype(jj)::value]));  // whole rows
+            mx = fmaxf(mx, ssn[decltype(jj)::value]);
         });
+        mx = sum_pair32(mx);
         mx = fmaxf(mx, lane_xor<1>(mx));
         mx = fmaxf(mx, lane_xor<2>(mx));
         mx = fmaxf(mx, lane_xor<4>(mx));
