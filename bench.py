@@ -47,8 +47,8 @@ SCOPE_RESIDENT = ("one routing call: the z pass, screen, threshold, collect and 
                   "kernels (+ histogram), timed together as one step")
 SCOPE_FUSED = ("one routing call: the z pass and the fused route kernel (screen, threshold, "
                "collect and finalize in one launch) (+ histogram), timed together as one step")
-SCOPE_LOCAL = ("one routing call: one launch of the local fused kernel (z pass, group norms, "
-               "screen, threshold, collect and finalize) (+ histogram)")
+SCOPE_LOCAL = ("one routing call: one launch of the local fused kernel (z pass, wave norm "
+               "bounds, screen, threshold, collect and finalize) (+ histogram)")
 SCOPES = {"expert-resident": SCOPE_RESIDENT, "fused": SCOPE_FUSED, "fused-local": SCOPE_LOCAL}
 
 
