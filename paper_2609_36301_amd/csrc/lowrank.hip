@@ -59,6 +59,7 @@ constexpr int kZWaves = 4;
 constexpr float kPhantomNorm = 0x1p100f;  // norm bound of a 4-expert group reaching past M
 constexpr int kZTokens = 32 * kZWaves;
 constexpr int kZChunk = 64;
+constexpr int kGroupNormBlocks = 4;  // 256-segment blocks per group-norm workgroup
 
 // Group norms: the largest Euclidean norm among expert rows 4g..4g+3 of R2t, rounded up, for
 // every group of the rows < `rows` (all tiles).  A group holding a row past M gets the norm bound
@@ -71,25 +72,34 @@ constexpr int kZChunk = 64;
 // r/8 segments of a row sit in consecutive lanes and the 4 rows of a group next to each other.
 template <int SPR>
 __device__ __forceinline__ void group_norms(const uint16_t* __restrict__ R2t, int32_t M,
-                                            int64_t rows, int64_t gid, float* __restrict__ gnorm) {
+                                            int64_t rows, int64_t gid0, float* __restrict__ gnorm) {
     constexpr int R = 8 * SPR;
-    const int64_t row = gid / SPR;
-    const int col = (int)(gid % SPR);
-    float ss = 0.0f;
-    if (row < M) {
-        const bf16x8 v = load_bf16x8(R2t + row * R + col * 8);
+    constexpr int NB = kGroupNormBlocks;  // segments gid0 + 256 b, all loaded before any is used
+    bf16x8 v[NB];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) ss = fmaf((float)v[q], (float)v[q], ss);
+    for (int b = 0; b < NB; ++b) {
+        const int64_t gid = gid0 + 256 * b;
+        const int64_t row = gid / SPR;
+        v[b] = row < M ? load_bf16x8(R2t + row * R + (gid % SPR) * 8) : zero_bf16x8();
     }
 #pragma unroll
-    for (int m = 1; m < SPR; m <<= 1) ss += __shfl_xor(ss, m, kWave);
-    ss = fmaxf(ss, __shfl_xor(ss, SPR, kWave));
-    ss = fmaxf(ss, __shfl_xor(ss, 2 * SPR, kWave));
-    if (col == 0 && (row & 3) == 0 && row < rows) {
-        // slot of group g4 = (row mod 32) / 4 = 2q + half of tile row / 32: [tile][half][q]
-        const int g4 = (int)(row & 31) >> 2;
-        gnorm[(row >> 5) * 8 + (g4 & 1) * 4 + (g4 >> 1)] =
-            row + 3 < M ? sqrtf(ss) * (1.0f + 0x1p-20f) : kPhantomNorm;
+    for (int b = 0; b < NB; ++b) {
+        const int64_t gid = gid0 + 256 * b;
+        const int64_t row = gid / SPR;
+        const int col = (int)(gid % SPR);
+        float ss = 0.0f;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) ss = fmaf((float)v[b][q], (float)v[b][q], ss);
+#pragma unroll
+        for (int m = 1; m < SPR; m <<= 1) ss += __shfl_xor(ss, m, kWave);
+        ss = fmaxf(ss, __shfl_xor(ss, SPR, kWave));
+        ss = fmaxf(ss, __shfl_xor(ss, 2 * SPR, kWave));
+        if (col == 0 && (row & 3) == 0 && row < rows) {
+            // slot of group g4 = (row mod 32) / 4 = 2q + half of tile row / 32: [tile][half][q]
+            const int g4 = (int)(row & 31) >> 2;
+            gnorm[(row >> 5) * 8 + (g4 & 1) * 4 + (g4 >> 1)] =
+                row + 3 < M ? sqrtf(ss) * (1.0f + 0x1p-20f) : kPhantomNorm;
+        }
     }
 }
 
@@ -106,7 +116,8 @@ __global__ __launch_bounds__(256) void zpass_kernel(const uint16_t* __restrict__
     // Workgroups [0, zblocks * hsplit) compute z (token block bx % zblocks, h split
     // bx / zblocks); the rest compute group norms.
     if ((int)blockIdx.x >= zblocks * hsplit) {  // workgroup-uniform: a group-norm workgroup
-        const int64_t gid = ((int64_t)blockIdx.x - (int64_t)zblocks * hsplit) * 256 + threadIdx.x;
+        const int64_t gid = ((int64_t)blockIdx.x - (int64_t)zblocks * hsplit) * 256 *
+                                kGroupNormBlocks + threadIdx.x;
         const int64_t rows = ((int64_t)M + 31) / 32 * 32;
         switch (r) {
             case 16: group_norms<2>(R2t, M, rows, gid, gnorm); break;
@@ -1244,21 +1255,25 @@ __device__ __forceinline__ void finalize_tokens(ZRowOf&& zrow_of,
 }
 
 // Final selection over the global candidate lists of the collect kernel, 32 tokens per
-// workgroup.
-template <int RC, int K>
+// workgroup.  With RCAP > 0 tokens with up to RCAP candidates take the rank-counting path:
+// shorter latency, chosen when there are few workgroups (small T); with many workgroups the
+// list path's fewer barriers and LDS round trips win.
+template <int RC, int K, int RCAP>
 __global__ __launch_bounds__(256) void finalize_kernel(
     const float* __restrict__ z, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
     int32_t k, const int32_t* __restrict__ count, const int32_t* __restrict__ cand, int32_t cap,
     int32_t* __restrict__ idx, float* __restrict__ gate, float* __restrict__ topval) {
+    __shared__ __attribute__((aligned(16))) float lv[32 * (RCAP > 0 ? RCAP : 1)];
+    __shared__ __attribute__((aligned(16))) int32_t le[32 * (RCAP > 0 ? RCAP : 1)];
     const int64_t tok0 = (int64_t)blockIdx.x * 32;
-    finalize_tokens<RC, K, 256, 0>(
+    finalize_tokens<RC, K, 256, RCAP>(
         [&](int j) __attribute__((always_inline)) {
             return z + (tok0 + j < T ? tok0 + j : 0) * (16 * RC);
         },
         R2t, T, M, k, tok0, cap,
         [&](int j) __attribute__((always_inline)) { return count[tok0 + j]; },
         [&](int j, int i) __attribute__((always_inline)) { return cand[(tok0 + j) * cap + i]; },
-        nullptr, nullptr, idx, gate, topval);
+        lv, le, idx, gate, topval);
 }
 
 // ------------------------------------------------------------------------------ fused route
@@ -1896,7 +1911,8 @@ static void launch_zpass(const LowrankPlan& p, const uint16_t* x, const uint16_t
                          int64_t T, int32_t h, int32_t r, const uint16_t* R2t, int32_t M,
                          float* gnorm, uint16_t* zhi, float* cz, hipStream_t st) {
     const int64_t zblocks = (T + kZTokens - 1) / kZTokens;
-    const int64_t nblocks = (((int64_t)M + 31) / 32 * 32 * (r / 8) + 255) / 256;  // group norms
+    const int64_t nblocks = (((int64_t)M + 31) / 32 * 32 * (r / 8) + 256 * kGroupNormBlocks - 1) /
+                            (256 * kGroupNormBlocks);  // group-norm workgroups
     dim3 grid((unsigned)(zblocks * p.hsplit + nblocks));
     constexpr int D = 2;
     hipLaunchKernelGGL((zpass_kernel<RT, D>), grid, dim3(256), 0, st, x, R1t, zparts, (int32_t)T,
@@ -1933,9 +1949,13 @@ static void launch_route(const LowrankPlan& p, const RouteArgs& a, hipStream_t s
     hipLaunchKernelGGL((collect_kernel<RC, K>), grid, dim3(kRouteThreads), 0, st, a.zhi, a.cz,
                        a.R2t, a.T, a.M, p.chunks, p.splits, a.theta, a.gnorm, a.count, a.cand,
                        p.cap);
-    hipLaunchKernelGGL((finalize_kernel<RC, K>), dim3((unsigned)((a.T + 31) / 32)), dim3(256), 0,
-                       st, a.z, a.R2t, a.T, a.M, a.k, a.count, a.cand, p.cap, a.idx, a.gate,
-                       a.topval);
+    const dim3 fgrid((unsigned)((a.T + 31) / 32));
+    if (a.T <= 32 * 256)  // at most one workgroup per CU
+        hipLaunchKernelGGL((finalize_kernel<RC, K, 32>), fgrid, dim3(256), 0, st, a.z, a.R2t, a.T,
+                           a.M, a.k, a.count, a.cand, p.cap, a.idx, a.gate, a.topval);
+    else
+        hipLaunchKernelGGL((finalize_kernel<RC, K, 0>), fgrid, dim3(256), 0, st, a.z, a.R2t, a.T,
+                           a.M, a.k, a.count, a.cand, p.cap, a.idx, a.gate, a.topval);
 }
 
 template <int RC>
