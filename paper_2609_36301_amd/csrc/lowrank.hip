@@ -1862,7 +1862,8 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     if (S > q.ntb) S = q.ntb;
     q.splits = (int32_t)S;
     q.theta_group = 1;
-    while (q.theta_group < 64 && q.theta_group * 16 < q.chunks) q.theta_group *= 2;
+    // threads per token in the threshold kernel: one per 4 chunk lists, at most 64
+    while (q.theta_group < 64 && q.theta_group * 4 < q.chunks) q.theta_group *= 2;
     // z pass: 128-token blocks; the h chunks are split over workgroups when there are fewer
     // token blocks than CUs (one workgroup of 4 waves per CU streams x too slowly to leave
     // CUs idle: at T = 16384, h = 4096 two splits and the partial-sum reduction take 46 us
