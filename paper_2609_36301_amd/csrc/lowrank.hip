@@ -414,7 +414,8 @@ __device__ __forceinline__ RouteSplit route_split(int32_t T, int32_t M, int32_t 
 template <int RC, int K>
 __device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ R2t,
                                            const float* __restrict__ gnorm, int32_t M,
-                                           int64_t t0, int64_t t1, uint16_t* rows, float* gn) {
+                                           int64_t t0, int64_t t1, uint16_t* rows, float* gn,
+                                           bool copy_gn = true) {
     using C = RouteCfg<RC, K>;
     const int tid = threadIdx.x;
     const int nseg = (int)(t1 - t0) * 32 * C::SPR;
@@ -440,8 +441,48 @@ __device__ __forceinline__ void load_chunk(const uint16_t* __restrict__ R2t,
             }
         }
     }
-    const int ngr = (int)(t1 - t0) * 8;
-    for (int g = tid; g < ngr; g += kRouteThreads) gn[g] = gnorm[t0 * 8 + g];
+    if (copy_gn) {
+        const int ngr = (int)(t1 - t0) * 8;
+        for (int g = tid; g < ngr; g += kRouteThreads) gn[g] = gnorm[t0 * 8 + g];
+    }
+    __syncthreads();
+}
+
+// Group norms of a chunk resident in LDS (as group_norms computes them from memory), written to
+// the LDS copy gn and, with out != nullptr, to the chunk's part of the global array for the
+// collect kernel.  Every thread of the workgroup takes part; rows past M hold copies of row
+// M - 1 and their groups get the bound 2^100.
+template <int RC, int K>
+__device__ __forceinline__ void chunk_group_norms(const uint16_t* rows, int32_t M, int64_t t0,
+                                                  int64_t t1, float* gn,
+                                                  float* __restrict__ out) {
+    using C = RouteCfg<RC, K>;
+    const int tid = threadIdx.x;
+    const int nrows = (int)(t1 - t0) * 32;
+    for (int rb = 0; rb < nrows; rb += kRouteThreads) {  // workgroup-uniform trip count
+        const int rr = rb + tid < nrows ? rb + tid : nrows - 1;
+        const int sw = C::swz(rr);
+        float ss = 0.0f;
+#pragma unroll
+        for (int sg = 0; sg < C::SPR; ++sg) {
+            const bf16x8 v = load_bf16x8(rows + rr * C::R + ((sg ^ sw) * 8));
+#pragma unroll
+            for (int q = 0; q < 8; q += 2) {
+                const bf16x2 pq = {v[q], v[q + 1]};
+                ss = __builtin_amdgcn_fdot2_f32_bf16(pq, pq, ss, false);
+            }
+        }
+        ss = fmaxf(ss, lane_xor<1>(ss));  // the 4 rows of the group sit in 4 consecutive lanes
+        ss = fmaxf(ss, lane_xor<2>(ss));
+        const int64_t row = t0 * 32 + rr;
+        if (rb + tid < nrows && (rr & 3) == 0) {
+            const int g4 = (rr & 31) >> 2;
+            const int slot = (rr >> 5) * 8 + (g4 & 1) * 4 + (g4 >> 1);
+            const float nb = row + 3 < M ? sqrtf(ss) * (1.0f + 0x1p-20f) : kPhantomNorm;
+            gn[slot] = nb;
+            if (out) out[t0 * 8 + slot] = nb;
+        }
+    }
     __syncthreads();
 }
 
@@ -815,13 +856,16 @@ template <int RC, int K>
 __global__ __launch_bounds__(kRouteThreads, 2) void screen_kernel(
     const uint16_t* __restrict__ zh, const float* __restrict__ cz,
     const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t chunks, int32_t splits,
-    const float* __restrict__ gnorm, float* __restrict__ top) {
+    float* __restrict__ gnorm, float* __restrict__ top) {
     using C = RouteCfg<RC, K>;
     constexpr int L = C::L, TPW = C::TPW;
     __shared__ __attribute__((aligned(16))) uint16_t rows[C::EMAX * C::R];
     __shared__ __attribute__((aligned(16))) float gn[C::EMAX / 4];
     const RouteSplit sp = route_split(T, M, chunks, splits, C::TOK);
-    load_chunk<RC, K>(R2t, gnorm, M, sp.t0, sp.t1, rows, gn);
+    // With one token split (small T) the group norms of the chunk are computed here from LDS
+    // and published for the collect kernel; otherwise the z pass has written them.
+    load_chunk<RC, K>(R2t, gnorm, M, sp.t0, sp.t1, rows, gn, splits > 1);
+    if (splits == 1) chunk_group_norms<RC, K>(rows, M, sp.t0, sp.t1, gn, gnorm);
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int n = lane & 31, half = lane >> 5;
@@ -1912,8 +1956,13 @@ static void launch_zpass(const LowrankPlan& p, const uint16_t* x, const uint16_t
                          int64_t T, int32_t h, int32_t r, const uint16_t* R2t, int32_t M,
                          float* gnorm, uint16_t* zhi, float* cz, hipStream_t st) {
     const int64_t zblocks = (T + kZTokens - 1) / kZTokens;
-    const int64_t nblocks = (((int64_t)M + 31) / 32 * 32 * (r / 8) + 256 * kGroupNormBlocks - 1) /
-                            (256 * kGroupNormBlocks);  // group-norm workgroups
+    // group-norm workgroups, unless the expert-resident route runs one token split: then its
+    // screen kernel computes the norms from its LDS chunk (each chunk is loaded once)
+    const int64_t nblocks =
+        p.fused || p.splits > 1
+            ? (((int64_t)M + 31) / 32 * 32 * (r / 8) + 256 * kGroupNormBlocks - 1) /
+                  (256 * kGroupNormBlocks)
+            : 0;
     dim3 grid((unsigned)(zblocks * p.hsplit + nblocks));
     constexpr int D = 2;
     hipLaunchKernelGGL((zpass_kernel<RT, D>), grid, dim3(256), 0, st, x, R1t, zparts, (int32_t)T,
