@@ -2,14 +2,14 @@
 // T x M logits (Appendix "Pseudocode", inference algorithm; MoRE layer in "Preliminaries").
 //
 // Routes of one call (chosen per shape by lowrank_make_plan):
-//   expert-resident  zpass (z = x R1, fp32, and the group norms of R2t's rows) [+ zreduce when
-//                    the h axis is split over workgroups for small T], then screen, threshold,
-//                    collect and finalize kernels; screen and collect workgroups hold one chunk
-//                    of the expert axis in LDS;
+//   expert-resident  zpass (z = x R1, fp32, and the group norms of R2t's rows unless the screen
+//                    kernel takes them) [+ zreduce when the h axis is split over workgroups],
+//                    then screen, threshold, collect and finalize kernels; screen and collect
+//                    workgroups hold one chunk of the expert axis in LDS;
 //   fused            zpass, then one fused_route_kernel: a workgroup of 64 tokens sweeps the
 //                    whole expert axis (operands streamed from L2) through the same four steps;
-//   local            one fused_local_kernel: the fused workgroup also computes z and the group
-//                    norms, and keeps its expert rows in registers.
+//   local            one fused_local_kernel: the fused workgroup also computes z and one norm
+//                    bound per wave, and keeps its expert rows in registers.
 // The steps: screening bounds on z_hi = bf16(z) give a per-token threshold that k experts
 // provably reach, the candidates above it are collected, and their logits are evaluated exactly
 // in fp32 for the final top k (see the route section).
@@ -1329,7 +1329,7 @@ __global__ __launch_bounds__(256) void finalize_kernel(
 // same candidate guarantee, same exact evaluation).
 //   fused_route_kernel  reads z, z_hi and the group norms written by the z pass and streams the
 //                       A operands from L2, D tiles ahead (r M <= 2^18);
-//   fused_local_kernel  also computes z for its tokens and the group norms of its tiles, and
+//   fused_local_kernel  also computes z for its tokens and a norm bound for its tiles, and
 //                       keeps the A operands in registers for both passes (r M <= 2^17, K <= 8):
 //                       the whole routing call is one launch.  Its z sums the h axis in four
 //                       quarters (one per wave pair) added in order, so its logits may differ
@@ -1676,7 +1676,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
 #pragma unroll
         for (int pt = 0; pt < RT; ++pt) za[pt] = zero_f32x16();
         for (int h0 = 0; h0 < h; h0 += ZHC) {
-            const int hc = h - h0 < ZHC ? h - h0 : ZHC;  // multiple of 32
+            const int hc = h - h0 < ZHC ? h - h0 : ZHC;  // multiple of 16
             const int segs = hc >> 3;                     // 16-byte segments per row
             const int swm = ((segs & -segs) < 32 ? (segs & -segs) : 32) - 1;
             const int ns = (kFusedTokens + r) * segs;
