@@ -787,11 +787,10 @@ __device__ __forceinline__ int collect_tile_sign(const f32x16& acc, int32_t code
         m = __builtin_amdgcn_alignbit(m, __builtin_bit_cast(uint32_t, ai), 31);
     }
     m ^= 0xFFFFu;  // element i (bit i) passes iff acc[i] >= +0
-    if (m) {
-        *slot(cnt < S ? cnt : S - 1) = ((uint32_t)code << 16) | m;
-        ++cnt;
-    }
-    return cnt;
+    // Stored without a branch: an entry with no hit sits in the next free slot until a hit
+    // overwrites it; slot S takes every entry past the first S (the token then overflows).
+    *slot(cnt < S ? cnt : S) = ((uint32_t)code << 16) | m;
+    return cnt + (m != 0u ? 1 : 0);
 }
 
 // Masks of the accumulator elements of lane half 0 and 1 that hold experts < M in the last
@@ -1375,7 +1374,7 @@ struct FusedLds {
     float tops[kRouteWaves][kFusedTokens][K];  // per wave and token: K best bucket maxima
     int32_t cand[kFusedTokens * kFusedCap];    // candidate lists
     union {
-        uint32_t slots[kFusedSlots][2][kRouteThreads];  // collect pass
+        uint32_t slots[kFusedSlots + 1][2][kRouteThreads];  // collect pass (+ overflow slot)
         struct {                                        // final selection (rank path)
             float lv[kFusedTokens][kFusedRankCap];
             int32_t le[kFusedTokens][kFusedRankCap];
