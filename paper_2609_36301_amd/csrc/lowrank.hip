@@ -1371,7 +1371,9 @@ __host__ __device__ constexpr int fused_reg_tiles(int RC) { return RC == 4 ? 4 :
 // LDS of the fused phases.
 template <int K>
 struct FusedLds {
-    float tops[kRouteWaves][kFusedTokens][K];  // per wave and token: K best bucket maxima
+    // per token and wave: K best bucket maxima (the token's row padded by 16 bytes, so that
+    // the 32 tokens a wave writes at once spread over the banks)
+    float tops[kFusedTokens][kRouteWaves * K + 4];
     int32_t cand[kFusedTokens * kFusedCap];    // candidate lists
     union {
         uint32_t slots[kFusedSlots + 1][2][kRouteThreads];  // collect pass (+ overflow slot)
@@ -1463,7 +1465,7 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
             vlist_merge<L>(bm[g], pb);
             if (half == 0) {
 #pragma unroll
-                for (int j = 0; j < K; ++j) sh.tops[w][32 * g + n][j] = bm[g][j];
+                for (int j = 0; j < K; ++j) sh.tops[32 * g + n][w * K + j] = bm[g][j];
             }
         }
     }
@@ -1473,7 +1475,7 @@ __device__ __forceinline__ void fused_phases(Sweep&& run_sweep, const TokenGroup
         const int jt = tid >> 3, sub = tid & 7;
         float v[K];
 #pragma unroll
-        for (int j = 0; j < K; ++j) v[j] = sh.tops[sub][jt][j];
+        for (int j = 0; j < K; ++j) v[j] = sh.tops[jt][sub * K + j];
         unroll<3>([&](auto ss) __attribute__((always_inline)) {
             float b[K];
 #pragma unroll
@@ -1616,7 +1618,8 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     int32_t* __restrict__ hist, int32_t* __restrict__ idx, float* __restrict__ gate,
     float* __restrict__ topval) {
     constexpr int R = 16 * RC, RT = (RC + 1) / 2, TPW = 2, NTW = fused_reg_tiles(RC);
-    constexpr int ZRED = 4 * 2 * RT * 64 * 16;  // floats: [h quarter][group][tile][lane][16]
+    constexpr int ZRED = 4 * 2 * RT * 64 * 16;  // floats: [h quarter][group][tile][quad][lane][4]
+    constexpr int ZSP = R + 4;  // z row stride in floats: an odd count of 16-byte segments
     constexpr int ZHC = local_zchunk(RC);       // h per staged chunk
     constexpr int STAGE = (kFusedTokens + R) * ZHC * 2;  // bytes: x rows, then R1t rows
     constexpr int POOL0 = (int)sizeof(FusedLds<K>) > 4 * ZRED ? (int)sizeof(FusedLds<K>) : 4 * ZRED;
@@ -1625,8 +1628,8 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
     __shared__ __attribute__((aligned(16))) unsigned char pool[POOL];
     FusedLds<K>& sh = *reinterpret_cast<FusedLds<K>*>(pool);
     float* zred = reinterpret_cast<float*>(pool);
-    __shared__ __attribute__((aligned(16))) float zs[kFusedTokens * R];  // z rows, fp32
-    __shared__ float csp[kFusedTokens][4][2];  // shares of the squared norms of z_lo, z_hi
+    __shared__ __attribute__((aligned(16))) float zs[kFusedTokens * ZSP];  // z rows, fp32
+    __shared__ float csp[4][2][kFusedTokens];  // shares of the squared norms of z_lo, z_hi
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -1744,10 +1747,10 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
         }
 #pragma unroll
         for (int pt = 0; pt < RT; ++pt) {
-            f32x4* dst = reinterpret_cast<f32x4*>(zred + (((hq * 2 + zg) * RT + pt) * 64 + lane) * 16);
+            f32x4* dst = reinterpret_cast<f32x4*>(zred + (((hq * 2 + zg) * RT + pt) * 256 + lane) * 4);
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-                dst[q] = f32x4{za[pt][4 * q], za[pt][4 * q + 1], za[pt][4 * q + 2], za[pt][4 * q + 3]};
+                dst[64 * q] = f32x4{za[pt][4 * q], za[pt][4 * q + 1], za[pt][4 * q + 2], za[pt][4 * q + 3]};
         }
     }
     lds_barrier();  // (the expert tiles may still be in flight)
@@ -1767,7 +1770,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
 #pragma unroll
             for (int hq = 0; hq < 4; ++hq) {
                 const f32x4 v = *reinterpret_cast<const f32x4*>(
-                    zred + (((hq * 2 + zg) * RT + pt) * 64 + lane) * 16 + 4 * part);
+                    zred + ((((hq * 2 + zg) * RT + pt) * 4 + part) * 64 + lane) * 4);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) zsum[i] = hq == 0 ? v[i] : zsum[i] + v[i];
             }
@@ -1779,14 +1782,14 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
                     hi2 = fmaf(hf, hf, hi2);
                     lo2 = fmaf(lf, lf, lo2);
                 }
-                *reinterpret_cast<f32x4*>(&zs[jt * R + 16 * c + 8 * half + q0]) = zsum;
+                *reinterpret_cast<f32x4*>(&zs[jt * ZSP + 16 * c + 8 * half + q0]) = zsum;
             }
         }
         hi2 = sum_pair32(hi2);
         lo2 = sum_pair32(lo2);
         if (half == 0) {
-            csp[jt][part][0] = lo2;
-            csp[jt][part][1] = hi2;
+            csp[part][0][jt] = lo2;
+            csp[part][1][jt] = hi2;
         }
     }
     // The wave's norm bound nw >= the norm of every row of its tiles, from the registers: a lane
@@ -1838,11 +1841,11 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
         for (int c = 0; c < RC; ++c) {
             bf16x8 v;
 #pragma unroll
-            for (int q = 0; q < 8; ++q) v[q] = (__bf16)zs[jt * R + 16 * c + 8 * half + q];
+            for (int q = 0; q < 8; ++q) v[q] = (__bf16)zs[jt * ZSP + 16 * c + 8 * half + q];
             tg.zhi[g][c] = ok ? v : zero_bf16x8();
         }
-        const float lo2 = ((csp[jt][0][0] + csp[jt][1][0]) + csp[jt][2][0]) + csp[jt][3][0];
-        const float hi2 = ((csp[jt][0][1] + csp[jt][1][1]) + csp[jt][2][1]) + csp[jt][3][1];
+        const float lo2 = ((csp[0][0][jt] + csp[1][0][jt]) + csp[2][0][jt]) + csp[3][0][jt];
+        const float hi2 = ((csp[0][1][jt] + csp[1][1][jt]) + csp[2][1][jt]) + csp[3][1][jt];
         tg.c[g] = ok ? screen_scale(lo2, hi2, r) : 0.0f;
     }
     fused_phases<RC, K, true>(
@@ -1850,7 +1853,7 @@ __global__ __launch_bounds__(kRouteThreads, 2) void fused_local_kernel(
             sweep_regs<RC, K, TPW, NTW, false>(areg, nullptr, nt, rot, e00, M, half, tg.zhi, cin,
                                                body);
         },
-        tg, wave_norm, sh, [&](int j) __attribute__((always_inline)) { return zs + j * R; }, R2t, T,
+        tg, wave_norm, sh, [&](int j) __attribute__((always_inline)) { return zs + j * ZSP; }, R2t, T,
         M, k, tok0, idx, gate, topval);
 }
 
