@@ -81,6 +81,16 @@ def test_workload_decode_all_tokens():
     _check(inp, w.k, idx, gate, topval, label="decode")
 
 
+def test_workload_decode_finer_chunking_is_bitwise_identical():
+    # full size: twice the library's expert chunks (512 instead of 256) give the same bits
+    w = WORKLOADS["decode"]
+    inp = make_workload_inputs("decode")
+    base = route_lowrank(inp, w.k, tag="decode")
+    finer = route_lowrank(inp, w.k, m_chunks=512, tag="decode chunks=512")
+    for a, b in zip(base[:3], finer[:3]):
+        assert np.array_equal(a, b)
+
+
 # r = 128 and k > 16 are outside the low-rank router's limits: their kernels spilled
 # registers, and the r = 128, k = 32 case faulted the GPU with a cause not yet found.
 _OUT_OF_LIMITS = pytest.mark.skip(reason="r = 128 / k > 16: low-rank route returns "
