@@ -9,9 +9,11 @@ distinct input batches (> 256 MB in total) that each step reads its batch from H
 than from the last-level cache.  K steps are timed with HIP events on the stream the
 library launches on, bracketed by device synchronisation.
 
-Printed: one JSON line with routed tokens/s, the roofline position of the routing call,
-the full-rank router measured on the same inputs, and the fp64 CPU oracle timed on a
-bounded sample of the same workload.
+Printed: one JSON line with routed tokens/s (mean over the K timed steps, plus the median and
+p10/p90 over graph replays), the roofline position of the routing call, the full-rank router
+measured on the same inputs, the fp64 CPU oracle timed on the same workload (all tokens when
+they fit its time budget), and the parity counts of the GPU result against that oracle run.
+The default workload is fine_grained, the largest of the five that fit one GPU.
 """
 from __future__ import annotations
 
@@ -117,54 +119,56 @@ def copy_calibration(nbytes):
           flush=True)
 
 
-def timed(fn, steps, warmup, stream):
-    """Seconds per call of fn(i), eager launches (for calls much longer than launch cost)."""
-    import torch
-    for i in range(warmup):
-        fn(i)
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    for i in range(steps):
-        fn(i)
-    end.record(stream)
-    torch.cuda.synchronize()
-    return start.elapsed_time(end) / 1e3 / steps
+def replay_split(steps):
+    """(replays, steps per replay) with replays * steps_per_replay == steps, replays <= 10."""
+    for reps in range(min(10, steps), 0, -1):
+        if steps % reps == 0:
+            return reps, steps // reps
+    return 1, steps
 
 
 def timed_graph(fn, steps, warmup):
-    """Seconds per step, with the `steps` timed steps captured in one HIP graph.
+    """Times exactly `steps` steps captured in HIP graphs; returns per-step seconds statistics.
 
     Host launch cost per routing call (ctypes + checks) exceeds the kernels' run time, so
-    eager launches would time the host.  The graph holds exactly the library's launches for
-    `steps` consecutive steps; after `warmup` eager steps it is replayed once untimed, then
-    once inside the timed region.
+    eager launches would time the host.  After `warmup` eager steps, `steps / R` consecutive
+    steps are captured in one HIP graph, which is replayed once untimed and then R times in
+    the timed region (R <= 10, so the K timed steps are exactly K); each replay is bracketed
+    by HIP events on the stream the library launches on, which gives the spread.
     """
     import torch
+    reps, per = replay_split(steps)
     for i in range(warmup):
         fn(i)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        for i in range(steps):
+        for i in range(per):
             fn(i)
     torch.cuda.synchronize()
     g.replay()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    start.record(stream)
-    g.replay()
-    end.record(stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
     torch.cuda.synchronize()
-    return start.elapsed_time(end) / 1e3 / steps
+    ev[0].record(stream)
+    for j in range(reps):
+        g.replay()
+        ev[j + 1].record(stream)
+    torch.cuda.synchronize()
+    per_step = np.array([ev[j].elapsed_time(ev[j + 1]) / 1e3 / per for j in range(reps)])
+    total = ev[0].elapsed_time(ev[reps]) / 1e3
+    return {"mean_s": total / steps, "median_s": float(np.median(per_step)),
+            "p10_s": float(np.percentile(per_step, 10)), "p90_s": float(np.percentile(per_step, 90)),
+            "replays": reps, "steps_per_replay": per}
 
 
-def cpu_baseline(w, inp, budget_s=12.0):
-    """fp64 oracle on a bounded token sample of the same workload (all host cores)."""
+def cpu_baseline_and_parity(w, inp, out, budget_s=40.0):
+    """The fp64 oracle timed on the host cores over the workload's tokens (all of them when
+    they fit the budget, else the first n), and the GPU result on those tokens compared with
+    it under the parity rules of oracle/parity.py."""
     import oracle
+    from oracle import parity
     cores = len(os.sched_getaffinity(0))
     n = min(w.T, 64)
     t0 = time.perf_counter()
@@ -172,10 +176,18 @@ def cpu_baseline(w, inp, budget_s=12.0):
     per_tok = (time.perf_counter() - t0) / n
     n = int(min(w.T, max(n, budget_s / max(per_tok, 1e-9))))
     t0 = time.perf_counter()
-    oracle.route_lowrank(inp.x[:n], inp.R1, inp.R2, w.k, threads=cores)
+    orc = oracle.route_lowrank(inp.x[:n], inp.R1, inp.R2, w.k, threads=cores)
     dt = time.perf_counter() - t0
-    return {"value": round(n / dt, 1), "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": "first %d of %d tokens of the same workload, fp64, %.1f s wall" % (n, w.T, dt)}
+    base = {"value": round(n / dt, 1), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": "first %d of %d tokens of the same workload, fp64, %.1f s wall"
+                      % (n, w.T, dt)}
+    idx, gate, topval = out
+    rep = parity.compare_with(orc, inp.x[:n], inp.R1, inp.R2, w.k, idx[:n], gate[:n],
+                              topval[:n], threads=cores)
+    par = rep.as_dict()
+    par["rules"] = ("oracle/parity.py: identical sets except near ties (1e-3 relative), "
+                    "band-valid top k on every token, gates 2e-3, logits 1e-4 relative")
+    return base, par
 
 
 def main():
@@ -183,8 +195,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="teaser_prefill")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default="fine_grained")
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip the oracle leg (CPU baseline and parity counts)")
     ap.add_argument("--no-fullrank", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy kernel of BYTES (counter calibration) and exit")
@@ -224,13 +237,13 @@ def main():
     torch.cuda.synchronize()
 
     lr = router.LowrankRouter(w.T, w.h, w.r, w.M, w.k, device=dev, histogram=w.histogram)
-    stream = torch.cuda.current_stream(dev)
 
     def step(i):
         xb, r1b, r2b = bufs[i % nbuf]
         lr(xb, r1b, r2b)
 
-    sec = timed_graph(step, args.steps, args.warmup)
+    tm = timed_graph(step, args.steps, args.warmup)
+    sec = tm["mean_s"]
     plan_chunks = router.lowrank_plan(w.T, w.h, w.r, w.M, w.k)
     route = "expert-resident"
     if plan_chunks == 0:  # fused; the local variant needs no workspace
@@ -254,28 +267,41 @@ def main():
                    "histogram": w.histogram, "route": route, "expert_chunks": plan_chunks,
                    "rotating_batches": nbuf, "launch": "hip graph of the timed steps"},
         "roofline": roofline(w, sec, SCOPES[route]),
+        "timing": {"median_ms": round(tm["median_s"] * 1e3, 5),
+                   "p10_ms": round(tm["p10_s"] * 1e3, 5), "p90_ms": round(tm["p90_s"] * 1e3, 5),
+                   "replays": tm["replays"], "steps_per_replay": tm["steps_per_replay"]},
     }
 
     if not args.no_fullrank:
         # full-rank router on the same token batches with W = R1 R2 rounded to bf16; logits
-        # materialised in fp32 and in bf16; the speedup uses the faster of the two.
+        # materialised in fp32 and in bf16; timed from HIP graphs like the low-rank router; the
+        # speedup uses the faster of the two.
         from paper_2609_36301_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
         W = bf16_bits_to_f32(inp.R1).astype(np.float64) @ bf16_bits_to_f32(inp.R2).astype(
             np.float64)
         Wt = to_dev(np.ascontiguousarray(f32_to_bf16_bits(W.astype(np.float32)).T))
         fr = {}
+        fsteps = max(2, min(args.steps, 20))
         for bits, key in ((32, "fp32_logits_ms"), (16, "bf16_logits_ms")):
             frr = router.FullrankRouter(w.T, w.h, w.M, w.k, device=dev, logit_bits=bits)
-            fr[key] = round(timed(lambda i: frr(bufs[i % nbuf][0], Wt),
-                                  max(5, args.steps // 10), 3, stream) * 1e3, 5)
+            ft = timed_graph(lambda i: frr(bufs[i % nbuf][0], Wt), fsteps, 2)
+            fr[key] = round(ft["mean_s"] * 1e3, 5)
             del frr
             torch.cuda.empty_cache()
         best = min(fr["fp32_logits_ms"], fr["bf16_logits_ms"])
         fr["speedup_lowrank_vs_fullrank"] = round(best / (sec * 1e3), 3)
         fr["speedup_target"] = round(w.M / (2 * w.r) * w.h / (w.h + w.M), 3)
+        fr["timed_steps"] = fsteps
         result["fullrank"] = fr
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(w, inp)
+        # one more routing call on the unrolled batch (bufs[0] holds the workload's own inputs),
+        # compared with the oracle in the CPU-baseline leg
+        chk = router.LowrankRouter(w.T, w.h, w.r, w.M, w.k, device=dev, topval=True)
+        o = chk(*bufs[0])
+        torch.cuda.synchronize()
+        out = (o.idx.cpu().numpy(), o.gate.cpu().numpy(), o.topval.cpu().numpy())
+        del chk, o
+        result["cpu_baseline"], result["parity"] = cpu_baseline_and_parity(w, inp, out)
     print(json.dumps(result), flush=True)
 
 

@@ -11,6 +11,10 @@ Functions and the passage they follow:
   route_lowrank   softmax(TopK(x R1 R2)), the MoRE router ("Preliminaries", MoRE layer)
   route_fullrank  softmax(TopK(x W)), the standard router ("Preliminaries")
   histogram       per-expert selection counts (Appendix "Training", statistic f)
+  logits_at       the logits x R1 R2 at given (token, expert) pairs ("Preliminaries"), to
+                  check a selection made elsewhere expert by expert
+  fullrank_logits_at  the same for the full-rank logits x W (W as bf16 bits)
+  parity          the comparison rules of a routing result against this oracle
 """
 from __future__ import annotations
 
@@ -52,6 +56,10 @@ def load_library(path: str):
         fn.restype = ctypes.c_int
     lib.oracle_histogram.argtypes = [P, i64, i32, i32, P]
     lib.oracle_histogram.restype = ctypes.c_int
+    lib.oracle_logits_at.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, P, i32, P, i32]
+    lib.oracle_logits_at.restype = ctypes.c_int
+    lib.oracle_fullrank_logits_at.argtypes = [P, P, i64, i32, i32, P, i64, P, i32, P]
+    lib.oracle_fullrank_logits_at.restype = ctypes.c_int
     return lib
 
 
@@ -151,6 +159,42 @@ def route_fullrank(x, W, k: int, rows=None, threads=None, lib=None) -> OracleRes
         raise TypeError("W must be float64 values or uint16 bfloat16 bits")
     _check(fn(_ptr(x), _ptr(W), T, h, M, k, None if rows_a is None else _ptr(rows_a), nrows,
               _ptr(out.idx), _ptr(out.gate), _ptr(out.topval), _ptr(out.next), _threads(threads)))
+    return out
+
+
+def logits_at(x, R1, R2, rows, experts, threads=None, lib=None) -> np.ndarray:
+    """fp64 logits l[rows[i], experts[i][j]] ([n][m] float64); the same sums as route_lowrank."""
+    x, R1, R2 = _u16(x), _u16(R1), _u16(R2)
+    T, h = x.shape
+    h2, r = R1.shape
+    r2, M = R2.shape
+    if h2 != h or r2 != r:
+        raise ValueError("shape mismatch")
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    experts = np.ascontiguousarray(experts, dtype=np.int32)
+    if rows.ndim != 1 or experts.ndim != 2 or experts.shape[0] != rows.size:
+        raise ValueError("rows must be [n] and experts [n][m]")
+    out = np.zeros(experts.shape, np.float64)
+    _check(_load(lib).oracle_logits_at(_ptr(x), _ptr(R1), _ptr(R2), T, h, r, M, _ptr(rows),
+                                       rows.size, _ptr(experts), experts.shape[1], _ptr(out),
+                                       _threads(threads)))
+    return out
+
+
+def fullrank_logits_at(x, W, rows, experts, lib=None) -> np.ndarray:
+    """fp64 logits (x W)[rows[i], experts[i][j]] with W bf16 bits [h][M]; [n][m] float64."""
+    x, W = _u16(x), _u16(W)
+    T, h = x.shape
+    h2, M = W.shape
+    if h2 != h:
+        raise ValueError("shape mismatch")
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    experts = np.ascontiguousarray(experts, dtype=np.int32)
+    if rows.ndim != 1 or experts.ndim != 2 or experts.shape[0] != rows.size:
+        raise ValueError("rows must be [n] and experts [n][m]")
+    out = np.zeros(experts.shape, np.float64)
+    _check(_load(lib).oracle_fullrank_logits_at(_ptr(x), _ptr(W), T, h, M, _ptr(rows), rows.size,
+                                                _ptr(experts), experts.shape[1], _ptr(out)))
     return out
 
 

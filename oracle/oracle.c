@@ -25,6 +25,10 @@
  * selections (bincount of the chosen indices, Appendix "Training", load-balancing
  * statistic f).
  *
+ * oracle_logits_at evaluates steps 2-3 at given (token, expert) pairs only, so that a
+ * selection made by another implementation can be checked expert by expert;
+ * oracle_fullrank_logits_at does the same for the full-rank logits x W.
+ *
  * Non-finite inputs are rejected (return value ORACLE_ERR_NONFINITE).
  */
 #include <math.h>
@@ -179,6 +183,72 @@ int oracle_route_lowrank(const uint16_t* x, const uint16_t* R1, const uint16_t* 
     return status;
 }
 
+/*
+ * Logits at chosen (token, expert) pairs, for checking a selection made elsewhere against the
+ * definition: out[i][j] = l_{rows[i], experts[i][j]} with z and the logit summed exactly as in
+ * steps 2 and 3 above (z over h in increasing order, the logit over r in increasing order), so
+ * every value equals the corresponding logit of oracle_route_lowrank bit for bit.
+ * x, R1, R2 as in oracle_route_lowrank; rows [nrows] token ids; experts [nrows][m] ids in
+ * [0, M); out double [nrows][m].
+ */
+int oracle_logits_at(const uint16_t* x, const uint16_t* R1, const uint16_t* R2, int64_t T,
+                     int32_t h, int32_t r, int32_t M, const int64_t* rows, int64_t nrows,
+                     const int32_t* experts, int32_t m, double* out, int32_t nthreads) {
+    if (!x || !R1 || !R2 || !rows || !experts || !out || m < 0) return ORACLE_ERR_ARG;
+    if (!check_shape(T, h, r, M, 1, rows, nrows)) return ORACLE_ERR_ARG;
+    for (int64_t i = 0; i < nrows * (int64_t)m; ++i)
+        if (experts[i] < 0 || experts[i] >= M) return ORACLE_ERR_ARG;
+    double* r1 = (double*)malloc(sizeof(double) * (size_t)h * (size_t)r);
+    double* r2 = (double*)malloc(sizeof(double) * (size_t)r * (size_t)M);
+    if (!r1 || !r2) {
+        free(r1);
+        free(r2);
+        return ORACLE_ERR_NOMEM;
+    }
+    int ok = decode_all(R1, (int64_t)h * r, r1) & decode_all(R2, (int64_t)r * M, r2);
+    int status = ok ? ORACLE_OK : ORACLE_ERR_NONFINITE;
+    if (status == ORACLE_OK) {
+#ifdef _OPENMP
+        if (nthreads > 0) omp_set_num_threads(nthreads);
+#endif
+#pragma omp parallel
+        {
+            double* xrow = (double*)malloc(sizeof(double) * (size_t)h);
+            double* z = (double*)malloc(sizeof(double) * (size_t)r);
+            int local_ok = xrow && z;
+#pragma omp for schedule(dynamic, 16)
+            for (int64_t t = 0; t < nrows; ++t) {
+                if (!local_ok) continue;
+                if (!decode_all(x + rows[t] * (int64_t)h, h, xrow)) {
+#pragma omp atomic write
+                    status = ORACLE_ERR_NONFINITE;
+                    continue;
+                }
+                for (int32_t i = 0; i < r; ++i) z[i] = 0.0;
+                for (int32_t j = 0; j < h; ++j) {
+                    const double* w1 = r1 + (int64_t)j * r; /* row j of R1 */
+                    for (int32_t i = 0; i < r; ++i) z[i] += xrow[j] * w1[i];
+                }
+                for (int32_t j = 0; j < m; ++j) {
+                    const int64_t e = experts[t * m + j];
+                    double l = 0.0;
+                    for (int32_t i = 0; i < r; ++i) l += z[i] * r2[(int64_t)i * M + e];
+                    out[t * m + j] = l;
+                }
+            }
+            if (!local_ok) {
+#pragma omp atomic write
+                status = ORACLE_ERR_NOMEM;
+            }
+            free(xrow);
+            free(z);
+        }
+    }
+    free(r1);
+    free(r2);
+    return status;
+}
+
 /* Shared body of the two full-rank entry points; W is already decoded to double [h][M]. */
 static int fullrank_body(const uint16_t* x, const double* W, int64_t T, int32_t h, int32_t M,
                          int32_t k, const int64_t* rows, int64_t nrows, int32_t* idx,
@@ -248,6 +318,35 @@ int oracle_route_fullrank_bf16(const uint16_t* x, const uint16_t* W, int64_t T, 
                      : ORACLE_ERR_NONFINITE;
     free(w);
     return status;
+}
+
+/*
+ * Full-rank logits at chosen (token, expert) pairs: out[i][j] = sum_h x[rows[i]][h] W[h][e]
+ * with e = experts[i][j], W given as bf16 bits [h][M], summed over h in increasing order as
+ * the full-rank router above does, so the values equal its logits bit for bit.
+ */
+int oracle_fullrank_logits_at(const uint16_t* x, const uint16_t* W, int64_t T, int32_t h,
+                              int32_t M, const int64_t* rows, int64_t nrows,
+                              const int32_t* experts, int32_t m, double* out) {
+    if (!x || !W || !rows || !experts || !out || m < 0) return ORACLE_ERR_ARG;
+    if (!check_shape(T, h, 1, M, 1, rows, nrows)) return ORACLE_ERR_ARG;
+    for (int64_t i = 0; i < nrows * (int64_t)m; ++i)
+        if (experts[i] < 0 || experts[i] >= M) return ORACLE_ERR_ARG;
+    for (int64_t t = 0; t < nrows; ++t) {
+        const uint16_t* xr = x + rows[t] * (int64_t)h;
+        for (int32_t j = 0; j < m; ++j) {
+            const int64_t e = experts[t * m + j];
+            double l = 0.0;
+            for (int32_t q = 0; q < h; ++q) {
+                const double xv = bf16_bits_to_double(xr[q]);
+                const double wv = bf16_bits_to_double(W[(int64_t)q * M + e]);
+                if (!isfinite(xv) || !isfinite(wv)) return ORACLE_ERR_NONFINITE;
+                l += xv * wv;
+            }
+            out[t * m + j] = l;
+        }
+    }
+    return ORACLE_OK;
 }
 
 /* counts[e] = number of (token, slot) pairs with idx == e.  Out-of-range ids -> error. */

@@ -101,12 +101,20 @@ class LowrankRouter:
             raise ValueError("shapes %s %s %s do not match the router's (T=%d, h=%d, r=%d, M=%d)"
                              % (tuple(x.shape), tuple(R1t.shape), tuple(R2t.shape), T, h, r, M))
         o = self.out
-        st = _lib.load().more_route_lowrank_ex(
-            _ptr(x), _ptr(R1t), _ptr(R2t), T, h, r, M, k, self.m_chunks, _ptr(o.idx),
-            _ptr(o.gate), _ptr(o.topval), _ptr(o.counts),
-            _ptr(self.workspace) if self.workspace_bytes else None, self.workspace_bytes,
-            _stream(x.device))
-        _lib.check(st, "more_route_lowrank_ex")
+        ws = _ptr(self.workspace) if self.workspace_bytes else None
+        lib = _lib.load()
+        if self.m_chunks == 0:  # the library's own plan: the plain entry point
+            st = lib.more_route_lowrank(_ptr(x), _ptr(R1t), _ptr(R2t), T, h, r, M, k,
+                                        _ptr(o.idx), _ptr(o.gate), _ptr(o.topval),
+                                        _ptr(o.counts), ws, self.workspace_bytes,
+                                        _stream(x.device))
+            _lib.check(st, "more_route_lowrank")
+        else:
+            st = lib.more_route_lowrank_ex(_ptr(x), _ptr(R1t), _ptr(R2t), T, h, r, M, k,
+                                           self.m_chunks, _ptr(o.idx), _ptr(o.gate),
+                                           _ptr(o.topval), _ptr(o.counts), ws,
+                                           self.workspace_bytes, _stream(x.device))
+            _lib.check(st, "more_route_lowrank_ex")
         return o
 
 

@@ -12,7 +12,9 @@ library) so the same checks can be run against deliberately broken builds of the
 * Thm-1 lift       -- the closed-form construction of the upper-bound proof;
 * Prop-1 top-1     -- the sign-pattern closed form of the load-balancing construction;
 * Prop-1 counts    -- the Bernstein bound of the load-balancing proposition;
-* histogram        -- counts equal numpy's bincount and sum to n k.
+* histogram        -- counts equal numpy's bincount and sum to n k;
+* logits at pairs  -- numpy BLAS logits at random (token, expert) pairs, including the
+                      first and last expert and repeated tokens (low-rank and full-rank).
 """
 from __future__ import annotations
 
@@ -202,6 +204,35 @@ def check_histogram(lib=None):
     assert c.sum() == idx.size
 
 
+# ------------------------------------------------------------------ logits at pairs
+def check_logits_at(lib=None, shapes=((50, 96, 16, 300), (7, 32, 48, 5), (33, 64, 64, 1000))):
+    for si, (T, h, r, M) in enumerate(shapes):
+        inp = make_inputs(T, h, r, M, seed=300 + si)
+        rng = np.random.default_rng(si)
+        rows = np.concatenate([np.arange(T), rng.integers(0, T, size=T)])
+        m = min(M, 6)
+        ex = rng.integers(0, M, size=(rows.size, m)).astype(np.int32)
+        ex[:, 0] = 0
+        ex[:, -1] = M - 1
+        got = oracle.logits_at(inp.x, inp.R1, inp.R2, rows, ex, lib=lib)
+        logits = (f64(inp.x) @ f64(inp.R1)) @ f64(inp.R2)
+        want = logits[rows[:, None], ex]
+        assert np.allclose(got, want, rtol=1e-12, atol=1e-12), "logits at pairs differ (shape %d)" % si
+
+
+def check_fullrank_logits_at(lib=None):
+    T, h, M = 30, 80, 50
+    inp = make_inputs(T, h, 16, M, seed=8)
+    rng = np.random.default_rng(4)
+    Wb = f32_to_bf16_bits(rng.standard_normal((h, M)).astype(np.float32) / 8)
+    rows = rng.integers(0, T, size=40)
+    ex = rng.integers(0, M, size=(40, 5)).astype(np.int32)
+    ex[:, 0] = M - 1
+    got = oracle.fullrank_logits_at(inp.x, Wb, rows, ex, lib=lib)
+    want = (f64(inp.x) @ f64(Wb))[rows[:, None], ex]
+    assert np.allclose(got, want, rtol=1e-12, atol=1e-12), "full-rank logits at pairs differ"
+
+
 ALL_CHECKS = [check_bruteforce, check_fullrank_bruteforce, check_identity, check_gates,
               check_equivariance, check_thm1, check_prop1_top1, check_prop1_counts,
-              check_histogram]
+              check_histogram, check_logits_at, check_fullrank_logits_at]

@@ -44,3 +44,10 @@ def test_traffic_record_is_dropped_when_sources_change(tmp_path, monkeypatch):
     assert bench.measured_traffic(w) == 1024 * (100 * 2 + 10)
     monkeypatch.setattr(bench, "kernel_source_digest", lambda: "1" * 64)
     assert bench.measured_traffic(w) is None
+
+
+def test_replay_split_times_exactly_the_requested_steps():
+    for steps in (1, 2, 5, 7, 20, 200, 97):
+        reps, per = bench.replay_split(steps)
+        assert reps * per == steps and 1 <= reps <= 10
+    assert bench.replay_split(20) == (10, 2)

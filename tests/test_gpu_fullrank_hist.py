@@ -3,7 +3,7 @@ import numpy as np
 import pytest
 
 import oracle
-import parity
+from oracle import parity
 from gpu_util import announce, require_gpu, to_dev
 from paper_2609_36301_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits, make_inputs
 
@@ -36,10 +36,9 @@ def test_fullrank_fp32_logits_parity(shape):
     inp = make_inputs(T, h, r, M, seed=5)
     Wb = _w_bf16(inp)
     idx, gate, topval = _fullrank(inp, Wb, k, 32, "fullrank")
-    rows = np.arange(T) if T <= 4096 else np.sort(
-        np.random.default_rng(0).choice(T, 3000, replace=False))
-    orc = oracle.route_fullrank(inp.x, Wb, k, rows=rows)
-    rep = parity.compare(orc, idx[rows], gate[rows], k, M)
+    orc = oracle.route_fullrank(inp.x, Wb, k)
+    picked = oracle.fullrank_logits_at(inp.x, Wb, np.arange(T), idx)
+    rep = parity.compare(orc, idx, gate, k, M, picked, topval)
     print("[parity] fullrank %s %s" % (shape, rep), flush=True)
     assert rep.ok(), str(rep)
 
@@ -48,8 +47,8 @@ def test_fullrank_bf16_logits_valid():
     T, h, r, M, k = 2000, 512, 32, 4096, 8
     inp = make_inputs(T, h, r, M, seed=6)
     Wb = _w_bf16(inp)
-    idx, gate, _ = _fullrank(inp, Wb, k, 16, "fullrank-bf16")
-    parity.check_valid(idx, gate, M)
+    idx, gate, topval = _fullrank(inp, Wb, k, 16, "fullrank-bf16")
+    parity.check_valid(idx, gate, M, topval)
     orc = oracle.route_fullrank(inp.x, Wb, k)
     same = np.all(np.sort(orc.idx, 1) == np.sort(idx, 1), axis=1)
     # bf16 logits carry 8 significant bits: most sets still agree

@@ -48,6 +48,15 @@ MUTANTS = {
     "fullrank_drops_last_hidden_term": (
         "for (int32_t j = 0; j < h; ++j) {\n                const double* wrow",
         "for (int32_t j = 0; j < h - 1; ++j) {\n                const double* wrow"),
+    "logits_at_drops_last_hidden_term": (
+        "for (int32_t i = 0; i < r; ++i) z[i] += xrow[j] * w1[i];",
+        "for (int32_t i = 0; i < r; ++i) z[i] += (j + 1 < h) * xrow[j] * w1[i];"),
+    "logits_at_wrong_expert_column": (
+        "l += z[i] * r2[(int64_t)i * M + e];",
+        "l += z[i] * r2[(int64_t)i * M + (e + 1) % M];"),
+    "fullrank_logits_at_transposed_W": (
+        "const double wv = bf16_bits_to_double(W[(int64_t)q * M + e]);",
+        "const double wv = bf16_bits_to_double(W[((int64_t)e * h + q) % ((int64_t)h * M)]);"),
     "histogram_off_by_one": (
         "counts[idx[i]] += 1;",
         "counts[(idx[i] + 1) % M] += 1;"),
