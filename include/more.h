@@ -143,6 +143,24 @@ more_status more_route_fullrank_workspace_size(int64_t T, int32_t h, int32_t M, 
 more_status more_expert_histogram(const int32_t* idx, int64_t T, int32_t k, int32_t M,
                                   int32_t* counts, void* stream);
 
+/*
+ * For callers that cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): more_route_lowrank without a workspace argument.  The
+ * scratch is a static device array of MORE_NOALLOC_SCRATCH_BYTES bytes per device, placed on
+ * a device by the first call there and held until the process ends; this call allocates and
+ * frees nothing.  Arguments, outputs and results are those of more_route_lowrank (bitwise
+ * identical).  A shape whose more_route_lowrank_workspace_size exceeds the array returns
+ * MORE_ERR_WORKSPACE before anything is launched.  Every call on a device shares its array:
+ * calls ordered on one stream are safe, calls that overlap in time on one device (other
+ * streams, other threads) race and give undefined results.  MORE_ERR_HIP when the array's
+ * device address cannot be obtained.
+ */
+#define MORE_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+more_status more_route_lowrank_noalloc(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
+                                       int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                       int32_t* idx, float* gate, float* topval, int32_t* counts,
+                                       void* stream);
+
 /* Static, never NULL. */
 const char* more_status_string(more_status s);
 

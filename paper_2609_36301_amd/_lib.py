@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmore.so"
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 K_MAX = 32
 LOWRANK_K_MAX = 16
+NOALLOC_SCRATCH_BYTES = 128 << 20
 
 # (name, restype, argtypes) for every symbol declared in include/more.h
 _P = ctypes.c_void_p
@@ -31,6 +32,8 @@ SIGNATURES = {
                                    _P]),
     "more_route_fullrank_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _I32, _PSZ]),
     "more_expert_histogram": (_I32, [_P, _I64, _I32, _I32, _P, _P]),
+    "more_route_lowrank_noalloc": (_I32, [_P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P,
+                                          _P, _P]),
     "more_status_string": (ctypes.c_char_p, [_I32]),
     "more_version": (ctypes.c_char_p, []),
 }

@@ -179,3 +179,17 @@ def test_binding_rejects_bad_tensors():
                              torch.zeros((8, 16), dtype=torch.bfloat16), 2)
     with pytest.raises(TypeError):
         router.route_lowrank(x.float(), x, x, 2)
+
+
+def test_noalloc_rejects_shapes_beyond_its_scratch(lib):
+    # checked on the host before anything is launched or looked up on a device
+    T, h, r, M, k = 200000, 64, 64, 20000, 8
+    n = ctypes.c_size_t(0)
+    assert lib.more_route_lowrank_workspace_size(T, h, r, M, k, ctypes.byref(n)) == _lib.OK
+    assert n.value > _lib.NOALLOC_SCRATCH_BYTES
+    assert lib.more_route_lowrank_noalloc(FAKE, FAKE, FAKE, T, h, r, M, k, FAKE, FAKE, None,
+                                          None, None) == _lib.ERR_WORKSPACE
+    assert lib.more_route_lowrank_noalloc(None, FAKE, FAKE, 10, h, r, M, k, FAKE, FAKE, None,
+                                          None, None) == _lib.ERR_INVALID_ARG
+    assert lib.more_route_lowrank_noalloc(FAKE, FAKE, FAKE, 0, h, r, M, k, FAKE, FAKE, None,
+                                          None, None) == _lib.OK
