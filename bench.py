@@ -51,10 +51,14 @@ SCOPE_FUSED = ("one routing call: the z pass and the fused route kernel (screen,
                "collect and finalize in one launch) (+ histogram), timed together as one step")
 SCOPE_LOCAL = ("one routing call: one launch of the local fused kernel (z pass, wave norm "
                "bounds, screen, threshold, collect and finalize) (+ histogram)")
-SCOPES = {"expert-resident": SCOPE_RESIDENT, "fused": SCOPE_FUSED, "fused-local": SCOPE_LOCAL}
+SCOPE_SINGLE = ("one routing call: the z + prescreen, collect and finalize kernels and the "
+                "histogram kernel, timed together as one step")
+SCOPES = {"expert-resident": SCOPE_RESIDENT, "fused": SCOPE_FUSED, "fused-local": SCOPE_LOCAL,
+          "single-pass": SCOPE_SINGLE}
 
 
-KERNEL_SOURCES = ("lowrank.hip", "lowrank.h", "device_common.h", "histogram.hip")
+KERNEL_SOURCES = ("lowrank.hip", "lowrank.h", "device_common.h", "route_device.h",
+                  "resident.hip", "histogram.hip")
 
 
 def kernel_source_digest():
@@ -245,10 +249,7 @@ def main():
     tm = timed_graph(step, args.steps, args.warmup)
     sec = tm["mean_s"]
     plan_chunks = router.lowrank_plan(w.T, w.h, w.r, w.M, w.k)
-    route = "expert-resident"
-    if plan_chunks == 0:  # fused; the local variant needs no workspace
-        local = router.lowrank_workspace_size(w.T, w.h, w.r, w.M, w.k) == 0
-        route = "fused-local" if local else "fused"
+    route = router.lowrank_route(w.T, w.h, w.r, w.M, w.k)
 
     result = {
         "metric": METRIC,

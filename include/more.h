@@ -96,7 +96,8 @@ more_status more_route_lowrank_workspace_size(int64_t T, int32_t h, int32_t r, i
  * bitwise identical results, and so does the fused route that reads the z pass (r M <= 2^18).
  * The one-launch fused route (r M <= 2^17 with K <= 8, and M <= 1024 at r = 64) computes z
  * inside the routing workgroup, summing the h axis in another order: its logits can differ from
- * the others' in the last bits (selections only where logits tie to rounding).  This entry
+ * the others' in the last bits (selections only where logits tie to rounding); so can those of
+ * the single-pass route, which m_chunks = 0 picks for T >= 4096 and M >= 32768.  This entry
  * point exists for tuning and for tests of these properties.  Its workspace size comes from
  * more_route_lowrank_workspace_size_ex with the same m_chunks (0 bytes for the one-launch
  * route).
@@ -111,10 +112,22 @@ more_status more_route_lowrank_workspace_size_ex(int64_t T, int32_t h, int32_t r
 
 /* The m_chunks value the library picks for this shape (written to *m_chunks, host): the
  * number of expert-axis slices of the expert-resident route, or 0 when the library routes this
- * shape with a fused route (expert sets with r * M <= 2^18 and M <= 16384: one workgroup per 64
- * tokens sweeps all experts; see more_route_lowrank_ex). */
+ * shape with a route that no m_chunks >= 1 selects: a fused route (expert sets with
+ * r * M <= 2^18 and M <= 16384: one workgroup per 64 tokens sweeps all experts) or the
+ * single-pass route (T >= 4096 and M >= 32768: one screening sweep over all experts after a
+ * prescreen of an eighth of them; see more_route_lowrank_ex). */
 more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
                                     int32_t* m_chunks);
+
+/* The route more_route_lowrank takes for this shape (written to *route, host): one of the
+ * MORE_ROUTE_* codes below.  Routes differ in speed and in the summation order of z = x R1 (see
+ * more_route_lowrank_ex); every route returns the exact top k of its own fp32 logits. */
+#define MORE_ROUTE_RESIDENT 0    /* z pass; screen, threshold, collect and finalize per chunk  */
+#define MORE_ROUTE_FUSED 1       /* z pass; one fused kernel per 64 tokens over all experts     */
+#define MORE_ROUTE_FUSED_LOCAL 2 /* one launch: the fused kernel also computes z                */
+#define MORE_ROUTE_SINGLE_PASS 3 /* z + prescreen, one collect sweep, finalize (+ histogram)    */
+more_status more_route_lowrank_route(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                     int32_t* route);
 
 /*
  * Full-rank (standard) router, the baseline (Section "Preliminaries": softmax(TopK(R x)) with

@@ -8,7 +8,8 @@ a ctypes binding with torch tensors (`router`), and the seeded input generator (
     out = route_lowrank(x, R1t, R2t, k)      # out.idx [T][k] int32, out.gate [T][k] fp32
 """
 __all__ = ["route_lowrank", "route_fullrank", "expert_histogram", "LowrankRouter",
-           "lowrank_workspace_size", "lowrank_plan", "fullrank_workspace_size", "Routing"]
+           "lowrank_workspace_size", "lowrank_plan", "lowrank_route", "fullrank_workspace_size",
+           "Routing"]
 
 
 def __getattr__(name):

@@ -18,7 +18,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmore.so")
-SOURCES = ["lowrank.hip", "fullrank.hip", "histogram.hip", "noalloc.hip", "more_api.cpp"]
+SOURCES = ["lowrank.hip", "resident.hip", "fullrank.hip", "histogram.hip", "noalloc.hip",
+           "more_api.cpp"]
 ARCH = "gfx950"
 
 
@@ -38,7 +39,7 @@ def compile_flags() -> list[str]:
 
 # Per-source extra flags.  The router kernels never see NaN (inputs are finite, masked logits
 # are -inf), so fmaxf/fminf need no NaN quieting.
-EXTRA_FLAGS = {"lowrank.hip": ["-fno-honor-nans"]}
+EXTRA_FLAGS = {"lowrank.hip": ["-fno-honor-nans"], "resident.hip": ["-fno-honor-nans"]}
 
 
 def _compile(src: str) -> str:

@@ -1,8 +1,9 @@
 // Per-expert selection counts (the bincount behind the load-balancing statistic f,
 // Appendix "Training"): counts[e] = #{(t, j) : idx[t][j] == e}.
 //
-// Each workgroup counts one slice of the ids for one range of 16384 experts in an LDS
-// histogram and flushes it with one global atomic per non-empty bin.  Counts are cleared by a
+// Up to 2048 experts, each workgroup counts one slice of the ids in an LDS histogram and
+// flushes it with one global atomic per non-empty bin; larger expert sets use an LDS hash table
+// per slice instead.  Counts are cleared by a
 // fill kernel (not a memset) so the sequence stays valid inside a captured HIP graph; the
 // routing call clears them in its threshold kernel instead.
 #include <hip/hip_runtime.h>
@@ -46,6 +47,44 @@ __global__ __launch_bounds__(256) void histogram_lds_kernel(const int32_t* __res
     }
 }
 
+// Larger expert sets (M > kHashMinExperts): each workgroup aggregates one slice of kHashSlice
+// ids in an LDS hash table (linear probing, twice as many slots as ids) and adds every distinct
+// expert of the slice to counts with one global atomic, so an expert chosen by many tokens gets
+// one atomic per slice instead of one per selection.
+constexpr int kHashSlice = 1024;
+constexpr int kHashSlots = 2 * kHashSlice;  // power of two
+constexpr int32_t kHashMinExperts = 2048;   // smaller sets: dense LDS bins
+
+__global__ __launch_bounds__(256) void histogram_hash_kernel(const int32_t* __restrict__ idx,
+                                                             int64_t n, int32_t M,
+                                                             int32_t* __restrict__ counts) {
+    __shared__ int32_t key[kHashSlots], cnt[kHashSlots];
+    for (int i = threadIdx.x; i < kHashSlots; i += blockDim.x) {
+        key[i] = -1;
+        cnt[i] = 0;
+    }
+    __syncthreads();
+    const int64_t i0 = (int64_t)blockIdx.x * kHashSlice;
+    const int64_t i1 = i0 + kHashSlice < n ? i0 + kHashSlice : n;
+    for (int64_t i = i0 + threadIdx.x; i < i1; i += blockDim.x) {
+        const int32_t e = idx[i];
+        if (e < 0 || e >= M) continue;
+        uint32_t hh = ((uint32_t)e * 2654435761u) & (kHashSlots - 1);
+        // at most kHashSlice distinct keys in kHashSlots slots: a free or matching slot exists
+        for (int probe = 0; probe < kHashSlots; ++probe) {
+            const int32_t old = atomicCAS(&key[hh], -1, e);
+            if (old == -1 || old == e) {
+                atomicAdd(&cnt[hh], 1);
+                break;
+            }
+            hh = (hh + 1) & (kHashSlots - 1);
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kHashSlots; i += blockDim.x)
+        if (key[i] >= 0) atomicAdd(&counts[key[i]], cnt[i]);
+}
+
 hipError_t histogram_launch(const int32_t* idx, int64_t n, int32_t M, int32_t* counts,
                             hipStream_t st, bool counts_zeroed) {
     if (!counts_zeroed) {
@@ -54,7 +93,10 @@ hipError_t histogram_launch(const int32_t* idx, int64_t n, int32_t M, int32_t* c
         hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)blocks), dim3(256), 0, st, counts,
                            (int64_t)M);
     }
-    if (n > 0) {
+    if (n > 0 && M > kHashMinExperts) {
+        hipLaunchKernelGGL(histogram_hash_kernel, dim3((unsigned)((n + kHashSlice - 1) / kHashSlice)),
+                           dim3(256), 0, st, idx, n, M, counts);
+    } else if (n > 0) {
         const int64_t ranges = ((int64_t)M + kLdsBins - 1) / kLdsBins;
         int64_t slices = n / 4096;
         const int64_t max_slices = 256 / ranges > 1 ? 256 / ranges : 1;

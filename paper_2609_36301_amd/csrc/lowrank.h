@@ -23,8 +23,33 @@ struct LowrankPlan {
     int32_t hsplit;           // workgroups sharing the h axis of one token group in the z pass
     int32_t steps_per_split;  // 64-wide h chunks per z-pass workgroup
     size_t off_zparts, off_z, off_zhi, off_cz, off_top, off_gnorm, off_tau, off_count, off_cand;
+    // single-pass route (zscreen, collect and finalize kernels of resident.hip)
+    int32_t single_pass;      // 1: this route
+    int32_t sub_tiles;        // expert tiles of the prescreen
+    int32_t slots;            // entry slots per lane and token group in the collect kernel
+    size_t off_theta0, off_rec, off_scratch;
     size_t workspace_bytes;
 };
+
+// Arguments of the single-pass route (pointers into the caller's buffers and workspace).
+struct SinglePassArgs {
+    const uint16_t *x, *R1t, *R2t;
+    int32_t T, h, r, M, k;
+    float* z;
+    uint16_t* zhi;
+    float *cz, *theta0;
+    int32_t* count;
+    int2* rec;
+    void* scratch;
+    int32_t* hist;
+    int32_t* idx;
+    float *gate, *topval;
+};
+
+hipError_t single_pass_launch(const LowrankPlan& plan, const SinglePassArgs& a, hipStream_t stream);
+
+// Bytes of the collect kernel's entry scratch for `grid` workgroups.
+size_t collect_scratch_bytes(int64_t grid, int32_t slots);
 
 // Returns false when m_chunks is not 0, 1 or a multiple of 8 up to 1024.
 bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, int32_t m_chunks,

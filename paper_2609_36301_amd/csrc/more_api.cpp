@@ -79,7 +79,21 @@ more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, 
     if (s != MORE_OK) return s;
     more::LowrankPlan p;
     if (!more::lowrank_make_plan(T > 0 ? T : 1, h, r, M, k, 0, &p)) return MORE_ERR_INVALID_ARG;
-    *m_chunks = p.fused ? 0 : p.chunks;
+    *m_chunks = p.fused || p.single_pass ? 0 : p.chunks;
+    return MORE_OK;
+}
+
+more_status more_route_lowrank_route(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                     int32_t* route) {
+    if (!route) return MORE_ERR_INVALID_ARG;
+    more_status s = check_lowrank(T, h, r, M, k, 0);
+    if (s != MORE_OK) return s;
+    more::LowrankPlan p;
+    if (!more::lowrank_make_plan(T > 0 ? T : 1, h, r, M, k, 0, &p)) return MORE_ERR_INVALID_ARG;
+    *route = p.single_pass ? MORE_ROUTE_SINGLE_PASS
+             : p.local     ? MORE_ROUTE_FUSED_LOCAL
+             : p.fused     ? MORE_ROUTE_FUSED
+                           : MORE_ROUTE_RESIDENT;
     return MORE_OK;
 }
 

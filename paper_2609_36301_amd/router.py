@@ -55,11 +55,23 @@ def lowrank_workspace_size(T: int, h: int, r: int, M: int, k: int, m_chunks: int
 
 
 def lowrank_plan(T: int, h: int, r: int, M: int, k: int) -> int:
-    """Number of expert-axis chunks the library picks for this shape (0: the fused route)."""
+    """Number of expert-axis chunks the library picks for this shape (0: the fused or the
+    single-pass route, which no m_chunks >= 1 selects)."""
     c = ctypes.c_int32(0)
     _lib.check(_lib.load().more_route_lowrank_plan(T, h, r, M, k, ctypes.byref(c)),
                "more_route_lowrank_plan")
     return c.value
+
+
+ROUTE_NAMES = {0: "expert-resident", 1: "fused", 2: "fused-local", 3: "single-pass"}
+
+
+def lowrank_route(T: int, h: int, r: int, M: int, k: int) -> str:
+    """Name of the route more_route_lowrank takes for this shape."""
+    c = ctypes.c_int32(0)
+    _lib.check(_lib.load().more_route_lowrank_route(T, h, r, M, k, ctypes.byref(c)),
+               "more_route_lowrank_route")
+    return ROUTE_NAMES[c.value]
 
 
 def fullrank_workspace_size(T: int, h: int, M: int, k: int, logit_bits: int = 32) -> int:

@@ -139,10 +139,26 @@ def test_plans_for_the_paper_shapes(lib):
             assert C == 0, name
             assert -(-T // 64) >= 256, name
             continue
+        if T >= 4096 and M >= 32768:  # single-pass route
+            assert C == 0, name
+            continue
         tokens_per_block = 1024 if (k <= 8 and r == 64) else 512  # 8 waves x 32 x (4 or 2)
         assert C & (C - 1) == 0, name
         assert r * M * 2 // C <= 2 << 20, name          # expert slice fits one L2
         assert C * -(-T // tokens_per_block) >= 256, name  # at least one workgroup per CU
+
+
+def test_routes_for_the_paper_shapes(lib):
+    from paper_2609_36301_amd import router
+    want = {(16384, 512, 32, 4096, 8): "fused-local", (32768, 2048, 64, 16384, 8): "expert-resident",
+            (16384, 4096, 64, 65536, 8): "single-pass", (128, 4096, 64, 262144, 16): "expert-resident",
+            (4096, 256, 32, 32768, 8): "single-pass", (4095, 256, 32, 32768, 8): "expert-resident",
+            (4096, 256, 32, 32767, 8): "expert-resident"}
+    for shape, name in want.items():
+        assert router.lowrank_route(*shape) == name, shape
+    c = ctypes.c_int32(0)
+    assert lib.more_route_lowrank_route(100, 64, 48, 1000, 4, ctypes.byref(c)) == _lib.ERR_UNSUPPORTED
+    assert lib.more_route_lowrank_route(100, 64, 32, 1000, 4, None) == _lib.ERR_INVALID_ARG
 
 
 def test_fullrank_validation(lib):
