@@ -1,9 +1,9 @@
 // Per-expert selection counts (the bincount behind the load-balancing statistic f,
 // Appendix "Training"): counts[e] = #{(t, j) : idx[t][j] == e}.
 //
-// Up to 2048 experts, each workgroup counts one slice of the ids in an LDS histogram and
+// Up to 16384 experts, each workgroup counts one slice of the ids in an LDS histogram and
 // flushes it with one global atomic per non-empty bin; larger expert sets use an LDS hash table
-// per slice instead.  Counts are cleared by a
+// per slice instead (one pass over the ids rather than one per range of 16384 bins).  Counts are cleared by a
 // fill kernel (not a memset) so the sequence stays valid inside a captured HIP graph; the
 // routing call clears them in its threshold kernel instead.
 #include <hip/hip_runtime.h>
@@ -53,7 +53,7 @@ __global__ __launch_bounds__(256) void histogram_lds_kernel(const int32_t* __res
 // one atomic per slice instead of one per selection.
 constexpr int kHashSlice = 1024;
 constexpr int kHashSlots = 2 * kHashSlice;  // power of two
-constexpr int32_t kHashMinExperts = 2048;   // smaller sets: dense LDS bins
+constexpr int32_t kHashMinExperts = kLdsBins;  // up to one LDS bin range: dense bins
 
 __global__ __launch_bounds__(256) void histogram_hash_kernel(const int32_t* __restrict__ idx,
                                                              int64_t n, int32_t M,

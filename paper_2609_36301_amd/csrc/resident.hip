@@ -599,12 +599,13 @@ __global__ __launch_bounds__(kRouteThreads, 1) void collect_kernel1(
 }
 
 // ------------------------------------------------------------------------------ finalize
-// Sixteen lanes per token and sixteen tokens per workgroup of 256 threads.  Lane sub of token j
-// keeps records sub, sub + 16, ... of the token's list in registers (one round of 256; longer
-// lists are walked in rounds, reloaded for each pass).  Per token:
+// Sixteen lanes per token and sixteen tokens per workgroup of 256 threads (eight lanes and
+// twice the records per lane measured slower, despite twice the tokens in flight per CU).  Lane
+// sub of token j keeps records sub, sub + 16, ... of the token's list in registers (one round
+// of 256; longer lists are walked in rounds, reloaded for each pass).  Per token:
 //  1. kub: each lane offers the two largest upper bounds of its records; kub = the
-//     min(3k, n, 32)-th largest of those (at most 32) values, so at least that many records reach
-//     it (3k rather than k: pass 1 below is then rarely needed);
+//     min(2k, n)-th largest of those (at most 32) values, so at least that many (>= k) records
+//     reach it;
 //  2. pass 0: the records with ub >= kub are evaluated exactly (z from LDS, the rows of two
 //     candidates per lane loaded together) into the token's candidate table in LDS; each
 //     candidate's rank under the selection order is counted against the others, and theta1 = the
@@ -681,8 +682,8 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel2(
         u2[j * 2 * kFinLanes + kFinLanes + sub] = m2;
     }
     __syncthreads();
-    int nk = 3 * k < n ? 3 * k : n;
-    nk = nk < 2 * kFinLanes ? nk : 2 * kFinLanes;
+    int nk = 2 * k < n ? 2 * k : n;
+    nk = nk < 2 * kFinLanes ? nk : 2 * kFinLanes;  // >= k: k <= 16 <= 2 kFinLanes
     if (live) {
         const float a = u2[j * 2 * kFinLanes + sub], b = u2[j * 2 * kFinLanes + kFinLanes + sub];
         int ga = 0, gb = 0, ea = 0, eb = 0;
@@ -700,6 +701,10 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel2(
     const float kub = thr[j];
     // exact logits of candidates cl = experts e0, e1 into table slots i0, i1 (i1 < 0: none)
     auto eval2 = [&](int32_t e0, int i0, int32_t e1, int i1) __attribute__((always_inline)) {
+        // table entries are written before they are read; the clamp keeps any row address in
+        // bounds regardless
+        e0 = (uint32_t)e0 < (uint32_t)M ? e0 : 0;
+        e1 = (uint32_t)e1 < (uint32_t)M ? e1 : 0;
         bf16x8 w0[2 * RC], w1[2 * RC];
 #pragma unroll
         for (int c = 0; c < 2 * RC; ++c) {
@@ -750,8 +755,8 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel2(
         }
     };
     // 2. pass 0 (lo = kub, hi = inf) and 3. pass 1 (lo = theta1, hi = kub): the selected records
-    //    are appended to the table (positions from a prefix sum over the token's 16 lanes, which
-    //    form one DPP row), evaluated, and ranked
+    //    are appended to the table (positions from a prefix sum over the token's lanes, within
+    //    one 16-lane DPP row), evaluated, and ranked
     float lo = kub, hi = __builtin_huge_valf();
     int cnt = 0;
 #pragma nounroll
@@ -767,10 +772,19 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel2(
             }
             const int c = __builtin_popcount(m);
             int incl = c;  // inclusive prefix over the row
-            incl += __builtin_amdgcn_update_dpp(0, incl, 0x111, 0xF, 0xF, false);  // row_shr:1
-            incl += __builtin_amdgcn_update_dpp(0, incl, 0x112, 0xF, 0xF, false);  // row_shr:2
-            incl += __builtin_amdgcn_update_dpp(0, incl, 0x114, 0xF, 0xF, false);  // row_shr:4
-            incl += __builtin_amdgcn_update_dpp(0, incl, 0x118, 0xF, 0xF, false);  // row_shr:8
+            // row_shr:d reads lane - d of the 16-lane DPP row.  Each move runs with all of the
+            // token's lanes active (a lane whose source lane is inactive would read 0), and its
+            // value is then dropped where the source lies in another token or outside the row.
+            const int s1 = __builtin_amdgcn_update_dpp(0, incl, 0x111, 0xF, 0xF, false);
+            incl += sub >= 1 ? s1 : 0;
+            const int s2 = __builtin_amdgcn_update_dpp(0, incl, 0x112, 0xF, 0xF, false);
+            incl += sub >= 2 ? s2 : 0;
+            const int s4 = __builtin_amdgcn_update_dpp(0, incl, 0x114, 0xF, 0xF, false);
+            incl += sub >= 4 ? s4 : 0;
+            if constexpr (kFinLanes > 8) {
+                const int s8 = __builtin_amdgcn_update_dpp(0, incl, 0x118, 0xF, 0xF, false);
+                incl += sub >= 8 ? s8 : 0;
+            }
             int o = base + incl - c;
 #pragma unroll
             for (int b = 0; b < kFinRegs; ++b) {
@@ -844,7 +858,7 @@ __global__ __launch_bounds__(kFinThreads) void finalize_kernel2(
         }
 #pragma unroll
         for (int i = 0; i < K; ++i)
-            if (i < k && i == sub) gate[tok * k + i] = e[i] / sum;
+            if (i < k && i % kFinLanes == sub) gate[tok * k + i] = e[i] / sum;
     }
     // Tokens left over (an overflowed record list or candidate table; rare): the whole workgroup
     // sweeps all experts, thread tid taking experts tid, tid + kFinThreads, ...
