@@ -168,7 +168,7 @@ more_status more_expert_histogram(const int32_t* idx, int64_t T, int32_t k, int3
  * streams, other threads) race and give undefined results.  MORE_ERR_HIP when the array's
  * device address cannot be obtained.
  */
-#define MORE_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+#define MORE_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
 more_status more_route_lowrank_noalloc(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
                                        int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
                                        int32_t* idx, float* gate, float* topval, int32_t* counts,

@@ -199,7 +199,7 @@ def test_binding_rejects_bad_tensors():
 
 def test_noalloc_rejects_shapes_beyond_its_scratch(lib):
     # checked on the host before anything is launched or looked up on a device
-    T, h, r, M, k = 200000, 64, 64, 20000, 8
+    T, h, r, M, k = 1 << 20, 64, 16, 65536, 8
     n = ctypes.c_size_t(0)
     assert lib.more_route_lowrank_workspace_size(T, h, r, M, k, ctypes.byref(n)) == _lib.OK
     assert n.value > _lib.NOALLOC_SCRATCH_BYTES

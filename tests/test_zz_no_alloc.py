@@ -1,5 +1,5 @@
 """The no-allocation entry point through the C ABI (marked `gpu`): two calls in a row, the
-second on a smaller input, each bitwise equal to more_route_lowrank with a torch-allocated
+second on a smaller input (single-pass route, then resident route), each bitwise equal to more_route_lowrank with a torch-allocated
 workspace, and in oracle parity."""
 import ctypes
 
@@ -37,8 +37,9 @@ def test_noalloc_matches_the_workspace_entry_point_on_two_calls():
     from paper_2609_36301_amd import _lib
     require_gpu()
     lib = _lib.load()
-    # the second call is smaller: it runs on scratch that still holds the first call's data
-    for shape in ((3000, 512, 64, 40000, 8), (700, 256, 32, 9000, 16)):
+    # the first call takes the single-pass route, the second (smaller) the resident route, on
+    # scratch that still holds the first call's data
+    for shape in ((4096, 512, 64, 40000, 8), (700, 256, 32, 9000, 16)):
         T, h, r, M, k = shape
         inp = make_inputs(T, h, r, M, seed=T + 11 * M)
         R1t, R2t = transposed_factors(inp)
