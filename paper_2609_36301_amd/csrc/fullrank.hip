@@ -4,9 +4,9 @@
 //
 //   1. hipBLASLt GEMM  L[T][M] = x[T][h] * Wt[M][h]^T, fp32 accumulate, fp32 or bf16 output,
 //      into the caller's workspace;
-//   2. rows_topk: one wave per token row; each lane scans its strided share of the row
-//      keeping a sorted register list, then a butterfly of list merges across the wave;
-//      lane 0 applies the softmax and stores the row.
+//   2. rows_topk: one wave per token row; each lane scans its strided share of the row in
+//      16-byte pieces keeping a sorted register list, then a butterfly of list merges across
+//      the wave; lane 0 applies the softmax and stores the row.
 #include <hip/hip_runtime.h>
 #include <hipblaslt/hipblaslt.h>
 #include <stdint.h>
@@ -20,19 +20,59 @@
 
 namespace more {
 
+// One wave per token row.  When a row starts on a 16-byte boundary (M a multiple of 8 for bf16
+// logits, of 4 for fp32), lane l reads 16-byte pieces l, l + 64, ..., four pieces in flight,
+// and tests a piece's largest value against the lane's K-th before looking at its elements
+// (after the first few hundred logits almost no piece has a candidate), so the loop runs at
+// the rate the logits stream in.  Other rows take one logit per lane and step.  Each lane
+// visits its ids in increasing order, so a strict > keeps the smaller id on equal logits.
 template <int K, bool BF16>
 __global__ __launch_bounds__(256) void rows_topk_kernel(const void* __restrict__ logits, int32_t T,
                                                         int32_t M, int32_t k,
                                                         int32_t* __restrict__ idx,
                                                         float* __restrict__ gate,
                                                         float* __restrict__ topval) {
+    constexpr int PER = BF16 ? 8 : 4;  // logits per 16-byte piece
+    constexpr int U = 4;               // pieces in flight per lane
     const int lane = threadIdx.x & 63;
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (row >= T) return;  // wave-uniform
     float v[K];
     int32_t ix[K];
     list_init<K>(v, ix);
-    if (BF16) {
+    if (M % PER == 0) {
+        const u32x4* P = reinterpret_cast<const u32x4*>(
+            static_cast<const char*>(logits) + row * (int64_t)M * (BF16 ? 2 : 4));
+        const int32_t np = M / PER;
+        for (int32_t c0 = lane; c0 < np; c0 += 64 * U) {
+            u32x4 q[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t c = c0 + 64 * u;
+                q[u] = P[c < np ? c : np - 1];  // past the end: a reload, masked below
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t c = c0 + 64 * u;
+                float x[PER];
+#pragma unroll
+                for (int t = 0; t < PER; ++t) {
+                    const uint32_t w = q[u][BF16 ? t / 2 : t];
+                    x[t] = BF16 ? __builtin_bit_cast(float, (t & 1) ? (w & 0xFFFF0000u) : (w << 16))
+                                : __builtin_bit_cast(float, w);
+                    if (c >= np) x[t] = -__builtin_huge_valf();
+                }
+                float mx = x[0];
+#pragma unroll
+                for (int t = 1; t < PER; ++t) mx = fmaxf(mx, x[t]);
+                if (mx > v[K - 1]) {
+#pragma unroll
+                    for (int t = 0; t < PER; ++t)
+                        if (x[t] > v[K - 1]) list_insert_newer<K>(v, ix, x[t], c * PER + t);
+                }
+            }
+        }
+    } else if (BF16) {
         const uint16_t* L = static_cast<const uint16_t*>(logits) + row * M;
 #pragma unroll 4
         for (int32_t e = lane; e < M; e += 64) {

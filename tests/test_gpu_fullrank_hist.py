@@ -29,7 +29,8 @@ def _fullrank(inp, Wb, k, bits, tag):
 
 
 @pytest.mark.parametrize("shape", [(16384, 512, 32, 4096, 8), (333, 128, 16, 1000, 5),
-                                   (64, 64, 16, 33, 32), (1, 32, 16, 7, 1)],
+                                   (500, 128, 16, 2048, 32), (64, 64, 16, 33, 32),
+                                   (1, 32, 16, 7, 1)],
                          ids=lambda s: "T%d_h%d_M%d_k%d" % (s[0], s[1], s[3], s[4]))
 def test_fullrank_fp32_logits_parity(shape):
     T, h, r, M, k = shape
@@ -43,8 +44,12 @@ def test_fullrank_fp32_logits_parity(shape):
     assert rep.ok(), str(rep)
 
 
-def test_fullrank_bf16_logits_valid():
-    T, h, r, M, k = 2000, 512, 32, 4096, 8
+@pytest.mark.parametrize("shape", [(2000, 512, 32, 4096, 8), (700, 256, 32, 1003, 16)],
+                         ids=lambda s: "T%d_M%d_k%d" % (s[0], s[3], s[4]))
+def test_fullrank_bf16_logits_valid(shape):
+    """Rows of 4096 bf16 logits take the 16-byte path of the row top-k, rows of 1003 the
+    one-logit path."""
+    T, h, r, M, k = shape
     inp = make_inputs(T, h, r, M, seed=6)
     Wb = _w_bf16(inp)
     idx, gate, topval = _fullrank(inp, Wb, k, 16, "fullrank-bf16")
