@@ -11,6 +11,8 @@ Functions and the passage they follow:
   route_lowrank   softmax(TopK(x R1 R2)), the MoRE router ("Preliminaries", MoRE layer)
   route_fullrank  softmax(TopK(x W)), the standard router ("Preliminaries")
   histogram       per-expert selection counts (Appendix "Training", statistic f)
+  dispatch_sort   "Sort + Count": positions grouped by expert plus offsets (MoE layer
+                  forward pass, efficiency appendix)
   logits_at       the logits x R1 R2 at given (token, expert) pairs ("Preliminaries"), to
                   check a selection made elsewhere expert by expert
   fullrank_logits_at  the same for the full-rank logits x W (W as bf16 bits)
@@ -55,6 +57,7 @@ def load_library(path: str):
         fn.argtypes = [P, P, i64, i32, i32, i32, P, i64, P, P, P, P, i32]
         fn.restype = ctypes.c_int
     lib.oracle_histogram.argtypes = [P, i64, i32, i32, P]
+    lib.oracle_dispatch_sort.argtypes = [P, i64, i32, i32, P, P]
     lib.oracle_histogram.restype = ctypes.c_int
     lib.oracle_logits_at.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, P, i32, P, i32]
     lib.oracle_logits_at.restype = ctypes.c_int
@@ -206,3 +209,17 @@ def histogram(idx, M: int, lib=None) -> np.ndarray:
     counts = np.zeros(M, np.int64)
     _check(_load(lib).oracle_histogram(_ptr(idx), idx.shape[0], idx.shape[1], M, _ptr(counts)))
     return counts
+
+
+def dispatch_sort(idx, M: int, lib=None):
+    """(offsets [M + 1], sorted [n k]) of the entries of idx ([n][k] int32): positions
+    p = t k + j grouped by expert id (ids outside [0, M) last), increasing within a group;
+    offsets[e] = number of entries with a smaller key.  int64 arrays."""
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    if idx.ndim != 2:
+        raise ValueError("idx must be [n][k]")
+    offsets = np.zeros(M + 1, np.int64)
+    srt = np.zeros(idx.size, np.int64)
+    _check(_load(lib).oracle_dispatch_sort(_ptr(idx), idx.shape[0], idx.shape[1], M,
+                                           _ptr(offsets), _ptr(srt)))
+    return offsets, srt

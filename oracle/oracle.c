@@ -25,6 +25,9 @@
  * selections (bincount of the chosen indices, Appendix "Training", load-balancing
  * statistic f).
  *
+ * oracle_dispatch_sort is the dispatch bookkeeping that consumes a selection: the selected
+ * (token, slot) positions grouped by expert, with per-expert offsets.
+ *
  * oracle_logits_at evaluates steps 2-3 at given (token, expert) pairs only, so that a
  * selection made by another implementation can be checked expert by expert;
  * oracle_fullrank_logits_at does the same for the full-rank logits x W.
@@ -350,6 +353,42 @@ int oracle_fullrank_logits_at(const uint16_t* x, const uint16_t* W, int64_t T, i
 }
 
 /* counts[e] = number of (token, slot) pairs with idx == e.  Out-of-range ids -> error. */
+/*
+ * Dispatch bookkeeping of the MoE layer ("Sort + Count" of the layer's forward-pass figure in the
+ * efficiency appendix: the (N, k) expert ids become N k sorted positions plus per-expert
+ * offsets).  The N k entries of idx are numbered p = t k + j in row-major order.  Each entry's
+ * key is its expert id, or M for an id outside [0, M) (such entries go after every expert).
+ *   offsets[e] = number of entries whose key is below e, for e = 0 .. M (offsets[M] is the
+ *                number of valid entries);
+ *   sorted[i]  = the positions ordered by key, positions in increasing order within a key
+ *                (a stable counting sort: each key's entries are placed in position order,
+ *                starting at its offset).
+ * offsets int64 [M + 1]; sorted int64 [N k].
+ */
+/* Key of an entry: its expert id, or M when the id lies outside [0, M). */
+static int32_t dispatch_key(int32_t e, int32_t M) { return (e >= 0 && e < M) ? e : M; }
+
+int oracle_dispatch_sort(const int32_t* idx, int64_t n, int32_t k, int32_t M, int64_t* offsets,
+                         int64_t* sorted) {
+    if (!idx || !offsets || !sorted || n < 0 || k < 1 || M < 1) return ORACLE_ERR_ARG;
+    const int64_t N = n * (int64_t)k;
+    int64_t* start = (int64_t*)calloc((size_t)M + 2, sizeof(int64_t));
+    if (!start) return ORACLE_ERR_NOMEM;
+    /* count the entries of each key */
+    for (int64_t p = 0; p < N; ++p) start[dispatch_key(idx[p], M) + 1] += 1;
+    /* first slot of each key: the number of entries with a smaller key */
+    for (int32_t e = 0; e <= M; ++e) start[e + 1] += start[e];
+    for (int32_t e = 0; e <= M; ++e) offsets[e] = start[e];
+    /* place the positions in increasing order */
+    for (int64_t p = 0; p < N; ++p) {
+        const int32_t key = dispatch_key(idx[p], M);
+        sorted[start[key]] = p;
+        start[key] += 1;
+    }
+    free(start);
+    return ORACLE_OK;
+}
+
 int oracle_histogram(const int32_t* idx, int64_t n, int32_t k, int32_t M, int64_t* counts) {
     if (!idx || !counts || n < 0 || k < 1 || M < 1) return ORACLE_ERR_ARG;
     for (int32_t e = 0; e < M; ++e) counts[e] = 0;

@@ -204,6 +204,35 @@ def check_histogram(lib=None):
     assert c.sum() == idx.size
 
 
+# ------------------------------------------------------------------ dispatch sort
+def check_dispatch_sort(lib=None):
+    """Against numpy's stable argsort and bincount, plus the invariants of the definition
+    (a permutation, keys non-decreasing along it, positions increasing within a key)."""
+    rng = np.random.default_rng(21)
+    cases = [(rng.integers(0, 300, size=(500, 7)), 300),
+             (rng.integers(-3, 70, size=(129, 4)), 64),     # some ids outside [0, M)
+             (np.zeros((40, 3), np.int64), 5),              # one expert for every entry
+             (np.full((10, 2), 9, np.int64), 9),            # only out-of-range ids
+             (rng.integers(0, 1, size=(0, 5)), 8),          # no tokens
+             (rng.integers(0, 1, size=(33, 1)), 1)]         # M = 1
+    for idx, M in cases:
+        idx = idx.astype(np.int32)
+        offsets, srt = oracle.dispatch_sort(idx, M, lib=lib)
+        flat = idx.ravel()
+        key = np.where((flat >= 0) & (flat < M), flat, M)
+        assert np.array_equal(srt, np.argsort(key, kind="stable"))
+        want = np.concatenate([[0], np.cumsum(np.bincount(key, minlength=M + 1))])[:M + 1]
+        assert np.array_equal(offsets, want)
+        assert np.array_equal(np.sort(srt), np.arange(flat.size))
+        ks = key[srt]
+        assert np.all(np.diff(ks) >= 0)
+        same = np.diff(ks) == 0
+        assert np.all(np.diff(srt)[same] > 0)
+        for e in range(M):  # group e is exactly offsets[e] .. offsets[e + 1]
+            hi = offsets[e + 1] if e + 1 <= M - 1 else offsets[M] if e + 1 == M else flat.size
+            assert np.all(ks[offsets[e]:hi] == e)
+
+
 # ------------------------------------------------------------------ logits at pairs
 def check_logits_at(lib=None, shapes=((50, 96, 16, 300), (7, 32, 48, 5), (33, 64, 64, 1000))):
     for si, (T, h, r, M) in enumerate(shapes):
@@ -233,6 +262,7 @@ def check_fullrank_logits_at(lib=None):
     assert np.allclose(got, want, rtol=1e-12, atol=1e-12), "full-rank logits at pairs differ"
 
 
-ALL_CHECKS = [check_bruteforce, check_fullrank_bruteforce, check_identity, check_gates,
+ALL_CHECKS = [check_dispatch_sort, check_bruteforce, check_fullrank_bruteforce, check_identity,
+              check_gates,
               check_equivariance, check_thm1, check_prop1_top1, check_prop1_counts,
               check_histogram, check_logits_at, check_fullrank_logits_at]

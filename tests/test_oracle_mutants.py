@@ -15,6 +15,15 @@ import oracle_pins
 SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
 
 MUTANTS = {
+    "dispatch_positions_reversed": (
+        "    for (int64_t p = 0; p < N; ++p) {\n        const int32_t key = dispatch_key(idx[p], M);",
+        "    for (int64_t p = N - 1; p >= 0; --p) {\n        const int32_t key = dispatch_key(idx[p], M);"),
+    "dispatch_offsets_inclusive": (
+        "for (int32_t e = 0; e <= M; ++e) offsets[e] = start[e];",
+        "for (int32_t e = 0; e <= M; ++e) offsets[e] = start[e + 1];"),
+    "dispatch_invalid_ids_to_expert_0": (
+        "return (e >= 0 && e < M) ? e : M;",
+        "return (e >= 0 && e < M) ? e : 0;"),
     "z_drops_last_hidden_term": (
         "for (int32_t j = 0; j < h; ++j) {\n                    const double* r1row",
         "for (int32_t j = 0; j < h - 1; ++j) {\n                    const double* r1row"),
