@@ -273,6 +273,21 @@ def main():
                    "replays": tm["replays"], "steps_per_replay": tm["steps_per_replay"]},
     }
 
+    # Sort + Count on this workload's routing output (the dispatch bookkeeping that consumes
+    # it): HBM-bound, algorithmic bytes = ids read once, positions written once, offsets
+    dsrc = router.LowrankRouter(w.T, w.h, w.r, w.M, w.k, device=dev)(*bufs[0]).idx.clone()
+    ds = router.DispatchSorter(w.T, w.k, w.M, device=dev)
+    dt = timed_graph(lambda i: ds(dsrc), args.steps, args.warmup)
+    dbytes = 8 * w.T * w.k + 4 * (w.M + 1)
+    dach = dbytes / dt["mean_s"] / 1e9
+    result["dispatch"] = {"op": "sort + count of the routing output (more_dispatch_sort)",
+                          "ms": round(dt["mean_s"] * 1e3, 5),
+                          "roofline": {"bound": "hbm", "achieved": round(dach, 2),
+                                       "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                       "frac": round(dach / PEAK_HBM_GBS, 5),
+                                       "algorithmic_bytes": dbytes}}
+    del ds, dsrc
+
     if not args.no_fullrank:
         # full-rank router on the same token batches with W = R1 R2 rounded to bf16; logits
         # materialised in fp32 and in bf16; timed from HIP graphs like the low-rank router; the

@@ -157,6 +157,27 @@ more_status more_expert_histogram(const int32_t* idx, int64_t T, int32_t k, int3
                                   int32_t* counts, void* stream);
 
 /*
+ * Dispatch bookkeeping that consumes a selection ("Sort + Count" of the MoE layer's forward
+ * pass in the efficiency appendix: the (N, k) expert ids become N k sorted positions plus
+ * per-expert offsets).  The T k entries of idx are numbered p = t k + j (row-major); an entry's
+ * key is its expert id, or M when the id lies outside [0, M).
+ *   idx      int32 [T][k]           expert ids (e.g. the idx output of a routing call)
+ *   offsets  int32 [M + 1]  out     offsets[e] = number of entries whose key is below e;
+ *                                   offsets[M] = number of entries with a valid id
+ *   sorted   int32 [T k]    out     the positions p ordered by key, increasing p within a key
+ *                                   (expert e's entries are sorted[offsets[e] .. offsets[e+1]);
+ *                                   entries with invalid ids follow all experts)
+ *   workspace / workspace_bytes     at least more_dispatch_sort_workspace_size() bytes,
+ *                                   256-byte aligned (0 bytes when T = 0)
+ * Limits: T k <= 2^31 - 1, M < 2^30.  T == 0 writes offsets (all zero).  A stable radix sort
+ * on the key: the result is unique, so every run gives the same bits.
+ */
+more_status more_dispatch_sort(const int32_t* idx, int64_t T, int32_t k, int32_t M,
+                               int32_t* offsets, int32_t* sorted, void* workspace,
+                               size_t workspace_bytes, void* stream);
+more_status more_dispatch_sort_workspace_size(int64_t T, int32_t k, int32_t M, size_t* bytes);
+
+/*
  * For callers that cannot allocate (code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc): more_route_lowrank without a workspace argument.  The
  * scratch is a static device array of MORE_NOALLOC_SCRATCH_BYTES bytes per device, placed on

@@ -1,0 +1,232 @@
+// Dispatch bookkeeping of an MoE layer ("Sort + Count" in the layer's forward-pass figure of the
+// efficiency appendix): the N = T k expert ids of a routing result become the positions
+// p = t k + j grouped by expert (ascending p within an expert, ids outside [0, M) last) and the
+// per-expert offsets.
+//
+// A least-significant-digit radix sort on the key (expert id, or M for an id outside [0, M)),
+// 8 bits per pass, each pass stable, so that equal keys keep their position order:
+//   dsort_hist_kernel     per block of 1024 entries, the count of each digit value;
+//   dsort_scan_kernel     one workgroup per digit value: the exclusive scan of that digit's
+//                         block counts, and the digit's total;
+//   dsort_scatter_kernel  each entry's rank among the block's earlier entries with its digit
+//                         (wave ballots within a wave, then counts of the earlier waves and
+//                         rounds), added to its (digit, block) start: the totals of the smaller
+//                         digits (a 256-wide scan in LDS) plus the digit's block prefix.
+// dsort_offsets_kernel derives offsets from the sorted keys: offsets[e] = the first slot whose
+// key is at least e.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lowrank.h"
+
+namespace more {
+
+constexpr int kDsThreads = 256;
+constexpr int kDsRounds = 4;                          // entries per thread and block
+constexpr int kDsBlock = kDsThreads * kDsRounds;      // 1024 entries per block
+constexpr int kDsDigits = 256;                        // 8-bit digits
+constexpr int kDsGroups = kDsRounds * (kDsThreads / 64);  // (round, wave) groups in entry order
+
+__device__ __forceinline__ int32_t ds_key(int32_t e, int32_t M) {
+    return (e >= 0 && e < M) ? e : M;
+}
+
+// Digit counts of block b: hist[d * nblocks + b].  Pass 0 reads the keys from idx.
+__global__ __launch_bounds__(kDsThreads) void dsort_hist_kernel(const int32_t* __restrict__ idx,
+                                                                const int32_t* __restrict__ keys,
+                                                                int64_t N, int32_t M, int shift,
+                                                                int32_t* __restrict__ hist) {
+    __shared__ int32_t cnt[kDsDigits];
+    const int tid = threadIdx.x;
+    cnt[tid] = 0;
+    __syncthreads();
+    const int64_t b0 = (int64_t)blockIdx.x * kDsBlock;
+    for (int r = 0; r < kDsRounds; ++r) {
+        const int64_t g = b0 + r * kDsThreads + tid;
+        if (g < N) {
+            const int32_t key = idx ? ds_key(idx[g], M) : keys[g];
+            atomicAdd(&cnt[(key >> shift) & (kDsDigits - 1)], 1);
+        }
+    }
+    __syncthreads();
+    hist[(int64_t)tid * gridDim.x + blockIdx.x] = cnt[tid];
+}
+
+// Workgroup d: in-place exclusive scan of hist[d][0 .. nb) (the digit's block counts, in
+// tiles of 1024, four consecutive counts per thread) and total[d], the digit's entry count.
+__global__ __launch_bounds__(kDsThreads) void dsort_scan_kernel(int32_t* __restrict__ hist,
+                                                                int64_t nb,
+                                                                int32_t* __restrict__ total) {
+    __shared__ int32_t part[kDsThreads];
+    const int tid = threadIdx.x;
+    int32_t* a = hist + (int64_t)blockIdx.x * nb;
+    int32_t carry = 0;
+    for (int64_t t0 = 0; t0 < nb; t0 += 4 * kDsThreads) {
+        int32_t v[4];
+        int32_t sum = 0;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t j = t0 + 4 * tid + i;
+            v[i] = j < nb ? a[j] : 0;
+            sum += v[i];
+        }
+        part[tid] = sum;
+        __syncthreads();
+        for (int d = 1; d < kDsThreads; d <<= 1) {  // inclusive scan of the threads' sums
+            const int32_t u = tid >= d ? part[tid - d] : 0;
+            __syncthreads();
+            part[tid] += u;
+            __syncthreads();
+        }
+        int32_t run = carry + part[tid] - sum;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t j = t0 + 4 * tid + i;
+            if (j < nb) a[j] = run;
+            run += v[i];
+        }
+        carry += part[kDsThreads - 1];
+        __syncthreads();  // part is rewritten by the next tile
+    }
+    if (tid == 0) total[blockIdx.x] = carry;
+}
+
+// Stable scatter of one pass.  Entry g = b0 + r 256 + tid of block b belongs to group
+// (r, wave); groups are in entry order, lanes within a group too.  keys_out may be null (not
+// needed after the last pass); pass 0 reads keys from idx and takes the position as value.
+__global__ __launch_bounds__(kDsThreads) void dsort_scatter_kernel(
+    const int32_t* __restrict__ idx, const int32_t* __restrict__ keys_in,
+    const int32_t* __restrict__ vals_in, int64_t N, int32_t M, int shift,
+    const int32_t* __restrict__ start, const int32_t* __restrict__ total,
+    int32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out) {
+    __shared__ int32_t cnt[kDsGroups][kDsDigits];  // count per group, then the group's offset
+    __shared__ int32_t base[kDsDigits];            // entries of the smaller digits
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    for (int i = tid; i < kDsGroups * kDsDigits; i += kDsThreads) (&cnt[0][0])[i] = 0;
+    base[tid] = total[tid];
+    __syncthreads();
+    for (int d = 1; d < kDsDigits; d <<= 1) {  // inclusive scan of the digit totals
+        const int32_t u = tid >= d ? base[tid - d] : 0;
+        __syncthreads();
+        base[tid] += u;
+        __syncthreads();
+    }
+    const int32_t mybase = base[tid] - total[tid];  // exclusive, digit tid
+    __syncthreads();
+    base[tid] = mybase;
+    __syncthreads();
+    const int64_t b0 = (int64_t)blockIdx.x * kDsBlock;
+    const uint64_t below = (1ull << lane) - 1ull;
+    int32_t key[kDsRounds], val[kDsRounds], rank[kDsRounds];
+    for (int r = 0; r < kDsRounds; ++r) {
+        const int64_t g = b0 + r * kDsThreads + tid;
+        const bool ok = g < N;
+        key[r] = ok ? (idx ? ds_key(idx[g], M) : keys_in[g]) : 0;
+        val[r] = ok ? (idx ? (int32_t)g : vals_in[g]) : 0;
+        const int d = (key[r] >> shift) & (kDsDigits - 1);
+        // lanes of this wave holding the same digit (all 64 lanes take part in every ballot)
+        uint64_t peers = __ballot(ok);
+#pragma unroll
+        for (int bit = 0; bit < 8; ++bit) {
+            const uint64_t m = __ballot((d >> bit) & 1);
+            peers &= ((d >> bit) & 1) ? m : ~m;
+        }
+        rank[r] = __popcll(peers & below);
+        if (ok && (peers & below) == 0) cnt[r * 4 + w][d] = __popcll(peers);
+    }
+    __syncthreads();
+    {  // thread tid = digit: exclusive offsets of the groups, in entry order
+        int32_t run = 0;
+        for (int gi = 0; gi < kDsGroups; ++gi) {
+            const int32_t c = cnt[gi][tid];
+            cnt[gi][tid] = run;
+            run += c;
+        }
+    }
+    __syncthreads();
+    for (int r = 0; r < kDsRounds; ++r) {
+        const int64_t g = b0 + r * kDsThreads + tid;
+        if (g >= N) continue;
+        const int d = (key[r] >> shift) & (kDsDigits - 1);
+        const int64_t dest = (int64_t)base[d] + start[(int64_t)d * gridDim.x + blockIdx.x] +
+                             cnt[r * 4 + w][d] + rank[r];
+        if (dest < N) {  // always true; keeps every write in bounds regardless
+            if (keys_out) keys_out[dest] = key[r];
+            vals_out[dest] = val[r];
+        }
+    }
+}
+
+// offsets[e] = the first slot i whose key is at least e (N if none), for e = 0 .. M: slot i
+// writes the e in (key[i - 1], key[i]], the last slot also those above its key.
+__global__ __launch_bounds__(256) void dsort_offsets_kernel(const int32_t* __restrict__ keys,
+                                                            int64_t N, int32_t M,
+                                                            int32_t* __restrict__ offsets) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i <= N;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t lo = i == 0 ? -1 : keys[i - 1];
+        const int32_t hi = i == N ? M : keys[i];
+        for (int32_t e = lo + 1; e <= hi && e <= M; ++e) offsets[e] = (int32_t)i;
+    }
+}
+
+__global__ __launch_bounds__(256) void dsort_fill_kernel(int32_t* __restrict__ p, int64_t n,
+                                                         int32_t v) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+int dispatch_passes(int32_t M) {
+    int bits = 1;
+    while (bits < 31 && ((int64_t)1 << bits) <= (int64_t)M) ++bits;  // keys 0 .. M
+    return (bits + 7) / 8;
+}
+
+size_t dispatch_workspace_bytes(int64_t N) {
+    if (N == 0) return 0;
+    const int64_t nblocks = (N + kDsBlock - 1) / kDsBlock;
+    auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    return 4 * al((size_t)N * 4) + al((size_t)nblocks * kDsDigits * 4) + al(kDsDigits * 4);
+}
+
+hipError_t dispatch_launch(const int32_t* idx, int64_t N, int32_t M, int32_t* offsets,
+                           int32_t* sorted, void* workspace, hipStream_t st) {
+    if (N == 0) {
+        const int64_t n = (int64_t)M + 1;
+        const unsigned blocks = (unsigned)((n + 255) / 256 < 1024 ? (n + 255) / 256 : 1024);
+        hipLaunchKernelGGL(dsort_fill_kernel, dim3(blocks), dim3(256), 0, st, offsets, n, 0);
+        return hipGetLastError();
+    }
+    const int64_t nblocks = (N + kDsBlock - 1) / kDsBlock;
+    auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
+    char* ws = static_cast<char*>(workspace);
+    int32_t* keys[2] = {reinterpret_cast<int32_t*>(ws), reinterpret_cast<int32_t*>(ws + al((size_t)N * 4))};
+    int32_t* vals[2] = {reinterpret_cast<int32_t*>(ws + 2 * al((size_t)N * 4)),
+                        reinterpret_cast<int32_t*>(ws + 3 * al((size_t)N * 4))};
+    int32_t* hist = reinterpret_cast<int32_t*>(ws + 4 * al((size_t)N * 4));
+    int32_t* total = reinterpret_cast<int32_t*>(ws + 4 * al((size_t)N * 4) +
+                                                al((size_t)nblocks * kDsDigits * 4));
+    const int passes = dispatch_passes(M);
+    for (int p = 0; p < passes; ++p) {
+        const int shift = 8 * p;
+        const int32_t* kin = p == 0 ? nullptr : keys[(p - 1) & 1];
+        const int32_t* vin = p == 0 ? nullptr : vals[(p - 1) & 1];
+        const int32_t* src_idx = p == 0 ? idx : nullptr;
+        int32_t* kout = keys[p & 1];
+        int32_t* vout = p == passes - 1 ? sorted : vals[p & 1];
+        hipLaunchKernelGGL(dsort_hist_kernel, dim3((unsigned)nblocks), dim3(kDsThreads), 0, st,
+                           src_idx, kin, N, M, shift, hist);
+        hipLaunchKernelGGL(dsort_scan_kernel, dim3(kDsDigits), dim3(kDsThreads), 0, st, hist,
+                           nblocks, total);
+        hipLaunchKernelGGL(dsort_scatter_kernel, dim3((unsigned)nblocks), dim3(kDsThreads), 0, st,
+                           src_idx, kin, vin, N, M, shift, hist, total, kout, vout);
+    }
+    const int64_t nth = N + 1;
+    const unsigned blocks = (unsigned)((nth + 255) / 256 < 4096 ? (nth + 255) / 256 : 4096);
+    hipLaunchKernelGGL(dsort_offsets_kernel, dim3(blocks), dim3(256), 0, st, keys[(passes - 1) & 1],
+                       N, M, offsets);
+    return hipGetLastError();
+}
+
+}  // namespace more

@@ -79,4 +79,10 @@ hipError_t fullrank_launch(const FullrankPlan& plan, const uint16_t* x, const ui
                            int64_t T, int32_t h, int32_t M, int32_t k, int32_t* idx, float* gate,
                            float* topval, void* workspace, hipStream_t stream, int* blas_status);
 
+// Dispatch bookkeeping (dispatch.hip): N = T k entries, keys 0 .. M.
+int dispatch_passes(int32_t M);
+size_t dispatch_workspace_bytes(int64_t N);
+hipError_t dispatch_launch(const int32_t* idx, int64_t N, int32_t M, int32_t* offsets,
+                           int32_t* sorted, void* workspace, hipStream_t stream);
+
 }  // namespace more

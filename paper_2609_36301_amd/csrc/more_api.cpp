@@ -170,6 +170,27 @@ more_status more_route_fullrank(const uint16_t* x, const uint16_t* Wt, int64_t T
     return from_hip(e);
 }
 
+more_status more_dispatch_sort_workspace_size(int64_t T, int32_t k, int32_t M, size_t* bytes) {
+    if (!bytes || T < 0 || k < 1 || M < 1) return MORE_ERR_INVALID_ARG;
+    if (T > kMaxT || M >= kMaxM || T * (int64_t)k > kMaxT) return MORE_ERR_UNSUPPORTED;
+    *bytes = more::dispatch_workspace_bytes(T * (int64_t)k);
+    return MORE_OK;
+}
+
+more_status more_dispatch_sort(const int32_t* idx, int64_t T, int32_t k, int32_t M,
+                               int32_t* offsets, int32_t* sorted, void* workspace,
+                               size_t workspace_bytes, void* stream) {
+    if (!offsets || (T > 0 && (!idx || !sorted))) return MORE_ERR_INVALID_ARG;
+    if (!aligned(idx, 4) || !aligned(offsets, 4) || !aligned(sorted, 4) || !aligned(workspace, 256))
+        return MORE_ERR_INVALID_ARG;
+    size_t need = 0;
+    more_status s = more_dispatch_sort_workspace_size(T, k, M, &need);
+    if (s != MORE_OK) return s;
+    if (need > 0 && (!workspace || workspace_bytes < need)) return MORE_ERR_WORKSPACE;
+    return from_hip(more::dispatch_launch(idx, T * (int64_t)k, M, offsets, sorted, workspace,
+                                          static_cast<hipStream_t>(stream)));
+}
+
 more_status more_expert_histogram(const int32_t* idx, int64_t T, int32_t k, int32_t M,
                                   int32_t* counts, void* stream) {
     if (!counts || (!idx && T > 0)) return MORE_ERR_INVALID_ARG;

@@ -202,3 +202,50 @@ def expert_histogram(idx: torch.Tensor, M: int) -> torch.Tensor:
     st = _lib.load().more_expert_histogram(_ptr(idx), T, k, M, _ptr(counts), _stream(idx.device))
     _lib.check(st, "more_expert_histogram")
     return counts
+
+
+def dispatch_sort(idx: torch.Tensor, M: int) -> tuple[torch.Tensor, torch.Tensor]:
+    """(offsets int32 [M + 1], sorted int32 [T k]): the positions p = t k + j of idx
+    (int32 [T][k]) grouped by expert id, increasing p within an expert, ids outside [0, M)
+    after all experts; offsets[e] = number of entries with a smaller id (more_dispatch_sort)."""
+    if idx.dtype != torch.int32 or idx.dim() != 2 or not idx.is_contiguous():
+        raise ValueError("idx must be a contiguous int32 [T][k] tensor")
+    if idx.device.type != "cuda":
+        raise ValueError("idx must be on a GPU device")
+    T, k = idx.shape
+    lib = _lib.load()
+    n = ctypes.c_size_t(0)
+    _lib.check(lib.more_dispatch_sort_workspace_size(T, k, M, ctypes.byref(n)),
+               "more_dispatch_sort_workspace_size")
+    ws = torch.empty((max(n.value, 1),), dtype=torch.uint8, device=idx.device)
+    offsets = torch.empty((M + 1,), dtype=torch.int32, device=idx.device)
+    srt = torch.empty((T * k,), dtype=torch.int32, device=idx.device)
+    st = lib.more_dispatch_sort(_ptr(idx), T, k, M, _ptr(offsets), _ptr(srt), _ptr(ws), n.value,
+                                _stream(idx.device))
+    _lib.check(st, "more_dispatch_sort")
+    return offsets, srt
+
+
+class DispatchSorter:
+    """Pre-allocated outputs and workspace for repeated more_dispatch_sort calls on one shape
+    (no allocation per call, so a call can be captured in a HIP graph)."""
+
+    def __init__(self, T: int, k: int, M: int, device="cuda"):
+        self.T, self.k, self.M = T, k, M
+        dev = torch.device(device)
+        n = ctypes.c_size_t(0)
+        _lib.check(_lib.load().more_dispatch_sort_workspace_size(T, k, M, ctypes.byref(n)),
+                   "more_dispatch_sort_workspace_size")
+        self.workspace_bytes = n.value
+        self.workspace = torch.empty((max(n.value, 1),), dtype=torch.uint8, device=dev)
+        self.offsets = torch.empty((M + 1,), dtype=torch.int32, device=dev)
+        self.sorted = torch.empty((T * k,), dtype=torch.int32, device=dev)
+
+    def __call__(self, idx: torch.Tensor):
+        if idx.dtype != torch.int32 or tuple(idx.shape) != (self.T, self.k) or not idx.is_contiguous():
+            raise ValueError("idx must be a contiguous int32 [%d][%d] tensor" % (self.T, self.k))
+        st = _lib.load().more_dispatch_sort(_ptr(idx), self.T, self.k, self.M, _ptr(self.offsets),
+                                            _ptr(self.sorted), _ptr(self.workspace),
+                                            self.workspace_bytes, _stream(idx.device))
+        _lib.check(st, "more_dispatch_sort")
+        return self.offsets, self.sorted

@@ -186,6 +186,33 @@ def test_histogram_validation(lib):
     assert lib.more_expert_histogram(ODD, 10, 4, 100, FAKE, None) == _lib.ERR_INVALID_ARG
 
 
+def test_dispatch_sort_validation(lib):
+    n = ctypes.c_size_t(0)
+    assert lib.more_dispatch_sort_workspace_size(1000, 8, 5000, ctypes.byref(n)) == _lib.OK
+    assert n.value >= 4 * 8000 * 4  # keys and positions, two buffers each
+    assert lib.more_dispatch_sort_workspace_size(0, 8, 5000, ctypes.byref(n)) == _lib.OK
+    assert n.value == 0
+    assert lib.more_dispatch_sort_workspace_size(1 << 29, 8, 5000,
+                                                 ctypes.byref(n)) == _lib.ERR_UNSUPPORTED
+    assert lib.more_dispatch_sort_workspace_size(10, 0, 5000, ctypes.byref(n)) == _lib.ERR_INVALID_ARG
+    assert lib.more_dispatch_sort_workspace_size(10, 4, 0, ctypes.byref(n)) == _lib.ERR_INVALID_ARG
+    # checked on the host before anything is launched
+    assert lib.more_dispatch_sort(FAKE, 10, 4, 100, None, FAKE, FAKE, 1 << 20,
+                                  None) == _lib.ERR_INVALID_ARG
+    assert lib.more_dispatch_sort(None, 10, 4, 100, FAKE, FAKE, FAKE, 1 << 20,
+                                  None) == _lib.ERR_INVALID_ARG
+    assert lib.more_dispatch_sort(FAKE, 10, 4, 100, FAKE, None, FAKE, 1 << 20,
+                                  None) == _lib.ERR_INVALID_ARG
+    assert lib.more_dispatch_sort(FAKE, -1, 4, 100, FAKE, FAKE, FAKE, 1 << 20,
+                                  None) == _lib.ERR_INVALID_ARG
+    assert lib.more_dispatch_sort(ODD, 10, 4, 100, FAKE, FAKE, FAKE, 1 << 20,
+                                  None) == _lib.ERR_INVALID_ARG
+    assert lib.more_dispatch_sort(FAKE, 10, 4, 100, FAKE, FAKE, None, 0,
+                                  None) == _lib.ERR_WORKSPACE
+    assert lib.more_dispatch_sort(FAKE, 10, 4, 100, FAKE, FAKE, FAKE, 16,
+                                  None) == _lib.ERR_WORKSPACE
+
+
 def test_binding_rejects_bad_tensors():
     import torch
     from paper_2609_36301_amd import router
