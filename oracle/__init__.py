@@ -11,6 +11,8 @@ Functions and the passage they follow:
   route_lowrank   softmax(TopK(x R1 R2)), the MoRE router ("Preliminaries", MoRE layer)
   route_fullrank  softmax(TopK(x W)), the standard router ("Preliminaries")
   histogram       per-expert selection counts (Appendix "Training", statistic f)
+  route_stats     training-forward softmax statistics m, Z and psum (Appendix "Pseudocode",
+                  training forward, eqs. app_softmax, app_psum, app_online)
   dispatch_sort   "Sort + Count": positions grouped by expert plus offsets (MoE layer
                   forward pass, efficiency appendix)
   logits_at       the logits x R1 R2 at given (token, expert) pairs ("Preliminaries"), to
@@ -58,6 +60,7 @@ def load_library(path: str):
         fn.restype = ctypes.c_int
     lib.oracle_histogram.argtypes = [P, i64, i32, i32, P]
     lib.oracle_dispatch_sort.argtypes = [P, i64, i32, i32, P, P]
+    lib.oracle_route_stats.argtypes = [P, P, P, i64, i32, i32, i32, P, P, P, i32]
     lib.oracle_histogram.restype = ctypes.c_int
     lib.oracle_logits_at.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, P, i32, P, i32]
     lib.oracle_logits_at.restype = ctypes.c_int
@@ -223,3 +226,19 @@ def dispatch_sort(idx, M: int, lib=None):
     _check(_load(lib).oracle_dispatch_sort(_ptr(idx), idx.shape[0], idx.shape[1], M,
                                            _ptr(offsets), _ptr(srt)))
     return offsets, srt
+
+
+def route_stats(x, R1, R2, threads=None, lib=None):
+    """(m [T], Z [T], psum [M]) in fp64: the row maximum of the logits x R1 R2, the softmax
+    normaliser sum_e exp(l - m), and the column sums of the row softmax over all experts."""
+    x, R1, R2 = _u16(x), _u16(R1), _u16(R2)
+    T, h = x.shape
+    r, M = R2.shape
+    if R1.shape != (h, r):
+        raise ValueError("R1 must be [h][r]")
+    m = np.zeros(T, np.float64)
+    Z = np.zeros(T, np.float64)
+    psum = np.zeros(M, np.float64)
+    _check(_load(lib).oracle_route_stats(_ptr(x), _ptr(R1), _ptr(R2), T, h, r, M, _ptr(m),
+                                         _ptr(Z), _ptr(psum), _threads(threads)))
+    return m, Z, psum

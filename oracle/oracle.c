@@ -25,6 +25,9 @@
  * selections (bincount of the chosen indices, Appendix "Training", load-balancing
  * statistic f).
  *
+ * oracle_route_stats gives the softmax statistics of the training forward pass: the row maximum
+ * m, the normaliser Z and the column sums psum of the full softmax over all experts.
+ *
  * oracle_dispatch_sort is the dispatch bookkeeping that consumes a selection: the selected
  * (token, slot) positions grouped by expert, with per-expert offsets.
  *
@@ -365,6 +368,88 @@ int oracle_fullrank_logits_at(const uint16_t* x, const uint16_t* W, int64_t T, i
  *                starting at its offset).
  * offsets int64 [M + 1]; sorted int64 [N k].
  */
+/*
+ * Softmax statistics of the training forward pass (Appendix "Pseudocode", training forward:
+ * the row softmax P of the logits, eq. app_softmax; its column sums psum, eq. app_psum; the row
+ * maximum m and the normaliser Z that the online softmax keeps, eq. app_online):
+ *   m[t]    = max_e l_t[e]
+ *   Z[t]    = sum_e exp(l_t[e] - m[t])
+ *   psum[e] = sum_t exp(l_t[e] - m[t]) / Z[t]
+ * with the logits l = x R1 R2 of steps 2-3 above, in fp64 over all M experts.  x, R1, R2 as
+ * in oracle_route_lowrank; m, Z double [T]; psum double [M].  Tokens are summed into psum in
+ * increasing order within fixed blocks of 64 tokens, then block by block, so the result does
+ * not depend on the thread count.
+ */
+int oracle_route_stats(const uint16_t* x, const uint16_t* R1, const uint16_t* R2, int64_t T,
+                       int32_t h, int32_t r, int32_t M, double* m, double* Z, double* psum,
+                       int32_t nthreads) {
+    if (!x || !R1 || !R2 || !m || !Z || !psum) return ORACLE_ERR_ARG;
+    if (T < 0 || h <= 0 || r <= 0 || M <= 0) return ORACLE_ERR_ARG;
+    const int64_t nb = (T + 63) / 64;
+    double* f1 = (double*)malloc(sizeof(double) * (size_t)h * (size_t)r);
+    double* f2 = (double*)malloc(sizeof(double) * (size_t)r * (size_t)M);
+    double* part = (double*)calloc((size_t)(nb > 0 ? nb : 1) * (size_t)M, sizeof(double));
+    if (!f1 || !f2 || !part) {
+        free(f1);
+        free(f2);
+        free(part);
+        return ORACLE_ERR_NOMEM;
+    }
+    int ok = decode_all(R1, (int64_t)h * r, f1) & decode_all(R2, (int64_t)r * M, f2);
+    int status = ok ? ORACLE_OK : ORACLE_ERR_NONFINITE;
+    if (status == ORACLE_OK) {
+#ifdef _OPENMP
+        if (nthreads > 0) omp_set_num_threads(nthreads);
+#endif
+#pragma omp parallel
+        {
+            double* xs = (double*)malloc(sizeof(double) * (size_t)h);
+            double* zz = (double*)malloc(sizeof(double) * (size_t)r);
+            double* lg = (double*)malloc(sizeof(double) * (size_t)M);
+            int local_ok = xs && zz && lg;
+#pragma omp for schedule(dynamic, 1)
+            for (int64_t b = 0; b < nb; ++b) {
+                if (!local_ok) continue;
+                double* pb = part + b * (int64_t)M;
+                for (int64_t t = 64 * b; t < T && t < 64 * b + 64; ++t) {
+                    if (!decode_all(x + t * (int64_t)h, h, xs)) {
+#pragma omp atomic write
+                        status = ORACLE_ERR_NONFINITE;
+                        continue;
+                    }
+                    for (int32_t i = 0; i < r; ++i) zz[i] = 0.0;
+                    for (int32_t j = 0; j < h; ++j)
+                        for (int32_t i = 0; i < r; ++i) zz[i] += xs[j] * f1[(int64_t)j * r + i];
+                    for (int32_t e = 0; e < M; ++e) lg[e] = 0.0;
+                    for (int32_t i = 0; i < r; ++i)
+                        for (int32_t e = 0; e < M; ++e) lg[e] += zz[i] * f2[(int64_t)i * M + e];
+                    double mx = lg[0];
+                    for (int32_t e = 1; e < M; ++e) mx = lg[e] > mx ? lg[e] : mx;
+                    double zs = 0.0;
+                    for (int32_t e = 0; e < M; ++e) zs += exp(lg[e] - mx);
+                    m[t] = mx;
+                    Z[t] = zs;
+                    for (int32_t e = 0; e < M; ++e) pb[e] += exp(lg[e] - mx) / zs;
+                }
+            }
+            if (!local_ok) {
+#pragma omp atomic write
+                status = ORACLE_ERR_NOMEM;
+            }
+            free(xs);
+            free(zz);
+            free(lg);
+        }
+        for (int32_t e = 0; e < M; ++e) psum[e] = 0.0;
+        for (int64_t b = 0; b < nb; ++b)
+            for (int32_t e = 0; e < M; ++e) psum[e] += part[b * (int64_t)M + e];
+    }
+    free(f1);
+    free(f2);
+    free(part);
+    return status;
+}
+
 /* Key of an entry: its expert id, or M when the id lies outside [0, M). */
 static int32_t dispatch_key(int32_t e, int32_t M) { return (e >= 0 && e < M) ? e : M; }
 

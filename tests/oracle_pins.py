@@ -13,6 +13,8 @@ library) so the same checks can be run against deliberately broken builds of the
 * Prop-1 top-1     -- the sign-pattern closed form of the load-balancing construction;
 * Prop-1 counts    -- the Bernstein bound of the load-balancing proposition;
 * histogram        -- counts equal numpy's bincount and sum to n k;
+* softmax stats    -- m, Z, psum against scipy's logsumexp and softmax over BLAS logits, with the
+                      zero-token, one-expert and large-logit special cases;
 * logits at pairs  -- numpy BLAS logits at random (token, expert) pairs, including the
                       first and last expert and repeated tokens (low-rank and full-rank).
 """
@@ -233,6 +235,43 @@ def check_dispatch_sort(lib=None):
             assert np.all(ks[offsets[e]:hi] == e)
 
 
+# ------------------------------------------------------------------ softmax statistics
+def check_route_stats(lib=None):
+    """m, Z and psum against numpy BLAS logits with scipy's logsumexp and softmax, plus the
+    invariants of the definition: sum_e psum = T; m is the top-1 logit of the routing; a zero
+    token ties every expert at 0 (m = 0, Z = M, 1/M to each column); M = 1 gives Z = 1 and
+    psum = T; logits near 1e3 (where exp without the max shift overflows) stay finite."""
+    from scipy.special import logsumexp, softmax
+    cases = [((200, 96, 16, 300), 1.0), ((64, 32, 48, 5), 1.0), ((70, 64, 32, 1), 1.0),
+             ((130, 64, 16, 77), 600.0), ((0, 32, 16, 9), 1.0)]
+    for si, ((T, h, r, M), scale) in enumerate(cases):
+        inp = make_inputs(T, h, r, M, seed=400 + si)
+        if scale != 1.0:
+            inp.R2 = f32_to_bf16_bits(bf16_bits_to_f32(inp.R2) * np.float32(scale))
+        if T >= 64:
+            inp.x[[0, 63]] = 0
+        m, Z, psum = oracle.route_stats(inp.x, inp.R1, inp.R2, lib=lib)
+        logits = (f64(inp.x) @ f64(inp.R1)) @ f64(inp.R2)
+        assert np.all(np.isfinite(m)) and np.all(np.isfinite(Z)) and np.all(np.isfinite(psum))
+        if T == 0:
+            assert np.all(psum == 0.0)
+            continue
+        assert np.allclose(m, logits.max(axis=1), rtol=1e-12, atol=1e-12), "row maximum (%d)" % si
+        assert np.allclose(m + np.log(Z), logsumexp(logits, axis=1), rtol=1e-12, atol=1e-9), \
+            "log-normaliser (%d)" % si
+        assert np.allclose(psum, softmax(logits, axis=1).sum(axis=0), rtol=1e-10, atol=1e-10), \
+            "column sums (%d)" % si
+        assert abs(psum.sum() - T) < 1e-9 * T
+        assert np.all(Z >= 1.0 - 1e-15) and np.all(Z <= M * (1 + 1e-15))
+        if M == 1:
+            assert np.all(Z == 1.0) and abs(psum[0] - T) < 1e-9
+        if T >= 64:
+            assert m[0] == 0.0 and Z[0] == M and m[63] == 0.0 and Z[63] == M
+        if M >= 8:
+            top = oracle.route_lowrank(inp.x, inp.R1, inp.R2, 1, lib=lib).topval
+            assert np.allclose(m, top[:, 0], rtol=1e-12, atol=1e-12)
+
+
 # ------------------------------------------------------------------ logits at pairs
 def check_logits_at(lib=None, shapes=((50, 96, 16, 300), (7, 32, 48, 5), (33, 64, 64, 1000))):
     for si, (T, h, r, M) in enumerate(shapes):
@@ -262,7 +301,7 @@ def check_fullrank_logits_at(lib=None):
     assert np.allclose(got, want, rtol=1e-12, atol=1e-12), "full-rank logits at pairs differ"
 
 
-ALL_CHECKS = [check_dispatch_sort, check_bruteforce, check_fullrank_bruteforce, check_identity,
+ALL_CHECKS = [check_route_stats, check_dispatch_sort, check_bruteforce, check_fullrank_bruteforce, check_identity,
               check_gates,
               check_equivariance, check_thm1, check_prop1_top1, check_prop1_counts,
               check_histogram, check_logits_at, check_fullrank_logits_at]

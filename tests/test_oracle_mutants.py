@@ -15,6 +15,21 @@ import oracle_pins
 SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
 
 MUTANTS = {
+    "stats_no_max_shift_in_Z": (
+        "zs += exp(lg[e] - mx);",
+        "zs += exp(lg[e]);"),
+    "stats_psum_not_normalised": (
+        "pb[e] += exp(lg[e] - mx) / zs;",
+        "pb[e] += exp(lg[e] - mx);"),
+    "stats_max_is_minimum": (
+        "mx = lg[e] > mx ? lg[e] : mx;",
+        "mx = lg[e] < mx ? lg[e] : mx;"),
+    "stats_Z_drops_last_expert": (
+        "for (int32_t e = 0; e < M; ++e) zs += exp",
+        "for (int32_t e = 0; e < M - 1; ++e) zs += exp"),
+    "stats_last_token_block_dropped": (
+        "for (int64_t b = 0; b < nb; ++b)\n            for (int32_t e = 0; e < M; ++e) psum[e]",
+        "for (int64_t b = 0; b < nb - 1; ++b)\n            for (int32_t e = 0; e < M; ++e) psum[e]"),
     "dispatch_positions_reversed": (
         "    for (int64_t p = 0; p < N; ++p) {\n        const int32_t key = dispatch_key(idx[p], M);",
         "    for (int64_t p = N - 1; p >= 0; --p) {\n        const int32_t key = dispatch_key(idx[p], M);"),
