@@ -29,7 +29,9 @@
  *    call returns after launching.  Launch failures return MORE_ERR_HIP; faults during
  *    execution surface at the caller's next synchronisation.
  *  - Arguments are validated on the host before anything is launched; an error status means
- *    nothing was enqueued.  T == 0 returns MORE_OK without launching.
+ *    nothing was enqueued.  T == 0 returns MORE_OK without launching (apart from clearing
+ *    the per-expert outputs counts and psum); the token-sized pointers (x, idx, gate, topval,
+ *    m, Z) may then be NULL.
  *  - Selection order: experts are ranked by logit, larger first; equal logits are ranked by
  *    expert id, smaller first.  idx[t][0..k-1] lists the selected experts in that order.
  *    (The paper's buffer leaves both the slot order and tie handling open; this total
@@ -128,6 +130,36 @@ more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, 
 #define MORE_ROUTE_SINGLE_PASS 3 /* z + prescreen, one collect sweep, finalize (+ histogram)    */
 more_status more_route_lowrank_route(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
                                      int32_t* route);
+
+/*
+ * Training forward pass of the low-rank router (Appendix "Pseudocode", training forward
+ * algorithm; eqs. app_softmax, app_psum and app_online): the routing of more_route_lowrank plus
+ * the statistics of the full row softmax over all M experts that the switch load-balancing
+ * loss L_bal = (M / T) sum_e f_e psum[e] needs (f_e = counts[e] / (T k); the loss itself is
+ * left to the caller):
+ *   m[t]    = max_e l_te                       (the token's top-1 logit)
+ *   Z[t]    = sum_e exp(l_te - m[t])           (the normaliser of the online softmax)
+ *   psum[e] = sum_t exp(l_te - m[t]) / Z[t]    (column sums of the softmax probabilities)
+ * with l = x R1 R2; no T x M matrix is written.
+ *   x, R1t, R2t, T, h, r, M, k, idx, gate, topval, counts   as in more_route_lowrank
+ *   m       fp32 [T]  out
+ *   Z       fp32 [T]  out
+ *   psum    fp32 [M]  out     (all zero when T == 0)
+ *   workspace / workspace_bytes   at least more_route_lowrank_train_workspace_size() bytes,
+ *                                 256-byte aligned
+ * Numerics: m is the top-1 logit of the routing (topval[t][0]).  Z and psum take the logits
+ * from the matrix cores with z carried as a bfloat16 hi/lo pair (about 16 significant bits):
+ * each exponent is within 2^-18 sum_i |z_i u_ei| + 2^-24 (2r + 1)(|m| + sum_i |z_i u_ei|)
+ * (times log2 e) of exact, and the sums run in fp32 in a fixed order, so a shape gives the same
+ * bits on every run.  Limits as for more_route_lowrank.
+ */
+more_status more_route_lowrank_train(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
+                                     int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                     int32_t* idx, float* gate, float* topval, int32_t* counts,
+                                     float* m, float* Z, float* psum, void* workspace,
+                                     size_t workspace_bytes, void* stream);
+more_status more_route_lowrank_train_workspace_size(int64_t T, int32_t h, int32_t r, int32_t M,
+                                                    int32_t k, size_t* bytes);
 
 /*
  * Full-rank (standard) router, the baseline (Section "Preliminaries": softmax(TopK(R x)) with

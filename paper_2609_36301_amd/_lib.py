@@ -29,6 +29,9 @@ SIGNATURES = {
     "more_route_lowrank_workspace_size_ex": (_I32, [_I64, _I32, _I32, _I32, _I32, _I32, _PSZ]),
     "more_route_lowrank_plan": (_I32, [_I64, _I32, _I32, _I32, _I32, _PI32]),
     "more_route_lowrank_route": (_I32, [_I64, _I32, _I32, _I32, _I32, _PI32]),
+    "more_route_lowrank_train": (_I32, [_P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P,
+                                        _P, _P, _P, _P, _P, _SZ, _P]),
+    "more_route_lowrank_train_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _I32, _PSZ]),
     "more_route_fullrank": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _SZ,
                                    _P]),
     "more_route_fullrank_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _I32, _PSZ]),

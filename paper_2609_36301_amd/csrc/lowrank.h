@@ -79,6 +79,37 @@ hipError_t fullrank_launch(const FullrankPlan& plan, const uint16_t* x, const ui
                            int64_t T, int32_t h, int32_t M, int32_t k, int32_t* idx, float* gate,
                            float* topval, void* workspace, hipStream_t stream, int* blas_status);
 
+// z = x R1 alone, fp32 [T][r] at z, for callers other than the routes (the h-split partials
+// and the z_hi / error-scale byproducts of the z pass go to scratch).
+size_t zonly_workspace_bytes(int64_t T, int32_t h, int32_t r);
+hipError_t zonly_launch(const uint16_t* x, const uint16_t* R1t, int64_t T, int32_t h, int32_t r,
+                        float* z, void* scratch, hipStream_t stream);
+
+// Softmax statistics of the training forward pass (stats.hip).
+struct StatsPlan {
+    int32_t RC;
+    int32_t chunks, splits;     // Z sweep: expert chunks x token splits
+    int32_t eblocks, psplits;   // psum sweep: expert blocks x token splits
+    int32_t own_z;              // 1: z is computed here (the routing call keeps none)
+    size_t off_tv, off_z, off_zscratch, off_zhl, off_mb, off_Zp, off_bias, off_part;
+    size_t workspace_bytes;
+};
+
+struct StatsArgs {
+    const uint16_t *x, *R1t, *R2t;
+    const float* z;      // z = x R1 [T][r] (unused with own_z)
+    const float* mtop;   // top-1 logit of token t at mtop[t ks]
+    int32_t ks;
+    int32_t T, h, r, M;
+    float *m, *Z, *psum;
+};
+
+bool stats_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, bool own_z,
+                     StatsPlan* plan);
+hipError_t stats_launch(const StatsPlan& plan, const StatsArgs& a, void* workspace,
+                        hipStream_t stream);
+hipError_t stats_zero_psum(float* psum, int32_t M, hipStream_t stream);
+
 // Dispatch bookkeeping (dispatch.hip): N = T k entries, keys 0 .. M.
 int dispatch_passes(int32_t M);
 size_t dispatch_workspace_bytes(int64_t N);

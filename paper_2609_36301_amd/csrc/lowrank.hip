@@ -1073,6 +1073,16 @@ static int pow2_at_least(int k) {
 
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
+// Split of the z pass's h axis: 64-wide chunks per split and the number of splits.
+static void zpass_split(int64_t T, int32_t h, int32_t* steps_per_split, int32_t* hsplit) {
+    const int32_t NC = (h / 16 + 3) / 4;
+    const int64_t ntbz = (T + kZTokens - 1) / kZTokens;
+    int64_t hs = ntbz >= 256 ? 1 : (256 + ntbz - 1) / ntbz;
+    if (hs > NC) hs = NC;
+    *steps_per_split = (int32_t)((NC + hs - 1) / hs);
+    *hsplit = (NC + *steps_per_split - 1) / *steps_per_split;
+}
+
 bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, int32_t m_chunks,
                        LowrankPlan* p) {
     LowrankPlan q{};
@@ -1121,12 +1131,7 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     // token blocks than CUs (one workgroup of 4 waves per CU streams x too slowly to leave
     // CUs idle: at T = 16384, h = 4096 two splits and the partial-sum reduction take 46 us
     // against 59 us unsplit).
-    const int32_t NC = (h / 16 + 3) / 4;
-    const int64_t ntbz = (T + kZTokens - 1) / kZTokens;
-    int64_t hs = ntbz >= 256 ? 1 : (256 + ntbz - 1) / ntbz;
-    if (hs > NC) hs = NC;
-    q.steps_per_split = (int32_t)((NC + hs - 1) / hs);  // chunks per split
-    q.hsplit = (NC + q.steps_per_split - 1) / q.steps_per_split;
+    zpass_split(T, h, &q.steps_per_split, &q.hsplit);
     const size_t zbytes = (size_t)T * r * sizeof(float);
     size_t off = 0;
     q.off_zparts = off;
@@ -1296,6 +1301,46 @@ static bool dispatch_local_k(const LowrankPlan& p, const uint16_t* x, const uint
             return true;
     }
     return false;
+}
+
+size_t zonly_workspace_bytes(int64_t T, int32_t h, int32_t r) {
+    int32_t sps, hs;
+    zpass_split(T, h, &sps, &hs);
+    return (hs > 1 ? align256((size_t)hs * T * r * sizeof(float)) : 0) +
+           align256((size_t)T * r * sizeof(uint16_t)) + align256((size_t)T * sizeof(float));
+}
+
+hipError_t zonly_launch(const uint16_t* x, const uint16_t* R1t, int64_t T, int32_t h, int32_t r,
+                        float* z, void* scratch, hipStream_t st) {
+    int32_t sps, hs;
+    zpass_split(T, h, &sps, &hs);
+    char* s = static_cast<char*>(scratch);
+    float* zparts = hs > 1 ? reinterpret_cast<float*>(s) : z;
+    const size_t o1 = hs > 1 ? align256((size_t)hs * T * r * sizeof(float)) : 0;
+    uint16_t* zhi = reinterpret_cast<uint16_t*>(s + o1);
+    float* cz = reinterpret_cast<float*>(s + o1 + align256((size_t)T * r * sizeof(uint16_t)));
+    const int64_t zblocks = (T + kZTokens - 1) / kZTokens;
+    const dim3 grid((unsigned)(zblocks * hs));  // no group-norm workgroups
+    constexpr int D = 2;
+    switch ((r / 16 + 1) / 2) {
+        case 1:
+            hipLaunchKernelGGL((zpass_kernel<1, D>), grid, dim3(256), 0, st, x, R1t, zparts,
+                               (int32_t)T, h, r, sps, nullptr, 0, (int32_t)zblocks, hs, nullptr,
+                               zhi, cz);
+            break;
+        case 2:
+            hipLaunchKernelGGL((zpass_kernel<2, D>), grid, dim3(256), 0, st, x, R1t, zparts,
+                               (int32_t)T, h, r, sps, nullptr, 0, (int32_t)zblocks, hs, nullptr,
+                               zhi, cz);
+            break;
+        default: return hipErrorInvalidValue;
+    }
+    if (hs > 1) {
+        const int64_t n = T * r;
+        hipLaunchKernelGGL(zreduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                           zparts, z, zhi, cz, (int32_t)T, r, hs);
+    }
+    return hipGetLastError();
 }
 
 hipError_t lowrank_launch(const LowrankPlan& p, const uint16_t* x, const uint16_t* R1t,

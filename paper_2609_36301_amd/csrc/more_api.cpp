@@ -102,7 +102,8 @@ more_status more_route_lowrank_ex(const uint16_t* x, const uint16_t* R1t, const 
                                   int32_t m_chunks, int32_t* idx, float* gate, float* topval,
                                   int32_t* counts, void* workspace, size_t workspace_bytes,
                                   void* stream) {
-    if (!x || !R1t || !R2t || !idx || !gate) return MORE_ERR_INVALID_ARG;
+    // the token-sized buffers of an empty batch may be NULL (an empty tensor has no storage)
+    if (!R1t || !R2t || (T != 0 && (!x || !idx || !gate))) return MORE_ERR_INVALID_ARG;
     if (!aligned(x, 16) || !aligned(R1t, 16) || !aligned(R2t, 16) || !aligned(idx, 4) ||
         !aligned(gate, 4) || !aligned(topval, 4) || !aligned(counts, 4) || !aligned(workspace, 16))
         return MORE_ERR_INVALID_ARG;
@@ -131,6 +132,86 @@ more_status more_route_lowrank(const uint16_t* x, const uint16_t* R1t, const uin
                                void* workspace, size_t workspace_bytes, void* stream) {
     return more_route_lowrank_ex(x, R1t, R2t, T, h, r, M, k, 0, idx, gate, topval, counts,
                                  workspace, workspace_bytes, stream);
+}
+
+static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Route plan and statistics plan of a training call; the workspace holds the route's workspace
+// followed by the statistics'.
+static bool train_plans(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                        more::LowrankPlan* lp, more::StatsPlan* sp, size_t* bytes) {
+    if (!more::lowrank_make_plan(T, h, r, M, k, 0, lp)) return false;
+    if (!more::stats_make_plan(T, h, r, M, k, lp->local != 0, sp)) return false;
+    *bytes = align256(lp->workspace_bytes) + sp->workspace_bytes;
+    return true;
+}
+
+more_status more_route_lowrank_train_workspace_size(int64_t T, int32_t h, int32_t r, int32_t M,
+                                                    int32_t k, size_t* bytes) {
+    if (!bytes) return MORE_ERR_INVALID_ARG;
+    more_status s = check_lowrank(T, h, r, M, k, 0);
+    if (s != MORE_OK) return s;
+    if (T == 0) {
+        *bytes = 0;
+        return MORE_OK;
+    }
+    more::LowrankPlan lp;
+    more::StatsPlan sp;
+    if (!train_plans(T, h, r, M, k, &lp, &sp, bytes)) return MORE_ERR_INVALID_ARG;
+    return MORE_OK;
+}
+
+more_status more_route_lowrank_train(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
+                                     int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
+                                     int32_t* idx, float* gate, float* topval, int32_t* counts,
+                                     float* m, float* Z, float* psum, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+    if (!R1t || !R2t || !psum || (T != 0 && (!x || !idx || !gate || !m || !Z)))
+        return MORE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(R1t, 16) || !aligned(R2t, 16) || !aligned(idx, 4) ||
+        !aligned(gate, 4) || !aligned(topval, 4) || !aligned(counts, 4) || !aligned(m, 4) ||
+        !aligned(Z, 4) || !aligned(psum, 4) || !aligned(workspace, 256))
+        return MORE_ERR_INVALID_ARG;
+    more_status s = check_lowrank(T, h, r, M, k, 0);
+    if (s != MORE_OK) return s;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (T == 0) {
+        if (counts) {
+            s = from_hip(more::histogram_launch(idx, 0, M, counts, st));
+            if (s != MORE_OK) return s;
+        }
+        return from_hip(more::stats_zero_psum(psum, M, st));
+    }
+    more::LowrankPlan lp;
+    more::StatsPlan sp;
+    size_t need = 0;
+    if (!train_plans(T, h, r, M, k, &lp, &sp, &need)) return MORE_ERR_INVALID_ARG;
+    if (!workspace || workspace_bytes < need) return MORE_ERR_WORKSPACE;
+    char* ws = static_cast<char*>(workspace);
+    char* sws = ws + align256(lp.workspace_bytes);
+    float* tv = topval ? topval : reinterpret_cast<float*>(sws + sp.off_tv);
+    hipError_t e = more::lowrank_launch(lp, x, R1t, R2t, T, h, r, M, k, idx, gate, tv, counts,
+                                        lp.local ? nullptr : ws, st);
+    if (e != hipSuccess) return MORE_ERR_HIP;
+    if (counts) {
+        e = more::histogram_launch(idx, T * (int64_t)k, M, counts, st, true);
+        if (e != hipSuccess) return MORE_ERR_HIP;
+    }
+    more::StatsArgs a;
+    a.x = x;
+    a.R1t = R1t;
+    a.R2t = R2t;
+    a.z = lp.local ? nullptr : reinterpret_cast<const float*>(ws + lp.off_z);
+    a.mtop = tv;
+    a.ks = k;
+    a.T = (int32_t)T;
+    a.h = h;
+    a.r = r;
+    a.M = M;
+    a.m = m;
+    a.Z = Z;
+    a.psum = psum;
+    return from_hip(more::stats_launch(sp, a, sws, st));
 }
 
 more_status more_route_fullrank_workspace_size(int64_t T, int32_t h, int32_t M, int32_t k,

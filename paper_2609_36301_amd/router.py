@@ -147,6 +147,81 @@ def route_lowrank(x: torch.Tensor, R1t: torch.Tensor, R2t: torch.Tensor, k: int,
     return router(x, R1t, R2t)
 
 
+@dataclasses.dataclass
+class TrainRouting(Routing):
+    """Routing plus the softmax statistics of the training forward pass."""
+    m: Optional[torch.Tensor] = None  # float32 [T], the top-1 logit
+    Z: Optional[torch.Tensor] = None  # float32 [T], sum_e exp(l_te - m_t)
+    psum: Optional[torch.Tensor] = None  # float32 [M], sum_t exp(l_te - m_t) / Z_t
+
+
+def lowrank_train_workspace_size(T: int, h: int, r: int, M: int, k: int) -> int:
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.load().more_route_lowrank_train_workspace_size(T, h, r, M, k,
+                                                                   ctypes.byref(n)),
+               "more_route_lowrank_train_workspace_size")
+    return n.value
+
+
+class LowrankTrainRouter:
+    """Pre-allocated outputs and workspace for repeated training-forward calls with one shape
+    (more_route_lowrank_train): the routing plus m, Z and psum."""
+
+    def __init__(self, T: int, h: int, r: int, M: int, k: int, *, device=None,
+                 topval: bool = False, histogram: bool = True):
+        self.shape = (T, h, r, M, k)
+        self.device = torch.device(device or "cuda")
+        dev = self.device
+        f32 = torch.float32
+        self.out = TrainRouting(
+            idx=torch.empty((T, k), dtype=torch.int32, device=dev),
+            gate=torch.empty((T, k), dtype=f32, device=dev),
+            topval=torch.empty((T, k), dtype=f32, device=dev) if topval else None,
+            counts=torch.empty((M,), dtype=torch.int32, device=dev) if histogram else None,
+            m=torch.empty((T,), dtype=f32, device=dev),
+            Z=torch.empty((T,), dtype=f32, device=dev),
+            psum=torch.empty((M,), dtype=f32, device=dev),
+        )
+        nbytes = lowrank_train_workspace_size(T, h, r, M, k)
+        self.workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+        self.workspace_bytes = nbytes
+
+    def __call__(self, x: torch.Tensor, R1t: torch.Tensor, R2t: torch.Tensor) -> TrainRouting:
+        T, h, r, M, k = self.shape
+        _check_bf16("x", x, 2)
+        _check_bf16("R1t", R1t, 2)
+        _check_bf16("R2t", R2t, 2)
+        if tuple(x.shape) != (T, h) or tuple(R1t.shape) != (r, h) or tuple(R2t.shape) != (M, r):
+            raise ValueError("shapes %s %s %s do not match the router's (T=%d, h=%d, r=%d, M=%d)"
+                             % (tuple(x.shape), tuple(R1t.shape), tuple(R2t.shape), T, h, r, M))
+        o = self.out
+        ws = _ptr(self.workspace) if self.workspace_bytes else None
+        st = _lib.load().more_route_lowrank_train(
+            _ptr(x), _ptr(R1t), _ptr(R2t), T, h, r, M, k, _ptr(o.idx), _ptr(o.gate),
+            _ptr(o.topval), _ptr(o.counts), _ptr(o.m), _ptr(o.Z), _ptr(o.psum), ws,
+            self.workspace_bytes, _stream(x.device))
+        _lib.check(st, "more_route_lowrank_train")
+        return o
+
+
+def route_lowrank_train(x: torch.Tensor, R1t: torch.Tensor, R2t: torch.Tensor, k: int, *,
+                        topval: bool = False, histogram: bool = True) -> TrainRouting:
+    """Training forward pass of the low-rank router: route_lowrank plus the row maximum m,
+    the softmax normaliser Z over all experts and the column sums psum of the row softmax."""
+    _check_bf16("x", x, 2)
+    _check_bf16("R1t", R1t, 2)
+    _check_bf16("R2t", R2t, 2)
+    T, h = x.shape
+    r, h2 = R1t.shape
+    M, r2 = R2t.shape
+    if h2 != h or r2 != r:
+        raise ValueError("inconsistent shapes x %s R1t %s R2t %s"
+                         % (tuple(x.shape), tuple(R1t.shape), tuple(R2t.shape)))
+    router = LowrankTrainRouter(T, h, r, M, k, device=x.device, topval=topval,
+                                histogram=histogram)
+    return router(x, R1t, R2t)
+
+
 class FullrankRouter:
     """Pre-allocated outputs and workspace (logits + GEMM scratch) for the full-rank router."""
 

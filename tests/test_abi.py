@@ -88,6 +88,9 @@ def test_lowrank_validation(lib, kw, status):
 
 def test_lowrank_empty_batch_is_a_no_op(lib):
     assert lowrank(lib, T=0) == _lib.OK
+    # an empty batch's token buffers may be NULL (torch gives empty tensors no storage)
+    assert lowrank(lib, T=0, x=None, idx=None, gate=None) == _lib.OK
+    assert lowrank(lib, T=0, R2t=None) == _lib.ERR_INVALID_ARG
 
 
 def test_lowrank_workspace_checked_before_launch(lib):
@@ -211,6 +214,52 @@ def test_dispatch_sort_validation(lib):
                                   None) == _lib.ERR_WORKSPACE
     assert lib.more_dispatch_sort(FAKE, 10, 4, 100, FAKE, FAKE, FAKE, 16,
                                   None) == _lib.ERR_WORKSPACE
+
+
+def train(lib, T=64, h=64, r=16, M=64, k=4, x=FAKE, idx=FAKE, gate=FAKE, m=FAKE, Z=FAKE,
+          psum=FAKE, ws=FAKE, wsb=1 << 30):
+    return lib.more_route_lowrank_train(x, FAKE, FAKE, T, h, r, M, k, idx, gate, None, None, m,
+                                        Z, psum, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), _lib.ERR_INVALID_ARG),
+    (dict(idx=None), _lib.ERR_INVALID_ARG),
+    (dict(m=None), _lib.ERR_INVALID_ARG),
+    (dict(Z=None), _lib.ERR_INVALID_ARG),
+    (dict(psum=None), _lib.ERR_INVALID_ARG),
+    (dict(psum=ctypes.c_void_p(0x10002)), _lib.ERR_INVALID_ARG),
+    (dict(ws=ctypes.c_void_p(0x10010)), _lib.ERR_INVALID_ARG),  # workspace: 256-byte aligned
+    (dict(T=-1), _lib.ERR_INVALID_ARG),
+    (dict(k=0), _lib.ERR_INVALID_ARG),
+    (dict(k=17), _lib.ERR_UNSUPPORTED),
+    (dict(r=48), _lib.ERR_UNSUPPORTED),
+    (dict(ws=None, wsb=0), _lib.ERR_WORKSPACE),
+    (dict(wsb=1000), _lib.ERR_WORKSPACE),
+])
+def test_train_validation(lib, kw, status):
+    assert train(lib, **kw) == status
+
+
+def test_train_workspace_size(lib):
+    n, route = ctypes.c_size_t(7), ctypes.c_size_t(0)
+    assert lib.more_route_lowrank_train_workspace_size(0, 512, 32, 4096, 8,
+                                                       ctypes.byref(n)) == _lib.OK
+    assert n.value == 0
+    assert lib.more_route_lowrank_train_workspace_size(16, 512, 32, 4096, 8,
+                                                       None) == _lib.ERR_INVALID_ARG
+    for T, h, r, M, k in [(256, 512, 16, 256, 8), (16384, 512, 32, 4096, 8),
+                          (32768, 2048, 64, 16384, 8), (16384, 4096, 64, 65536, 8),
+                          (128, 4096, 64, 262144, 16)]:
+        assert lib.more_route_lowrank_train_workspace_size(T, h, r, M, k,
+                                                           ctypes.byref(n)) == _lib.OK
+        assert lib.more_route_lowrank_workspace_size(T, h, r, M, k, ctypes.byref(route)) == 0
+        # the route's workspace, then at least an internal top-k buffer, z' hi/lo, the per-chunk
+        # normaliser partials and the psum partials
+        assert n.value >= route.value + T * k * 4 + T * r * 4 + T * 4 + M * 4
+    # workspace one byte short of the query is refused before any launch
+    assert lib.more_route_lowrank_train_workspace_size(64, 64, 16, 64, 4, ctypes.byref(n)) == 0
+    assert train(lib, wsb=n.value - 1) == _lib.ERR_WORKSPACE
 
 
 def test_binding_rejects_bad_tensors():
