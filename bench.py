@@ -288,6 +288,25 @@ def main():
                                        "algorithmic_bytes": dbytes}}
     del ds, dsrc
 
+    # Training forward pass on the same batches: the routing call plus the softmax statistics
+    # m, Z and psum over all experts (two expert sweeps).  Algorithmic flops of the statistics:
+    # the T x M logits once per sweep, 2 T r M each; the exponentials: T M per sweep.
+    trr = router.LowrankTrainRouter(w.T, w.h, w.r, w.M, w.k, device=dev, histogram=w.histogram)
+    tt = timed_graph(lambda i: trr(*bufs[i % nbuf]), args.steps, args.warmup)
+    stats_s = tt["mean_s"] - sec
+    sflops = 4 * w.T * w.r * w.M
+    sach = sflops / stats_s / 1e12
+    result["train"] = {
+        "op": "training forward (more_route_lowrank_train): routing + m, Z, psum over all experts",
+        "ms": round(tt["mean_s"] * 1e3, 5), "tokens_per_s": round(w.T / tt["mean_s"], 1),
+        "stats_ms": round(stats_s * 1e3, 5),
+        "stats_roofline": {"bound": "mfma", "achieved": round(sach, 2), "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": round(sach / PEAK_BF16_TFLOPS, 4),
+                           "algorithmic_flops": sflops,
+                           "exp_per_s": round(2 * w.T * w.M / stats_s, 1)}}
+    del trr
+    torch.cuda.empty_cache()
+
     if not args.no_fullrank:
         # full-rank router on the same token batches with W = R1 R2 rounded to bf16; logits
         # materialised in fp32 and in bf16; timed from HIP graphs like the low-rank router; the

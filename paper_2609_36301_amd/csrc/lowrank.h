@@ -90,6 +90,7 @@ struct StatsPlan {
     int32_t RC;
     int32_t chunks, splits;     // Z sweep: expert chunks x token splits
     int32_t eblocks, psplits;   // psum sweep: expert blocks x token splits
+    int32_t gz, gp;             // threads per output summing the Z and psum partials
     int32_t own_z;              // 1: z is computed here (the routing call keeps none)
     size_t off_tv, off_z, off_zscratch, off_zhl, off_mb, off_Zp, off_bias, off_part;
     size_t workspace_bytes;

@@ -143,136 +143,211 @@ __global__ __launch_bounds__(kRouteThreads, 1) void stats_z_kernel(
     }
 }
 
-// ------------------------------------------------------------------------------ combine
+// ------------------------------------------------------------------------------ partial sums
+// out[j] = sum over p < P of in[p N + j] in a fixed order: G threads per output (consecutive
+// blocks of 256 / G outputs per workgroup, the outputs fastest so that loads coalesce); thread q
+// sums p = q, q + G, ... in increasing order, then the G partials are added in order of q.
+template <typename Epilogue>
+__device__ __forceinline__ void column_sums(const float* __restrict__ in, int32_t P, int64_t N,
+                                            int G, float* red, Epilogue&& epi) {
+    const int per = 256 / G;
+    const int q = threadIdx.x / per, jj = threadIdx.x % per;
+    const int64_t j = (int64_t)blockIdx.x * per + jj;
+    float s = 0.0f;
+    if (j < N) {
+        int32_t p = q;
+        for (; p + 7 * G < P; p += 8 * G) {  // eight loads in flight, added in order
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = in[(int64_t)(p + u * G) * N + j];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; p < P; p += G) s += in[(int64_t)p * N + j];
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    if (q == 0 && j < N) {
+        float t = red[jj];
+        for (int qq = 1; qq < G; ++qq) t += red[qq * per + jj];
+        epi(j, t);
+    }
+}
+
+// Z[t] = the chunk partials in order; m[t]; bias[t] = -(m' + log2 Z) for the psum sweep.
 __global__ __launch_bounds__(256) void stats_combine_kernel(const float* __restrict__ Zp,
-                                                            int32_t chunks,
+                                                            int32_t chunks, int32_t G,
                                                             const float* __restrict__ mtop,
                                                             int32_t ks,
                                                             const float* __restrict__ mb,
                                                             int32_t T, float* __restrict__ m_out,
                                                             float* __restrict__ Z_out,
                                                             float* __restrict__ bias) {
-    const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (t >= T) return;
-    float s = 0.0f;
-    for (int32_t c = 0; c < chunks; ++c) s += Zp[(int64_t)c * T + t];
-    m_out[t] = mtop[t * ks];
-    Z_out[t] = s;
-    bias[t] = mb[t] - log2f(s);
+    __shared__ float red[256];
+    column_sums(Zp, chunks, T, G, red, [&](int64_t t, float z) {
+        m_out[t] = mtop[t * ks];
+        Z_out[t] = z;
+        bias[t] = mb[t] - log2f(z);
+    });
 }
 
 // ------------------------------------------------------------------------------ psum sweep
-// A workgroup of 4 waves owns 4 NE expert tiles (wave w tiles NE w .. NE w + NE - 1 of its
-// block), held as A operands in registers, and streams the 32-token tiles of its token split:
-// each lane keeps, per tile and accumulator element, the running sum over the tokens of its
-// column; the 32 columns are added up once at the end.  The token operands (z'_hi, z'_lo and
-// the bias) of the next tile are loaded while the current one is processed.
-constexpr int kPsumWaves = 4;
-constexpr int kPsumNE = 2;
-constexpr int kPsumExperts = 32 * kPsumNE * kPsumWaves;
+// A workgroup of 8 waves owns 8 NE expert tiles (wave w tiles NE w .. NE w + NE - 1 of its
+// block), held as B operands (expert columns) in registers, and streams the 32-token tiles of
+// its token split through LDS: stages of SB tiles (z'_hi, z'_lo and the bias of each token),
+// double buffered, loaded by the whole workgroup one stage ahead.  Tokens are the MFMA rows, so
+// a lane holds one expert column and sixteen token rows of each tile, adds the sixteen
+// probabilities, and keeps one running sum per expert tile; the two lane halves (disjoint token
+// rows) are added at the end.  The bias -(m' + log2 Z) of a row enters through the MFMA's C
+// operand, read from LDS as four 16-byte pieces per tile.
+constexpr int kPsumWaves = 8;
+constexpr int kPsumThreads = 64 * kPsumWaves;
+constexpr int kPsumSB = 4;  // token tiles per stage
 
-template <int RC, int NE>
-__global__ __launch_bounds__(64 * kPsumWaves, 2) void stats_psum_kernel(
+template <int RC>
+struct PsumCfg {
+    static constexpr int R = 16 * RC;
+    static constexpr int NE = 4;                                  // expert tiles per wave
+    static constexpr int EXPERTS = 32 * NE * kPsumWaves;          // experts per workgroup
+    static constexpr int ROW = 2 * R + 8;                         // bf16 per token row in LDS
+    static constexpr int SEGS = kPsumSB * 32 * (2 * R / 8);       // 16-byte pieces per stage
+    static constexpr int SEG_PER_THREAD = SEGS / kPsumThreads;
+    static_assert(SEGS % kPsumThreads == 0, "whole pieces per thread");
+};
+
+template <int RC>
+__global__ __launch_bounds__(kPsumThreads, 1) void stats_psum_kernel(
     const uint16_t* __restrict__ zhl, const float* __restrict__ bias,
     const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t eblocks, int32_t splits,
     float* __restrict__ part) {
-    constexpr int R = 16 * RC;
-    const int lane = threadIdx.x & 63;
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    using C = PsumCfg<RC>;
+    constexpr int R = C::R, NE = C::NE, ROW = C::ROW, SB = kPsumSB, SPT = C::SEG_PER_THREAD;
+    constexpr int RSEG = 2 * R / 8;  // 16-byte pieces per token (hi then lo)
+    __shared__ __attribute__((aligned(16))) uint16_t zs[2][SB * 32 * ROW];
+    __shared__ __attribute__((aligned(16))) float bs[2][SB * 32];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, half = lane >> 5;
     const int32_t eb = (int32_t)(blockIdx.x % (unsigned)eblocks);
     const int32_t split = (int32_t)(blockIdx.x / (unsigned)eblocks);
     const int64_t Tt = ((int64_t)T + 31) / 32;
     const int64_t tt0 = Tt * split / splits, tt1 = Tt * (split + 1) / splits;
+    const int ntiles = (int)(tt1 - tt0);
+    const int nstages = (ntiles + SB - 1) / SB;
     const int32_t Mt = (M + 31) / 32;
     const int32_t tile0 = (eb * kPsumWaves + w) * NE;
-    bf16x8 a[NE][RC];
+    const bool active = tile0 < Mt;  // wave-uniform; idle waves still stage tokens
+    bf16x8 b[NE][RC];
 #pragma unroll
     for (int j = 0; j < NE; ++j) {
         int64_t e = (int64_t)32 * (tile0 + j) + n;
-        e = e < M ? e : M - 1;  // rows past M: copies of row M - 1, never stored
+        e = e < M ? e : M - 1;  // columns past M: copies of expert M - 1, never stored
 #pragma unroll
-        for (int c = 0; c < RC; ++c) a[j][c] = load_bf16x8(R2t + e * R + 16 * c + 8 * half);
+        for (int c = 0; c < RC; ++c) b[j][c] = load_bf16x8(R2t + e * R + 16 * c + 8 * half);
     }
-    f32x16 pacc[NE];
+    // Stage loads: piece g of a stage is token g / RSEG of the stage, piece g % RSEG of its row.
+    u32x4 rg[SPT];
+    float rb = 0.0f;
+    auto gload = [&](int st) __attribute__((always_inline)) {
+        const int64_t tok0 = (tt0 + (int64_t)st * SB) * 32;
 #pragma unroll
-    for (int j = 0; j < NE; ++j) pacc[j] = zero_f32x16();
-    auto load_tok = [&](int64_t tt, bf16x8 (&b)[2 * RC], float& cb) __attribute__((always_inline)) {
-        const int64_t t = 32 * tt + n;
-        const bool ok = t < T;
-        const uint16_t* zr = zhl + (ok ? t : 0) * (2 * R) + 8 * half;
-#pragma unroll
-        for (int c = 0; c < RC; ++c) {
-            b[c] = load_bf16x8(zr + 16 * c);
-            b[RC + c] = load_bf16x8(zr + R + 16 * c);
+        for (int i = 0; i < SPT; ++i) {
+            const int g = tid + i * kPsumThreads;
+            int64_t t = tok0 + g / RSEG;
+            t = t < T ? t : T - 1;  // rows past T: bias kNoToken below
+            rg[i] = *reinterpret_cast<const u32x4*>(zhl + t * (2 * R) + 8 * (g % RSEG));
         }
-        const float v = bias[ok ? t : 0];
-        cb = ok ? v : kNoToken;
+        if (tid < SB * 32) {
+            const int64_t t = tok0 + tid;
+            const float v = bias[t < T ? t : T - 1];
+            rb = t < T ? v : kNoToken;
+        }
     };
-    if (tt0 < tt1 && tile0 < Mt) {  // wave-uniform
-        bf16x8 b[2 * RC], nb[2 * RC];
-        float cb, ncb = 0.0f;
-        load_tok(tt0, b, cb);
-        for (int64_t tt = tt0; tt < tt1; ++tt) {
-            if (tt + 1 < tt1) load_tok(tt + 1, nb, ncb);
-            f32x16 cin;
+    auto stash = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) cin[i] = cb;
-            f32x16 acc[NE];
+        for (int i = 0; i < SPT; ++i) {
+            const int g = tid + i * kPsumThreads;
+            *reinterpret_cast<u32x4*>(&zs[buf][(g / RSEG) * ROW + 8 * (g % RSEG)]) = rg[i];
+        }
+        if (tid < SB * 32) bs[buf][tid] = rb;
+    };
+    float pacc[NE];
 #pragma unroll
-            for (int j = 0; j < NE; ++j) acc[j] = mfma_32x32x16(a[j][0], b[0], cin);
+    for (int j = 0; j < NE; ++j) pacc[j] = 0.0f;
+    if (nstages > 0) {  // workgroup-uniform
+        gload(0);
+        stash(0);
+        if (nstages > 1) gload(1);
+        __syncthreads();
+        for (int st = 0; st < nstages; ++st) {
+            const int buf = st & 1;
+            const int cnt = min(SB, ntiles - st * SB);
+            if (active) {
 #pragma unroll
-            for (int c = 1; c < 2 * RC; ++c)
+                for (int tl = 0; tl < SB; ++tl) {
+                    if (tl < cnt) {
+                        const uint16_t* zr = &zs[buf][(tl * 32 + n) * ROW + 8 * half];
+                        bf16x8 a[2 * RC];
 #pragma unroll
-                for (int j = 0; j < NE; ++j) acc[j] = mfma_32x32x16(a[j][c % RC], b[c], acc[j]);
+                        for (int c = 0; c < 2 * RC; ++c) a[c] = load_bf16x8(zr + 16 * c);
+                        f32x16 cin;
 #pragma unroll
-            for (int j = 0; j < NE; ++j)
+                        for (int q = 0; q < 4; ++q) {
+                            const f32x4 v = *reinterpret_cast<const f32x4*>(
+                                &bs[buf][tl * 32 + 8 * q + 4 * half]);
 #pragma unroll
-                for (int i = 0; i < 16; ++i) pacc[j][i] += exp2_fast(acc[j][i]);
+                            for (int p = 0; p < 4; ++p) cin[4 * q + p] = v[p];
+                        }
+                        f32x16 acc[NE];
 #pragma unroll
-            for (int c = 0; c < 2 * RC; ++c) b[c] = nb[c];
-            cb = ncb;
+                        for (int j = 0; j < NE; ++j) acc[j] = mfma_32x32x16(a[0], b[j][0], cin);
+#pragma unroll
+                        for (int c = 1; c < 2 * RC; ++c)
+#pragma unroll
+                            for (int j = 0; j < NE; ++j)
+                                acc[j] = mfma_32x32x16(a[c], b[j][c % RC], acc[j]);
+#pragma unroll
+                        for (int j = 0; j < NE; ++j) {
+                            float s = 0.0f;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) s += exp2_fast(acc[j][i]);
+                            pacc[j] += s;
+                        }
+                    }
+                }
+            }
+            if (st + 1 < nstages) stash(buf ^ 1);
+            if (st + 2 < nstages) gload(st + 2);
+            __syncthreads();
         }
     }
-    // sum over the 32 token columns of each lane half (a butterfly: every lane gets the total)
+    // the two lane halves hold disjoint token rows of the same expert column
 #pragma unroll
-    for (int j = 0; j < NE; ++j)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-            float v = pacc[j][i];
-            v += lane_xor<1>(v);
-            v += lane_xor<2>(v);
-            v += lane_xor<4>(v);
-            v += lane_xor<8>(v);
-            v += lane_xor<16>(v);
-            pacc[j][i] = v;
-        }
-    if (n == 0) {
-#pragma unroll
-        for (int j = 0; j < NE; ++j) {
-            if (tile0 + j >= Mt) continue;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) {
-                const int32_t e = 32 * (tile0 + j) + acc_row(i, half);
-                if (e < M) part[(int64_t)split * M + e] = pacc[j][i];
-            }
-        }
+    for (int j = 0; j < NE; ++j) {
+        const float tot = sum_pair32(pacc[j]);
+        const int32_t e = 32 * (tile0 + j) + n;
+        if (half == 0 && tile0 + j < Mt && e < M) part[(int64_t)split * M + e] = tot;
     }
 }
 
-// psum[e] = sum of the split partials in split order (0 when there are none).
+// psum[e] = the split partials in order (0 when there are none).
 __global__ __launch_bounds__(256) void stats_reduce_kernel(const float* __restrict__ part,
-                                                           int32_t splits, int32_t M,
+                                                           int32_t splits, int32_t G, int32_t M,
                                                            float* __restrict__ psum) {
-    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (e >= M) return;
-    float s = 0.0f;
-    for (int32_t p = 0; p < splits; ++p) s += part[(int64_t)p * M + e];
-    psum[e] = s;
+    __shared__ float red[256];
+    column_sums(part, splits, M, G, red, [&](int64_t e, float v) { psum[e] = v; });
 }
 
 // ------------------------------------------------------------------------------ host side
 static size_t align256s(size_t b) { return (b + 255) & ~(size_t)255; }
+
+// Threads per output of column_sums for P partials: about eight partials per thread, at most 16.
+static int32_t sum_group(int64_t P) {
+    int32_t G = 1;
+    while (G < 16 && (int64_t)G * 8 < P) G *= 2;
+    return G;
+}
 
 bool stats_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, bool own_z,
                      StatsPlan* out) {
@@ -293,14 +368,17 @@ bool stats_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, bool
     if (S < 1) S = 1;
     if (S > ntb) S = ntb;
     q.splits = (int32_t)S;
-    // psum sweep: expert blocks of 256, about 1024 workgroups in all
-    const int64_t eb = (M + kPsumExperts - 1) / kPsumExperts;
+    // psum sweep: expert blocks of 32 NE waves tiles, about 512 workgroups in all
     const int64_t Tt = (T + 31) / 32;
-    int64_t P = (1024 + eb - 1) / eb;
+    const int64_t per_block = PsumCfg<1>::EXPERTS;  // the same for every rank
+    const int64_t eb = (M + per_block - 1) / per_block;
+    int64_t P = (512 + eb - 1) / eb;
     if (P > Tt) P = Tt;
     if (P < 1) P = 1;
     q.eblocks = (int32_t)eb;
     q.psplits = (int32_t)P;
+    q.gz = sum_group(C);
+    q.gp = sum_group(P);
     q.own_z = own_z ? 1 : 0;
     size_t o = 0;
     q.off_tv = o;
@@ -331,11 +409,12 @@ static void launch_stats_sweeps(const StatsPlan& p, const StatsArgs& a, const ui
     hipLaunchKernelGGL((stats_z_kernel<RC>), dim3((unsigned)((int64_t)p.chunks * p.splits)),
                        dim3(kRouteThreads), 0, st, zhl, mb, a.R2t, a.T, a.M, p.chunks, p.splits,
                        Zp);
-    hipLaunchKernelGGL(stats_combine_kernel, dim3((unsigned)((a.T + 255) / 256)), dim3(256), 0, st,
-                       Zp, p.chunks, a.mtop, a.ks, mb, a.T, a.m, a.Z, bias);
-    hipLaunchKernelGGL((stats_psum_kernel<RC, kPsumNE>),
-                       dim3((unsigned)((int64_t)p.eblocks * p.psplits)), dim3(64 * kPsumWaves), 0,
-                       st, zhl, bias, a.R2t, a.T, a.M, p.eblocks, p.psplits, part);
+    const int64_t zper = 256 / p.gz;
+    hipLaunchKernelGGL(stats_combine_kernel, dim3((unsigned)((a.T + zper - 1) / zper)), dim3(256),
+                       0, st, Zp, p.chunks, p.gz, a.mtop, a.ks, mb, a.T, a.m, a.Z, bias);
+    hipLaunchKernelGGL((stats_psum_kernel<RC>), dim3((unsigned)((int64_t)p.eblocks * p.psplits)),
+                       dim3(kPsumThreads), 0, st, zhl, bias, a.R2t, a.T, a.M, p.eblocks,
+                       p.psplits, part);
 }
 
 hipError_t stats_launch(const StatsPlan& p, const StatsArgs& a, void* workspace, hipStream_t st) {
@@ -361,14 +440,15 @@ hipError_t stats_launch(const StatsPlan& p, const StatsArgs& a, void* workspace,
         case 4: launch_stats_sweeps<4>(p, a, zhl, mb, Zp, bias, part, st); break;
         default: return hipErrorInvalidValue;
     }
-    hipLaunchKernelGGL(stats_reduce_kernel, dim3((unsigned)((a.M + 255) / 256)), dim3(256), 0, st,
-                       part, p.psplits, a.M, a.psum);
+    const int64_t pper = 256 / p.gp;
+    hipLaunchKernelGGL(stats_reduce_kernel, dim3((unsigned)((a.M + pper - 1) / pper)), dim3(256), 0,
+                       st, part, p.psplits, p.gp, a.M, a.psum);
     return hipGetLastError();
 }
 
 hipError_t stats_zero_psum(float* psum, int32_t M, hipStream_t st) {
     hipLaunchKernelGGL(stats_reduce_kernel, dim3((unsigned)((M + 255) / 256)), dim3(256), 0, st,
-                       nullptr, 0, M, psum);
+                       nullptr, 0, 1, M, psum);
     return hipGetLastError();
 }
 
