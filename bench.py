@@ -309,8 +309,8 @@ def main():
 
     if not args.no_fullrank:
         # full-rank router on the same token batches with W = R1 R2 rounded to bf16; logits
-        # materialised in fp32 and in bf16; timed from HIP graphs like the low-rank router; the
-        # speedup uses the faster of the two.
+        # materialised in fp32 and in bf16, and (h <= 2112) the fused router that writes none;
+        # timed from HIP graphs like the low-rank router; the speedup uses the fastest.
         from paper_2609_36301_amd.inputs import bf16_bits_to_f32, f32_to_bf16_bits
         W = bf16_bits_to_f32(inp.R1).astype(np.float64) @ bf16_bits_to_f32(inp.R2).astype(
             np.float64)
@@ -323,7 +323,15 @@ def main():
             fr[key] = round(ft["mean_s"] * 1e3, 5)
             del frr
             torch.cuda.empty_cache()
-        best = min(fr["fp32_logits_ms"], fr["bf16_logits_ms"])
+        if w.h <= 2112:
+            # fused standard router (no logits written): rows of x per token block in LDS,
+            # the rows of W streamed through the matrix cores for every block
+            ffr = router.FusedFullrankRouter(w.T, w.h, w.M, w.k, device=dev)
+            ft = timed_graph(lambda i: ffr(bufs[i % nbuf][0], Wt), fsteps, 2)
+            fr["fused_ms"] = round(ft["mean_s"] * 1e3, 5)
+            del ffr
+            torch.cuda.empty_cache()
+        best = min(v for key, v in fr.items() if key.endswith("_ms"))
         fr["speedup_lowrank_vs_fullrank"] = round(best / (sec * 1e3), 3)
         fr["speedup_target"] = round(w.M / (2 * w.r) * w.h / (w.h + w.M), 3)
         fr["timed_steps"] = fsteps

@@ -179,6 +179,27 @@ more_status more_route_fullrank_workspace_size(int64_t T, int32_t h, int32_t M, 
                                                int32_t logit_bits, size_t* bytes);
 
 /*
+ * Fused full-rank (standard) router, the stronger baseline (efficiency appendix, "Fusing a
+ * standard MoE layer": the low-rank router's fusion with the rank replaced by h).  Same result
+ * definition and arguments as more_route_fullrank with fp32 logits, but the T x M logits are
+ * never written: a workgroup keeps the x rows of 32-128 tokens in LDS, streams the rows of Wt
+ * through the matrix cores (fp32 accumulation of exact bf16 products) and folds each logit
+ * into register top-k lists.  The rows of Wt are re-read for every token block, so this suits
+ * small h and M (the paper finds the fusion's benefit vanishing at large h).
+ *   workspace   at least more_route_fullrank_fused_workspace_size() bytes (the lists of the
+ *               expert splits; 0 bytes when one workgroup sweeps all experts of a token block)
+ * Limits: h <= 2112 (the x rows of 32 tokens fit one workgroup's LDS), k <= 32; larger h returns
+ * MORE_ERR_UNSUPPORTED.  Logits can differ from more_route_fullrank's in the last bits (another
+ * fp32 summation order).
+ */
+more_status more_route_fullrank_fused(const uint16_t* x, const uint16_t* Wt, int64_t T, int32_t h,
+                                      int32_t M, int32_t k, int32_t* idx, float* gate,
+                                      float* topval, void* workspace, size_t workspace_bytes,
+                                      void* stream);
+more_status more_route_fullrank_fused_workspace_size(int64_t T, int32_t h, int32_t M, int32_t k,
+                                                     size_t* bytes);
+
+/*
  * Per-expert histogram of a selection (the bincount behind the load-balancing statistic,
  * Appendix "Training"): counts[e] = #{(t, j) : idx[t][j] == e}.
  *   idx     int32 [T][k]   selections; every entry must lie in [0, M)

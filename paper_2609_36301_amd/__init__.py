@@ -8,7 +8,8 @@ a ctypes binding with torch tensors (`router`), and the seeded input generator (
     out = route_lowrank(x, R1t, R2t, k)      # out.idx [T][k] int32, out.gate [T][k] fp32
     tr = route_lowrank_train(x, R1t, R2t, k) # + tr.m, tr.Z [T], tr.psum [M] fp32
 """
-__all__ = ["route_lowrank", "route_lowrank_train", "route_fullrank", "expert_histogram",
+__all__ = ["route_lowrank", "route_lowrank_train", "route_fullrank", "route_fullrank_fused",
+           "expert_histogram",
            "dispatch_sort", "LowrankRouter", "LowrankTrainRouter", "lowrank_workspace_size",
            "lowrank_train_workspace_size", "lowrank_plan", "lowrank_route",
            "fullrank_workspace_size", "Routing", "TrainRouting"]

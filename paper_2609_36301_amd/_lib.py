@@ -35,6 +35,9 @@ SIGNATURES = {
     "more_route_fullrank": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _SZ,
                                    _P]),
     "more_route_fullrank_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _I32, _PSZ]),
+    "more_route_fullrank_fused": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _SZ,
+                                         _P]),
+    "more_route_fullrank_fused_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _PSZ]),
     "more_expert_histogram": (_I32, [_P, _I64, _I32, _I32, _P, _P]),
     "more_dispatch_sort": (_I32, [_P, _I64, _I32, _I32, _P, _P, _P, _SZ, _P]),
     "more_dispatch_sort_workspace_size": (_I32, [_I64, _I32, _I32, _PSZ]),

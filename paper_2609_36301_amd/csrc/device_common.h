@@ -87,20 +87,24 @@ __device__ __forceinline__ void list_init(float (&v)[K], int32_t (&ix)[K]) {
 }
 
 // Insert a candidate whose expert id is larger than every id already in the list (a lane
-// visits its experts in increasing order), so "better" reduces to a strict value compare.
-// The last pair falls off the end.
+// visits its experts in increasing order): it goes after every entry with a value at least its
+// own (a strict value compare), and the entries after it shift down by one in their order (an
+// entry carried down is never compared again: with equal values it must stay ahead of the
+// entries it was ahead of).  The last pair falls off the end.
 template <int K>
 __device__ __forceinline__ void list_insert_newer(float (&v)[K], int32_t (&ix)[K], float nv,
                                                   int32_t ni) {
+    bool placed = false;
 #pragma unroll
     for (int j = 0; j < K; ++j) {
-        bool b = nv > v[j];
+        const bool b = placed || nv > v[j];
         float tv = v[j];
         int32_t ti = ix[j];
         v[j] = b ? nv : tv;
         ix[j] = b ? ni : ti;
         nv = b ? tv : nv;
         ni = b ? ti : ni;
+        placed = b;
     }
 }
 

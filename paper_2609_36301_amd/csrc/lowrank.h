@@ -111,6 +111,22 @@ hipError_t stats_launch(const StatsPlan& plan, const StatsArgs& a, void* workspa
                         hipStream_t stream);
 hipError_t stats_zero_psum(float* psum, int32_t M, hipStream_t stream);
 
+// Fused standard router (fullrank_fused.hip): x rows of a token block resident in LDS, the
+// logits of each expert tile folded into register top-K lists.
+struct FusedFullrankPlan {
+    int32_t NT;        // 32-token tiles per workgroup
+    int32_t K;         // list length (power of two >= k)
+    int32_t esplits;   // workgroups sharing the expert axis of one token block
+    size_t workspace_bytes;  // the splits' lists (none with one split)
+};
+
+// false when the x rows of one 32-token tile do not fit the workgroup's LDS (h > 2112) or k > 32
+bool fullrank_fused_make_plan(int64_t T, int32_t h, int32_t M, int32_t k, FusedFullrankPlan* plan);
+hipError_t fullrank_fused_launch(const FusedFullrankPlan& plan, const uint16_t* x,
+                                 const uint16_t* Wt, int64_t T, int32_t h, int32_t M, int32_t k,
+                                 int32_t* idx, float* gate, float* topval, void* workspace,
+                                 hipStream_t stream);
+
 // Dispatch bookkeeping (dispatch.hip): N = T k entries, keys 0 .. M.
 int dispatch_passes(int32_t M);
 size_t dispatch_workspace_bytes(int64_t N);

@@ -251,6 +251,36 @@ more_status more_route_fullrank(const uint16_t* x, const uint16_t* Wt, int64_t T
     return from_hip(e);
 }
 
+more_status more_route_fullrank_fused_workspace_size(int64_t T, int32_t h, int32_t M, int32_t k,
+                                                     size_t* bytes) {
+    if (!bytes) return MORE_ERR_INVALID_ARG;
+    more_status s = check_common(T, h, M, k);
+    if (s != MORE_OK) return s;
+    more::FusedFullrankPlan p;
+    if (!more::fullrank_fused_make_plan(T > 0 ? T : 1, h, M, k, &p)) return MORE_ERR_UNSUPPORTED;
+    *bytes = T == 0 ? 0 : p.workspace_bytes;
+    return MORE_OK;
+}
+
+more_status more_route_fullrank_fused(const uint16_t* x, const uint16_t* Wt, int64_t T, int32_t h,
+                                      int32_t M, int32_t k, int32_t* idx, float* gate,
+                                      float* topval, void* workspace, size_t workspace_bytes,
+                                      void* stream) {
+    if (!Wt || (T != 0 && (!x || !idx || !gate))) return MORE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(Wt, 16) || !aligned(idx, 4) || !aligned(gate, 4) ||
+        !aligned(topval, 4) || !aligned(workspace, 16))
+        return MORE_ERR_INVALID_ARG;
+    size_t need = 0;
+    more_status s = more_route_fullrank_fused_workspace_size(T, h, M, k, &need);
+    if (s != MORE_OK) return s;
+    if (T == 0) return MORE_OK;
+    if (need > 0 && (!workspace || workspace_bytes < need)) return MORE_ERR_WORKSPACE;
+    more::FusedFullrankPlan p;
+    more::fullrank_fused_make_plan(T, h, M, k, &p);
+    return from_hip(more::fullrank_fused_launch(p, x, Wt, T, h, M, k, idx, gate, topval, workspace,
+                                                static_cast<hipStream_t>(stream)));
+}
+
 more_status more_dispatch_sort_workspace_size(int64_t T, int32_t k, int32_t M, size_t* bytes) {
     if (!bytes || T < 0 || k < 1 || M < 1) return MORE_ERR_INVALID_ARG;
     if (T > kMaxT || M >= kMaxM || T * (int64_t)k > kMaxT) return MORE_ERR_UNSUPPORTED;

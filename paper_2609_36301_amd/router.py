@@ -266,6 +266,55 @@ def route_fullrank(x: torch.Tensor, Wt: torch.Tensor, k: int, *, topval: bool = 
     return FullrankRouter(T, h, M, k, device=x.device, topval=topval, logit_bits=logit_bits)(x, Wt)
 
 
+def fullrank_fused_workspace_size(T: int, h: int, M: int, k: int) -> int:
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.load().more_route_fullrank_fused_workspace_size(T, h, M, k, ctypes.byref(n)),
+               "more_route_fullrank_fused_workspace_size")
+    return n.value
+
+
+class FusedFullrankRouter:
+    """Pre-allocated outputs and workspace for the fused full-rank router (no logits written)."""
+
+    def __init__(self, T: int, h: int, M: int, k: int, *, device=None, topval: bool = False):
+        self.shape = (T, h, M, k)
+        dev = torch.device(device or "cuda")
+        self.out = Routing(
+            idx=torch.empty((T, k), dtype=torch.int32, device=dev),
+            gate=torch.empty((T, k), dtype=torch.float32, device=dev),
+            topval=torch.empty((T, k), dtype=torch.float32, device=dev) if topval else None)
+        self.workspace_bytes = fullrank_fused_workspace_size(T, h, M, k)
+        self.workspace = torch.empty((max(self.workspace_bytes, 1),), dtype=torch.uint8,
+                                     device=dev)
+
+    def __call__(self, x: torch.Tensor, Wt: torch.Tensor) -> Routing:
+        T, h, M, k = self.shape
+        _check_bf16("x", x, 2)
+        _check_bf16("Wt", Wt, 2)
+        if tuple(x.shape) != (T, h) or tuple(Wt.shape) != (M, h):
+            raise ValueError("shapes %s %s do not match (T=%d, h=%d, M=%d)"
+                             % (tuple(x.shape), tuple(Wt.shape), T, h, M))
+        o = self.out
+        ws = _ptr(self.workspace) if self.workspace_bytes else None
+        st = _lib.load().more_route_fullrank_fused(_ptr(x), _ptr(Wt), T, h, M, k, _ptr(o.idx),
+                                                   _ptr(o.gate), _ptr(o.topval), ws,
+                                                   self.workspace_bytes, _stream(x.device))
+        _lib.check(st, "more_route_fullrank_fused")
+        return o
+
+
+def route_fullrank_fused(x: torch.Tensor, Wt: torch.Tensor, k: int, *,
+                         topval: bool = False) -> Routing:
+    """softmax(TopK(x W)) with Wt = W^T [M][h], fused: no logits written (h <= 2112)."""
+    _check_bf16("x", x, 2)
+    _check_bf16("Wt", Wt, 2)
+    T, h = x.shape
+    M, h2 = Wt.shape
+    if h2 != h:
+        raise ValueError("inconsistent shapes x %s Wt %s" % (tuple(x.shape), tuple(Wt.shape)))
+    return FusedFullrankRouter(T, h, M, k, device=x.device, topval=topval)(x, Wt)
+
+
 def expert_histogram(idx: torch.Tensor, M: int) -> torch.Tensor:
     """counts[e] = number of entries of idx (int32 [T][k]) equal to e."""
     if idx.dtype != torch.int32 or idx.dim() != 2 or not idx.is_contiguous():

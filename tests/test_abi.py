@@ -262,6 +262,33 @@ def test_train_workspace_size(lib):
     assert train(lib, wsb=n.value - 1) == _lib.ERR_WORKSPACE
 
 
+def test_fullrank_fused_validation(lib):
+    n = ctypes.c_size_t(0)
+    # one token block of 100 tokens against 40000 experts: many expert splits, lists in workspace
+    assert lib.more_route_fullrank_fused_workspace_size(100, 256, 40000, 8, ctypes.byref(n)) == 0
+    assert n.value > 0
+    assert lib.more_route_fullrank_fused_workspace_size(0, 256, 40000, 8, ctypes.byref(n)) == 0
+    assert n.value == 0
+    # the x rows of 32 tokens must fit a workgroup's LDS: h <= 2112
+    assert lib.more_route_fullrank_fused_workspace_size(100, 2112, 4000, 8, ctypes.byref(n)) == 0
+    assert lib.more_route_fullrank_fused_workspace_size(
+        100, 2128, 4000, 8, ctypes.byref(n)) == _lib.ERR_UNSUPPORTED
+    assert lib.more_route_fullrank_fused_workspace_size(
+        100, 512, 4000, 33, ctypes.byref(n)) == _lib.ERR_UNSUPPORTED
+    assert lib.more_route_fullrank_fused_workspace_size(100, 72, 4000, 8,
+                                                        ctypes.byref(n)) == _lib.ERR_UNSUPPORTED
+    call = lambda **kw: lib.more_route_fullrank_fused(
+        kw.get("x", FAKE), kw.get("Wt", FAKE), kw.get("T", 100), kw.get("h", 256),
+        kw.get("M", 40000), kw.get("k", 8), kw.get("idx", FAKE), kw.get("gate", FAKE), None,
+        kw.get("ws", FAKE), kw.get("wsb", 1 << 30), None)
+    assert call(x=None) == _lib.ERR_INVALID_ARG
+    assert call(Wt=ODD) == _lib.ERR_INVALID_ARG
+    assert call(k=0) == _lib.ERR_INVALID_ARG
+    assert call(h=4096) == _lib.ERR_UNSUPPORTED
+    assert call(ws=None, wsb=0) == _lib.ERR_WORKSPACE
+    assert call(T=0, x=None, idx=None, gate=None) == _lib.OK
+
+
 def test_binding_rejects_bad_tensors():
     import torch
     from paper_2609_36301_amd import router

@@ -44,6 +44,27 @@ def test_fullrank_fp32_logits_parity(shape):
     assert rep.ok(), str(rep)
 
 
+@pytest.mark.parametrize("bits", [32, 16])
+def test_fullrank_exact_ties_keep_the_selection_order(bits):
+    """Duplicated columns of W tie exactly: the row top-k must keep equal logits in expert-id
+    order also when a later, larger logit shifts them down its register list."""
+    T, h, r, M, k = 700, 256, 16, 3000, 8
+    inp = make_inputs(T, h, r, M, seed=91)
+    Wb = _w_bf16(inp)
+    rng = np.random.default_rng(92)
+    src = rng.choice(M, size=M // 10, replace=False)
+    dst = rng.choice(np.setdiff1d(np.arange(M), src), size=src.size, replace=False)
+    Wb[:, dst] = Wb[:, src]
+    idx, gate, topval = _fullrank(inp, Wb, k, bits, "fullrank ties")
+    parity.check_valid(idx, gate, M, topval)  # (logit descending, id ascending) order
+    if bits == 32:
+        orc = oracle.route_fullrank(inp.x, Wb, k)
+        picked = oracle.fullrank_logits_at(inp.x, Wb, np.arange(T), idx)
+        rep = parity.compare(orc, idx, gate, k, M, picked, topval)
+        print("[parity] fullrank ties %s" % rep, flush=True)
+        assert rep.ok(), str(rep)
+
+
 @pytest.mark.parametrize("shape", [(2000, 512, 32, 4096, 8), (700, 256, 32, 1003, 16)],
                          ids=lambda s: "T%d_M%d_k%d" % (s[0], s[3], s[4]))
 def test_fullrank_bf16_logits_valid(shape):
