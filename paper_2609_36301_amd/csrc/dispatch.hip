@@ -13,7 +13,8 @@
 //                         rounds), added to its (digit, block) start: the totals of the smaller
 //                         digits (a 256-wide scan in LDS) plus the digit's block prefix.
 // dsort_offsets_kernel derives offsets from the sorted keys: offsets[e] = the first slot whose
-// key is at least e.
+// key is at least e.  Up to 4096 entries (decode-sized batches) one workgroup runs all passes in
+// LDS instead (dsort_small_kernel).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -157,16 +158,130 @@ __global__ __launch_bounds__(kDsThreads) void dsort_scatter_kernel(
     }
 }
 
-// offsets[e] = the first slot i whose key is at least e (N if none), for e = 0 .. M: slot i
-// writes the e in (key[i - 1], key[i]], the last slot also those above its key.
-__global__ __launch_bounds__(256) void dsort_offsets_kernel(const int32_t* __restrict__ keys,
-                                                            int64_t N, int32_t M,
-                                                            int32_t* __restrict__ offsets) {
+// offsets[e] = the first slot i whose key is at least e (N if none), for e = 0 .. M.  With at
+// least as many entries as experts, slot i writes the e in (key[i - 1], key[i]] (the last slot
+// also those above its key): a few writes per slot.  With fewer entries, one thread per expert
+// searches the sorted keys (coalesced writes; the first levels of neighbouring threads' searches
+// read the same slots), since the gaps between keys would make the per-slot writes long.
+__global__ __launch_bounds__(256) void dsort_offsets_gap_kernel(const int32_t* __restrict__ keys,
+                                                                int64_t N, int32_t M,
+                                                                int32_t* __restrict__ offsets) {
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i <= N;
          i += (int64_t)gridDim.x * blockDim.x) {
         const int32_t lo = i == 0 ? -1 : keys[i - 1];
         const int32_t hi = i == N ? M : keys[i];
         for (int32_t e = lo + 1; e <= hi && e <= M; ++e) offsets[e] = (int32_t)i;
+    }
+}
+
+__global__ __launch_bounds__(256) void dsort_offsets_kernel(const int32_t* __restrict__ keys,
+                                                            int64_t N, int32_t M,
+                                                            int32_t* __restrict__ offsets) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e > M) return;
+    int64_t lo = 0, hi = N;  // keys[lo - 1] < e <= keys[hi] (virtual ends)
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (keys[mid] < e)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    offsets[e] = (int32_t)lo;
+}
+
+// All passes of the sort in one workgroup, for at most kDsSmallN entries: keys and positions
+// ping-pong between two LDS buffers; per pass a digit histogram, its exclusive scan, then the
+// entries in rounds of 1024 (entry order): ranks within a wave from ballots, counts of the
+// earlier waves of the round per digit, and each digit's running base across rounds.  The
+// sorted keys go to keys_out (for the offsets) and the positions to sorted.
+constexpr int kDsSmallThreads = 1024;
+constexpr int kDsSmallN = 4096;
+constexpr int kDsSmallWaves = kDsSmallThreads / 64;
+
+__global__ __launch_bounds__(kDsSmallThreads) void dsort_small_kernel(
+    const int32_t* __restrict__ idx, int32_t N, int32_t M, int passes,
+    int32_t* __restrict__ keys_out, int32_t* __restrict__ sorted) {
+    __shared__ int32_t kbuf[2][kDsSmallN];
+    __shared__ int32_t vbuf[2][kDsSmallN];
+    __shared__ int32_t cnt[kDsSmallWaves][kDsDigits];
+    __shared__ int32_t base[kDsDigits];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int i = tid; i < N; i += kDsSmallThreads) {
+        kbuf[0][i] = ds_key(idx[i], M);
+        vbuf[0][i] = i;
+    }
+    int cur = 0;
+    for (int p = 0; p < passes; ++p) {
+        const int shift = 8 * p;
+        if (tid < kDsDigits) base[tid] = 0;
+        __syncthreads();
+        for (int i = tid; i < N; i += kDsSmallThreads)
+            atomicAdd(&base[(kbuf[cur][i] >> shift) & (kDsDigits - 1)], 1);
+        __syncthreads();
+        if (tid < 64) {  // exclusive scan of the 256 digit counts by one wave, four per lane
+            int32_t v[4], sum = 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[i] = base[4 * tid + i];
+                sum += v[i];
+            }
+            int32_t incl = sum;
+            for (int d = 1; d < 64; d <<= 1) {
+                const int32_t u = __shfl_up(incl, d, 64);
+                incl += tid >= d ? u : 0;
+            }
+            int32_t run = incl - sum;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                base[4 * tid + i] = run;
+                run += v[i];
+            }
+        }
+        __syncthreads();
+        for (int r0 = 0; r0 < N; r0 += kDsSmallThreads) {
+            for (int i = tid; i < kDsSmallWaves * kDsDigits; i += kDsSmallThreads)
+                (&cnt[0][0])[i] = 0;
+            __syncthreads();
+            const int g = r0 + tid;
+            const bool ok = g < N;
+            const int32_t key = ok ? kbuf[cur][g] : 0;
+            const int32_t val = ok ? vbuf[cur][g] : 0;
+            const int d = (key >> shift) & (kDsDigits - 1);
+            uint64_t peers = __ballot(ok);  // lanes of this wave with the same digit
+#pragma unroll
+            for (int bit = 0; bit < 8; ++bit) {
+                const uint64_t m = __ballot((d >> bit) & 1);
+                peers &= ((d >> bit) & 1) ? m : ~m;
+            }
+            const int rank = __popcll(peers & below);
+            if (ok && (peers & below) == 0) cnt[w][d] = __popcll(peers);
+            __syncthreads();
+            if (tid < kDsDigits) {  // digit tid: exclusive offsets of the waves, then the base
+                int32_t run = base[tid];
+                for (int ww = 0; ww < kDsSmallWaves; ++ww) {
+                    const int32_t c = cnt[ww][tid];
+                    cnt[ww][tid] = run;
+                    run += c;
+                }
+                base[tid] = run;  // the next round's entries of this digit follow
+            }
+            __syncthreads();
+            if (ok) {
+                const int dest = cnt[w][d] + rank;
+                if (dest < N) {  // always true; keeps every write in bounds regardless
+                    kbuf[cur ^ 1][dest] = key;
+                    vbuf[cur ^ 1][dest] = val;
+                }
+            }
+            __syncthreads();
+        }
+        cur ^= 1;
+    }
+    for (int i = tid; i < N; i += kDsSmallThreads) {
+        keys_out[i] = kbuf[cur][i];
+        sorted[i] = vbuf[cur][i];
     }
 }
 
@@ -201,6 +316,15 @@ hipError_t dispatch_launch(const int32_t* idx, int64_t N, int32_t M, int32_t* of
     const int64_t nblocks = (N + kDsBlock - 1) / kDsBlock;
     auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
     char* ws = static_cast<char*>(workspace);
+    const unsigned oblocks = (unsigned)(((int64_t)M + 1 + 255) / 256);
+    if (N <= kDsSmallN) {  // one workgroup sorts, a second launch derives the offsets
+        int32_t* keys = reinterpret_cast<int32_t*>(ws);
+        hipLaunchKernelGGL(dsort_small_kernel, dim3(1), dim3(kDsSmallThreads), 0, st, idx,
+                           (int32_t)N, M, dispatch_passes(M), keys, sorted);
+        hipLaunchKernelGGL(dsort_offsets_kernel, dim3(oblocks), dim3(256), 0, st, keys, N, M,
+                           offsets);
+        return hipGetLastError();
+    }
     int32_t* keys[2] = {reinterpret_cast<int32_t*>(ws), reinterpret_cast<int32_t*>(ws + al((size_t)N * 4))};
     int32_t* vals[2] = {reinterpret_cast<int32_t*>(ws + 2 * al((size_t)N * 4)),
                         reinterpret_cast<int32_t*>(ws + 3 * al((size_t)N * 4))};
@@ -222,10 +346,15 @@ hipError_t dispatch_launch(const int32_t* idx, int64_t N, int32_t M, int32_t* of
         hipLaunchKernelGGL(dsort_scatter_kernel, dim3((unsigned)nblocks), dim3(kDsThreads), 0, st,
                            src_idx, kin, vin, N, M, shift, hist, total, kout, vout);
     }
-    const int64_t nth = N + 1;
-    const unsigned blocks = (unsigned)((nth + 255) / 256 < 4096 ? (nth + 255) / 256 : 4096);
-    hipLaunchKernelGGL(dsort_offsets_kernel, dim3(blocks), dim3(256), 0, st, keys[(passes - 1) & 1],
-                       N, M, offsets);
+    if (N >= M) {
+        const int64_t nth = N + 1;
+        const unsigned blocks = (unsigned)((nth + 255) / 256 < 4096 ? (nth + 255) / 256 : 4096);
+        hipLaunchKernelGGL(dsort_offsets_gap_kernel, dim3(blocks), dim3(256), 0, st,
+                           keys[(passes - 1) & 1], N, M, offsets);
+    } else {
+        hipLaunchKernelGGL(dsort_offsets_kernel, dim3(oblocks), dim3(256), 0, st,
+                           keys[(passes - 1) & 1], N, M, offsets);
+    }
     return hipGetLastError();
 }
 
