@@ -65,6 +65,29 @@ def test_fullrank_exact_ties_keep_the_selection_order(bits):
         assert rep.ok(), str(rep)
 
 
+@pytest.mark.parametrize("bits,M,k", [(32, 4096, 8), (16, 4096, 16), (32, 1000, 32),
+                                      (16, 16384, 8)])
+def test_fullrank_zero_tokens_tie_every_expert(bits, M, k):
+    """All-zero tokens tie every expert at logit 0: more logits reach the short-row threshold than
+    it holds, so those rows take the list path; the result is experts 0 .. k-1 with gates 1/k."""
+    T, h, r = 300, 128, 16
+    inp = make_inputs(T, h, r, M, seed=M + k)
+    zero_rows = [0, 1, 63, 64, 299]
+    inp.x[zero_rows] = 0
+    Wb = _w_bf16(inp)
+    idx, gate, topval = _fullrank(inp, Wb, k, bits, "fullrank zero tokens")
+    parity.check_valid(idx, gate, M, topval)
+    for t in zero_rows:
+        assert np.array_equal(idx[t], np.arange(k, dtype=np.int32)), (t, idx[t])
+        assert np.allclose(gate[t], 1.0 / k, atol=1e-7)
+        assert np.all(topval[t] == 0.0)
+    if bits == 32:
+        orc = oracle.route_fullrank(inp.x, Wb, k)
+        picked = oracle.fullrank_logits_at(inp.x, Wb, np.arange(T), idx)
+        rep = parity.compare(orc, idx, gate, k, M, picked, topval)
+        assert rep.ok(), str(rep)
+
+
 @pytest.mark.parametrize("shape", [(2000, 512, 32, 4096, 8), (700, 256, 32, 1003, 16)],
                          ids=lambda s: "T%d_M%d_k%d" % (s[0], s[3], s[4]))
 def test_fullrank_bf16_logits_valid(shape):
