@@ -13,6 +13,9 @@ Functions and the passage they follow:
   histogram       per-expert selection counts (Appendix "Training", statistic f)
   route_stats     training-forward softmax statistics m, Z and psum (Appendix "Pseudocode",
                   training forward, eqs. app_softmax, app_psum, app_online)
+  route_backward  training backward: gradients of x, R1 and R2 from those of the selected
+                  logits and of psum (Appendix "Pseudocode", backward pass, eqs. app_chain,
+                  app_jac, app_kernelgrad)
   dispatch_sort   "Sort + Count": positions grouped by expert plus offsets (MoE layer
                   forward pass, efficiency appendix)
   logits_at       the logits x R1 R2 at given (token, expert) pairs ("Preliminaries"), to
@@ -61,6 +64,9 @@ def load_library(path: str):
     lib.oracle_histogram.argtypes = [P, i64, i32, i32, P]
     lib.oracle_dispatch_sort.argtypes = [P, i64, i32, i32, P, P]
     lib.oracle_route_stats.argtypes = [P, P, P, i64, i32, i32, i32, P, P, P, i32]
+    lib.oracle_route_backward.argtypes = [P, P, P, i64, i32, i32, i32, i32, P, P, P, P, P, P, P,
+                                          P, P, P, i32]
+    lib.oracle_route_backward.restype = ctypes.c_int
     lib.oracle_histogram.restype = ctypes.c_int
     lib.oracle_logits_at.argtypes = [P, P, P, i64, i32, i32, i32, P, i64, P, i32, P, i32]
     lib.oracle_logits_at.restype = ctypes.c_int
@@ -242,3 +248,43 @@ def route_stats(x, R1, R2, threads=None, lib=None):
     _check(_load(lib).oracle_route_stats(_ptr(x), _ptr(R1), _ptr(R2), T, h, r, M, _ptr(m),
                                          _ptr(Z), _ptr(psum), _threads(threads)))
     return m, Z, psum
+
+
+@dataclasses.dataclass
+class BackwardResult:
+    dx: np.ndarray   # float64 [T][h]
+    dR1: np.ndarray  # float64 [h][r]
+    dR2: np.ndarray  # float64 [r][M]
+    g: np.ndarray    # float64 [T], sum_e pbar_e P_te (0 without pbar)
+    dz: np.ndarray   # float64 [T][r]
+
+
+def route_backward(x, R1, R2, idx, dtop, pbar=None, m=None, Z=None, threads=None, lib=None):
+    """Gradients of a loss with respect to x [T][h], R1 [h][r] and R2 [r][M] (bf16 bits), given
+    its gradient dtop [T][k] with respect to the selected logits l_t[idx[t][j]] and pbar [M]
+    with respect to psum (None: no balancing term; then m and Z are not read), with the saved
+    statistics m [T], Z [T] defining P = exp(l - m) / Z.  fp64 throughout."""
+    x, R1, R2 = _u16(x), _u16(R1), _u16(R2)
+    T, h = x.shape
+    r, M = R2.shape
+    if R1.shape != (h, r):
+        raise ValueError("R1 must be [h][r]")
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    dtop = np.ascontiguousarray(dtop, dtype=np.float64)
+    if idx.ndim != 2 or idx.shape[0] != T or dtop.shape != idx.shape:
+        raise ValueError("idx and dtop must be [T][k]")
+    k = idx.shape[1]
+    if pbar is not None:
+        pbar = np.ascontiguousarray(pbar, dtype=np.float64)
+        m = np.ascontiguousarray(m, dtype=np.float64)
+        Z = np.ascontiguousarray(Z, dtype=np.float64)
+        if pbar.shape != (M,) or m.shape != (T,) or Z.shape != (T,):
+            raise ValueError("pbar must be [M], m and Z [T]")
+    res = BackwardResult(dx=np.zeros((T, h)), dR1=np.zeros((h, r)), dR2=np.zeros((r, M)),
+                         g=np.zeros(T), dz=np.zeros((T, r)))
+    opt = (lambda a: None if a is None else _ptr(a))
+    _check(_load(lib).oracle_route_backward(
+        _ptr(x), _ptr(R1), _ptr(R2), T, h, r, M, k, _ptr(idx), _ptr(dtop), opt(pbar), opt(m),
+        opt(Z), _ptr(res.dx), _ptr(res.dR1), _ptr(res.dR2), _ptr(res.g), _ptr(res.dz),
+        _threads(threads)))
+    return res

@@ -28,6 +28,9 @@
  * oracle_route_stats gives the softmax statistics of the training forward pass: the row maximum
  * m, the normaliser Z and the column sums psum of the full softmax over all experts.
  *
+ * oracle_route_backward is the training backward pass: the gradients of a loss with respect to
+ * x, R1 and R2, given its gradients with respect to the selected logits and to psum.
+ *
  * oracle_dispatch_sort is the dispatch bookkeeping that consumes a selection: the selected
  * (token, slot) positions grouped by expert, with per-expert offsets.
  *
@@ -482,4 +485,203 @@ int oracle_histogram(const int32_t* idx, int64_t n, int32_t k, int32_t M, int64_
         counts[idx[i]] += 1;
     }
     return ORACLE_OK;
+}
+
+/*
+ * Training backward pass of the low-rank router (Appendix "Pseudocode", backward pass: eqs.
+ * app_chain, app_jac and app_kernelgrad and the backward algorithm with recompute), in this
+ * file's orientation x [T][h], R1 [h][r], R2 [r][M] (the paper's appendix names the expert
+ * factor R1 [M][r], which is R2^T here, and the hidden factor R2 [r][h], which is R1^T here).
+ * Inputs: the selection idx [T][k]; dtop [T][k], the gradient of the loss with respect to the
+ * selected logits l_t[idx[t][j]]; pbar [M], the gradient with respect to psum (NULL: no
+ * balancing term); m [T] and Z [T], the saved softmax statistics (read only when pbar is given).
+ * Per token t:
+ *   z_t      = x_t R1
+ *   l_t[e]   = z_t R2[:, e]
+ *   P_te     = exp(l_t[e] - m_t) / Z_t
+ *   g_t      = sum_e pbar_e P_te                                  (eq. app_kernelgrad)
+ *   ybar_te  = P_te (pbar_e - g_t), then dtop[t][j] added at e = idx[t][j] for j = 0 .. k-1
+ *   dz_t[i]  = sum_e ybar_te R2[i][e]
+ *   dx_t[c]  = sum_i dz_t[i] R1[c][i]
+ * and over all tokens
+ *   dR1[c][i] = sum_t x[t][c] dz_t[i]
+ *   dR2[i][e] = sum_t z_t[i] ybar_te
+ * Entries of idx outside [0, M) add nothing.  Every sum runs in increasing order of its index
+ * (t, e, i or j), so the result does not depend on the thread count.  g [T] and dz [T][r] are
+ * outputs too (g is 0 without pbar).
+ */
+int oracle_route_backward(const uint16_t* x, const uint16_t* R1, const uint16_t* R2, int64_t T,
+                          int32_t h, int32_t r, int32_t M, int32_t k, const int32_t* idx,
+                          const double* dtop, const double* pbar, const double* m,
+                          const double* Z, double* dx, double* dR1, double* dR2, double* g,
+                          double* dz, int32_t nthreads) {
+    if (!x || !R1 || !R2 || !dR1 || !dR2) return ORACLE_ERR_ARG;
+    if (T < 0 || h <= 0 || r <= 0 || M <= 0 || k < 1) return ORACLE_ERR_ARG;
+    if (T > 0 && (!idx || !dtop || !dx || !g || !dz || (pbar && (!m || !Z)))) return ORACLE_ERR_ARG;
+    for (int64_t i = 0; i < T * (int64_t)k; ++i)
+        if (!isfinite(dtop[i])) return ORACLE_ERR_NONFINITE;
+    if (pbar) {
+        for (int32_t e = 0; e < M; ++e)
+            if (!isfinite(pbar[e])) return ORACLE_ERR_NONFINITE;
+        for (int64_t t = 0; t < T; ++t) {
+            if (!isfinite(m[t]) || !isfinite(Z[t])) return ORACLE_ERR_NONFINITE;
+            if (!(Z[t] > 0.0)) return ORACLE_ERR_ARG;
+        }
+    }
+    double* f1 = (double*)malloc(sizeof(double) * (size_t)h * (size_t)r);
+    double* f2 = (double*)malloc(sizeof(double) * (size_t)r * (size_t)M);
+    double* zall = (double*)malloc(sizeof(double) * (size_t)(T > 0 ? T : 1) * (size_t)r);
+    if (!f1 || !f2 || !zall) {
+        free(f1);
+        free(f2);
+        free(zall);
+        return ORACLE_ERR_NOMEM;
+    }
+    int status = (decode_all(R1, (int64_t)h * r, f1) & decode_all(R2, (int64_t)r * M, f2))
+                     ? ORACLE_OK
+                     : ORACLE_ERR_NONFINITE;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#endif
+    /* Per token: z, the logits, P, g, ybar, dz and dx. */
+    if (status == ORACLE_OK) {
+#pragma omp parallel
+        {
+            double* xs = (double*)malloc(sizeof(double) * (size_t)h);
+            double* lg = (double*)malloc(sizeof(double) * (size_t)M);
+            double* yb = (double*)malloc(sizeof(double) * (size_t)M);
+            int local_ok = xs && lg && yb;
+#pragma omp for schedule(dynamic, 4)
+            for (int64_t t = 0; t < T; ++t) {
+                if (!local_ok) continue;
+                if (!decode_all(x + t * (int64_t)h, h, xs)) {
+#pragma omp atomic write
+                    status = ORACLE_ERR_NONFINITE;
+                    continue;
+                }
+                double* zt = zall + t * (int64_t)r;
+                for (int32_t i = 0; i < r; ++i) zt[i] = 0.0;
+                for (int32_t c = 0; c < h; ++c)
+                    for (int32_t i = 0; i < r; ++i) zt[i] += xs[c] * f1[(int64_t)c * r + i];
+                double gt = 0.0;
+                if (pbar) {
+                    for (int32_t e = 0; e < M; ++e) lg[e] = 0.0;
+                    for (int32_t i = 0; i < r; ++i)
+                        for (int32_t e = 0; e < M; ++e) lg[e] += zt[i] * f2[(int64_t)i * M + e];
+                    for (int32_t e = 0; e < M; ++e) lg[e] = exp(lg[e] - m[t]) / Z[t];  /* P */
+                    for (int32_t e = 0; e < M; ++e) gt += pbar[e] * lg[e];
+                    for (int32_t e = 0; e < M; ++e) yb[e] = lg[e] * (pbar[e] - gt);
+                } else {
+                    for (int32_t e = 0; e < M; ++e) yb[e] = 0.0;
+                }
+                for (int32_t j = 0; j < k; ++j) {
+                    const int32_t e = idx[t * k + j];
+                    if (e >= 0 && e < M) yb[e] += dtop[t * k + j];
+                }
+                g[t] = gt;
+                double* dzt = dz + t * (int64_t)r;
+                for (int32_t i = 0; i < r; ++i) {
+                    double s = 0.0;
+                    for (int32_t e = 0; e < M; ++e) s += yb[e] * f2[(int64_t)i * M + e];
+                    dzt[i] = s;
+                }
+                double* dxt = dx + t * (int64_t)h;
+                for (int32_t c = 0; c < h; ++c) {
+                    double s = 0.0;
+                    for (int32_t i = 0; i < r; ++i) s += dzt[i] * f1[(int64_t)c * r + i];
+                    dxt[c] = s;
+                }
+            }
+            if (!local_ok) {
+#pragma omp atomic write
+                status = ORACLE_ERR_NOMEM;
+            }
+            free(xs);
+            free(lg);
+            free(yb);
+        }
+    }
+    /* dR2 = z^T ybar: blocks of 64 experts, every token in order, ybar recomputed as above. */
+    const int32_t EB = 64;
+    if (status == ORACLE_OK) {
+        const int32_t nblk = (M + EB - 1) / EB;
+#pragma omp parallel
+        {
+            double* acc = (double*)malloc(sizeof(double) * (size_t)EB * (size_t)r);
+            double* yb = (double*)malloc(sizeof(double) * (size_t)EB);
+            int local_ok = acc && yb;
+#pragma omp for schedule(dynamic, 1)
+            for (int32_t b = 0; b < nblk; ++b) {
+                if (!local_ok) continue;
+                const int32_t e0 = b * EB, e1 = (e0 + EB < M) ? e0 + EB : M;
+                for (int64_t q = 0; q < (int64_t)EB * r; ++q) acc[q] = 0.0;
+                for (int64_t t = 0; t < T; ++t) {
+                    const double* zt = zall + t * (int64_t)r;
+                    for (int32_t e = e0; e < e1; ++e) {
+                        double y = 0.0;
+                        if (pbar) {
+                            double l = 0.0;
+                            for (int32_t i = 0; i < r; ++i) l += zt[i] * f2[(int64_t)i * M + e];
+                            const double p = exp(l - m[t]) / Z[t];
+                            y = p * (pbar[e] - g[t]);
+                        }
+                        yb[e - e0] = y;
+                    }
+                    for (int32_t j = 0; j < k; ++j) {
+                        const int32_t e = idx[t * k + j];
+                        if (e >= e0 && e < e1) yb[e - e0] += dtop[t * k + j];
+                    }
+                    for (int32_t e = e0; e < e1; ++e)
+                        for (int32_t i = 0; i < r; ++i)
+                            acc[(int64_t)(e - e0) * r + i] += zt[i] * yb[e - e0];
+                }
+                for (int32_t e = e0; e < e1; ++e)
+                    for (int32_t i = 0; i < r; ++i)
+                        dR2[(int64_t)i * M + e] = acc[(int64_t)(e - e0) * r + i];
+            }
+            if (!local_ok) {
+#pragma omp atomic write
+                status = ORACLE_ERR_NOMEM;
+            }
+            free(acc);
+            free(yb);
+        }
+    }
+    /* dR1 = x^T dz: blocks of 64 hidden columns, every token in order. */
+    const int32_t CB = 64;
+    if (status == ORACLE_OK) {
+        const int32_t nblk = (h + CB - 1) / CB;
+#pragma omp parallel
+        {
+            double* acc = (double*)malloc(sizeof(double) * (size_t)CB * (size_t)r);
+            double* xs = (double*)malloc(sizeof(double) * (size_t)CB);
+            int local_ok = acc && xs;
+#pragma omp for schedule(dynamic, 1)
+            for (int32_t b = 0; b < nblk; ++b) {
+                if (!local_ok) continue;
+                const int32_t c0 = b * CB, c1 = (c0 + CB < h) ? c0 + CB : h;
+                for (int64_t q = 0; q < (int64_t)CB * r; ++q) acc[q] = 0.0;
+                for (int64_t t = 0; t < T; ++t) {
+                    decode_all(x + t * (int64_t)h + c0, c1 - c0, xs);
+                    const double* dzt = dz + t * (int64_t)r;
+                    for (int32_t c = c0; c < c1; ++c)
+                        for (int32_t i = 0; i < r; ++i)
+                            acc[(int64_t)(c - c0) * r + i] += xs[c - c0] * dzt[i];
+                }
+                for (int32_t c = c0; c < c1; ++c)
+                    for (int32_t i = 0; i < r; ++i)
+                        dR1[(int64_t)c * r + i] = acc[(int64_t)(c - c0) * r + i];
+            }
+            if (!local_ok) {
+#pragma omp atomic write
+                status = ORACLE_ERR_NOMEM;
+            }
+            free(acc);
+            free(xs);
+        }
+    }
+    free(f1);
+    free(f2);
+    free(zall);
+    return status;
 }

@@ -15,6 +15,11 @@ library) so the same checks can be run against deliberately broken builds of the
 * histogram        -- counts equal numpy's bincount and sum to n k;
 * softmax stats    -- m, Z, psum against scipy's logsumexp and softmax over BLAS logits, with the
                       zero-token, one-expert and large-logit special cases;
+* backward         -- central finite differences of the loss sum_tj dtop_tj l_t[idx_tj] +
+                      sum_e pbar_e sum_t softmax(l_t)_e (numpy fp64 forward); a constant pbar
+                      cancels (g_t = pbar); the trace identity <dx, x> = <dR1, R1> = <dR2, R2> =
+                      <dz, z>; relabelling experts; a one-hot pbar gives g = softmax column;
+                      ids outside [0, M) add nothing; M = 1 and T = 0;
 * logits at pairs  -- numpy BLAS logits at random (token, expert) pairs, including the
                       first and last expert and repeated tokens (low-rank and full-rank).
 """
@@ -272,6 +277,119 @@ def check_route_stats(lib=None):
             assert np.allclose(m, top[:, 0], rtol=1e-12, atol=1e-12)
 
 
+# ------------------------------------------------------------------ backward
+def _bwd_loss(xf, R1f, R2f, idx, dtop, pbar):
+    """The loss whose gradient the backward pass returns, evaluated directly: the selected
+    logits weighted by dtop (ids outside [0, M) left out) plus pbar . psum."""
+    from scipy.special import softmax
+    lg = xf @ R1f @ R2f
+    M = lg.shape[1]
+    ok = (idx >= 0) & (idx < M)
+    rows = np.nonzero(ok)[0]
+    L = float(np.sum(dtop[ok] * lg[rows, idx[ok]]))
+    if pbar is not None:
+        L += float(pbar @ softmax(lg, axis=1).sum(axis=0))
+    return L
+
+
+def _bwd_stats(inp):
+    lg = (f64(inp.x) @ f64(inp.R1)) @ f64(inp.R2)
+    m = lg.max(axis=1)
+    return lg, m, np.exp(lg - m[:, None]).sum(axis=1)
+
+
+def _fd_grad(fun, a, eps=1e-5):
+    g = np.zeros_like(a)
+    it = np.nditer(a, flags=["multi_index"])
+    for _ in it:
+        i = it.multi_index
+        d = eps * max(1.0, abs(a[i]))
+        ap, am = a.copy(), a.copy()
+        ap[i] += d
+        am[i] -= d
+        g[i] = (fun(ap) - fun(am)) / (2 * d)
+    return g
+
+
+def check_route_backward(lib=None):
+    """Gradients of x, R1 and R2 against central finite differences of the loss itself, plus
+    the closed forms and invariants of the definition."""
+    rng = np.random.default_rng(77)
+    # finite differences on tiny cases, with and without the balancing term
+    for si, (T, h, r, M, k, use_p) in enumerate([(5, 6, 3, 7, 2, True), (4, 5, 2, 9, 3, False),
+                                                 (3, 4, 3, 1, 1, True)]):
+        inp = make_inputs(T, h, r, M, seed=500 + si)
+        idx = np.stack([rng.permutation(M)[:k] for _ in range(T)]).astype(np.int32)
+        if k >= 2:
+            idx[0, 1] = M        # outside [0, M): adds nothing
+            idx[1 % T, 0] = -1
+        dtop = rng.standard_normal((T, k))
+        pbar = (rng.random(M) * 2 - 0.5) if use_p else None
+        lg, m, Z = _bwd_stats(inp)
+        res = oracle.route_backward(inp.x, inp.R1, inp.R2, idx, dtop, pbar, m, Z, lib=lib)
+        xf, R1f, R2f = f64(inp.x), f64(inp.R1), f64(inp.R2)
+        want_x = _fd_grad(lambda a: _bwd_loss(a, R1f, R2f, idx, dtop, pbar), xf)
+        want_1 = _fd_grad(lambda a: _bwd_loss(xf, a, R2f, idx, dtop, pbar), R1f)
+        want_2 = _fd_grad(lambda a: _bwd_loss(xf, R1f, a, idx, dtop, pbar), R2f)
+        for name, got, want in (("dx", res.dx, want_x), ("dR1", res.dR1, want_1),
+                                ("dR2", res.dR2, want_2)):
+            err = np.abs(got - want).max()
+            assert err <= 1e-6 * (1 + np.abs(want).max()), "%s vs finite differences (%d): %g" % (
+                name, si, err)
+        if use_p and M > 1:
+            from scipy.special import softmax
+            assert np.allclose(res.g, softmax(lg, axis=1) @ pbar, rtol=1e-12, atol=1e-12)
+    # a constant pbar cancels: g_t = c and the dense term vanishes
+    T, h, r, M, k = 40, 32, 16, 50, 4
+    inp = make_inputs(T, h, r, M, seed=520)
+    idx = np.stack([rng.permutation(M)[:k] for _ in range(T)]).astype(np.int32)
+    dtop = rng.standard_normal((T, k))
+    lg, m, Z = _bwd_stats(inp)
+    c = 0.37
+    a = oracle.route_backward(inp.x, inp.R1, inp.R2, idx, dtop, np.full(M, c), m, Z, lib=lib)
+    b = oracle.route_backward(inp.x, inp.R1, inp.R2, idx, dtop, None, lib=lib)
+    assert np.allclose(a.g, c, rtol=1e-12)
+    for name in ("dx", "dR1", "dR2", "dz"):
+        ga, gb = getattr(a, name), getattr(b, name)
+        assert np.allclose(ga, gb, rtol=1e-9, atol=1e-9 * np.abs(gb).max()), "constant pbar: " + name
+    # a one-hot pbar: g_t is the softmax column of that expert
+    from scipy.special import softmax
+    onehot = np.zeros(M)
+    onehot[17] = 2.5
+    o = oracle.route_backward(inp.x, inp.R1, inp.R2, idx, dtop, onehot, m, Z, lib=lib)
+    assert np.allclose(o.g, 2.5 * softmax(lg, axis=1)[:, 17], rtol=1e-12, atol=1e-15)
+    # trace identity: every factor enters the logits linearly, so all four pairings agree
+    T, h, r, M, k = 64, 96, 16, 300, 8
+    inp = make_inputs(T, h, r, M, seed=521)
+    idx = np.stack([rng.permutation(M)[:k] for _ in range(T)]).astype(np.int32)
+    dtop = rng.standard_normal((T, k))
+    pbar = rng.random(M) * M / T
+    lg, m, Z = _bwd_stats(inp)
+    res = oracle.route_backward(inp.x, inp.R1, inp.R2, idx, dtop, pbar, m, Z, lib=lib)
+    xf, R1f, R2f = f64(inp.x), f64(inp.R1), f64(inp.R2)
+    ref = np.sum(res.dz * (xf @ R1f))
+    for name, v in (("x", np.sum(res.dx * xf)), ("R1", np.sum(res.dR1 * R1f)),
+                    ("R2", np.sum(res.dR2 * R2f))):
+        assert abs(v - ref) <= 1e-9 * (1 + abs(ref)), "trace identity " + name
+    assert np.allclose(res.dx, res.dz @ R1f.T, rtol=1e-12, atol=1e-12)
+    assert np.allclose(res.dR1, xf.T @ res.dz, rtol=1e-10, atol=1e-10)
+    # relabelling the experts relabels dR2 and leaves the rest unchanged
+    perm = rng.permutation(M)
+    inv = np.argsort(perm)
+    inp2 = make_inputs(T, h, r, M, seed=521)
+    inp2.R2 = np.ascontiguousarray(inp.R2[:, perm])
+    res2 = oracle.route_backward(inp2.x, inp2.R1, inp2.R2, inv[idx].astype(np.int32), dtop,
+                                 pbar[perm], m, Z, lib=lib)
+    assert np.allclose(res2.dR2, res.dR2[:, perm], rtol=1e-10, atol=1e-12)
+    for name in ("dx", "dR1", "g", "dz"):
+        assert np.allclose(getattr(res2, name), getattr(res, name), rtol=1e-10, atol=1e-12), name
+    # no tokens: zero weight gradients
+    inp0 = make_inputs(0, 32, 16, 9, seed=522)
+    z0 = oracle.route_backward(inp0.x, inp0.R1, inp0.R2, np.zeros((0, 2), np.int32),
+                               np.zeros((0, 2)), np.ones(9), np.zeros(0), np.zeros(0), lib=lib)
+    assert not z0.dR1.any() and not z0.dR2.any()
+
+
 # ------------------------------------------------------------------ logits at pairs
 def check_logits_at(lib=None, shapes=((50, 96, 16, 300), (7, 32, 48, 5), (33, 64, 64, 1000))):
     for si, (T, h, r, M) in enumerate(shapes):
@@ -301,7 +419,7 @@ def check_fullrank_logits_at(lib=None):
     assert np.allclose(got, want, rtol=1e-12, atol=1e-12), "full-rank logits at pairs differ"
 
 
-ALL_CHECKS = [check_route_stats, check_dispatch_sort, check_bruteforce, check_fullrank_bruteforce, check_identity,
+ALL_CHECKS = [check_route_backward, check_route_stats, check_dispatch_sort, check_bruteforce, check_fullrank_bruteforce, check_identity,
               check_gates,
               check_equivariance, check_thm1, check_prop1_top1, check_prop1_counts,
               check_histogram, check_logits_at, check_fullrank_logits_at]

@@ -15,6 +15,33 @@ import oracle_pins
 SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
 
 MUTANTS = {
+    "bwd_g_not_subtracted": (
+        "for (int32_t e = 0; e < M; ++e) yb[e] = lg[e] * (pbar[e] - gt);",
+        "for (int32_t e = 0; e < M; ++e) yb[e] = lg[e] * pbar[e];"),
+    "bwd_P_not_normalised": (
+        "lg[e] = exp(lg[e] - m[t]) / Z[t];  /* P */",
+        "lg[e] = exp(lg[e] - m[t]);  /* P */"),
+    "bwd_dz_reads_R2_transposed": (
+        "for (int32_t e = 0; e < M; ++e) s += yb[e] * f2[(int64_t)i * M + e];",
+        "for (int32_t e = 0; e < M; ++e) s += yb[e] * f2[((int64_t)e * r + i) % ((int64_t)r * M)];"),
+    "bwd_dx_drops_last_rank_term": (
+        "for (int32_t i = 0; i < r; ++i) s += dzt[i] * f1[(int64_t)c * r + i];",
+        "for (int32_t i = 0; i < r - 1; ++i) s += dzt[i] * f1[(int64_t)c * r + i];"),
+    "bwd_sparse_term_subtracted": (
+        "if (e >= 0 && e < M) yb[e] += dtop[t * k + j];",
+        "if (e >= 0 && e < M) yb[e] -= dtop[t * k + j];"),
+    "bwd_invalid_id_counted": (
+        "if (e >= 0 && e < M) yb[e] += dtop[t * k + j];",
+        "if (e >= -1 && e < M) yb[e < 0 ? 0 : e] += dtop[t * k + j];"),
+    "bwd_dR2_sparse_at_next_expert": (
+        "if (e >= e0 && e < e1) yb[e - e0] += dtop[t * k + j];",
+        "if (e + 1 >= e0 && e + 1 < e1) yb[e + 1 - e0] += dtop[t * k + j];"),
+    "bwd_dR2_drops_last_token": (
+        "for (int64_t t = 0; t < T; ++t) {\n                    const double* zt = zall",
+        "for (int64_t t = 0; t < T - 1; ++t) {\n                    const double* zt = zall"),
+    "bwd_dR1_uses_z": (
+        "acc[(int64_t)(c - c0) * r + i] += xs[c - c0] * dzt[i];",
+        "acc[(int64_t)(c - c0) * r + i] += xs[c - c0] * zall[t * r + i];"),
     "stats_no_max_shift_in_Z": (
         "zs += exp(lg[e] - mx);",
         "zs += exp(lg[e]);"),
