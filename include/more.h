@@ -162,6 +162,48 @@ more_status more_route_lowrank_train_workspace_size(int64_t T, int32_t h, int32_
                                                     int32_t k, size_t* bytes);
 
 /*
+ * Training backward pass of the low-rank router with recompute (Appendix "Pseudocode",
+ * backward pass: eqs. app_chain, app_jac, app_kernelgrad and the backward algorithm).  Given
+ * the selection of the forward pass, the gradient of the loss with respect to the selected
+ * logits and (optionally) with respect to psum, it returns the gradients with respect to x,
+ * R1 and R2.  With l = x R1 R2 recomputed tile by tile (never written) and
+ * P_te = exp(l_te - m[t]) / Z[t]:
+ *   g_t      = sum_e pbar[e] P_te
+ *   ybar_te  = P_te (pbar[e] - g_t) + sum_{j : idx[t][j] == e} dtop[t][j]
+ *   dx       = ybar R2^T R1^T     dR1t = (x^T ybar R2^T)^T     dR2t = (R1^T x^T ybar)^T
+ * i.e. dz = ybar R2^T [T][r], dx = dz R1^T, dR1t[i][c] = sum_t dz[t][i] x[t][c],
+ * dR2t[e][i] = sum_t ybar_te z[t][i].
+ *   x, R1t, R2t, T, h, r, M   as in more_route_lowrank (device, bf16)
+ *   k         selections per token, 1 <= k <= min(M, MORE_K_MAX)
+ *   idx       int32 [T][k]  the selection (device); entries outside [0, M) add nothing
+ *   dtop      fp32 [T][k]   gradient with respect to the selected logits l_t[idx[t][j]] (device)
+ *   pbar      fp32 [M]      gradient with respect to psum (device), or NULL: no balancing term
+ *                           (then m and Z are not read and may be NULL)
+ *   m, Z      fp32 [T]      the statistics saved by more_route_lowrank_train (device)
+ *   dx        fp32 [T][h]   out (device), overwritten
+ *   dR1t      fp32 [r][h]   out (device), overwritten; zero when T == 0
+ *   dR2t      fp32 [M][r]   out (device), overwritten; zero when T == 0
+ *   workspace / workspace_bytes   at least more_route_lowrank_backward_workspace_size() bytes
+ *             with balance = (pbar != NULL), 256-byte aligned (device; NULL allowed when T == 0)
+ * Numerics: the recomputed logits are those of the training forward pass's statistics (z as a
+ * bf16 hi/lo pair); P (pbar - g) is rounded to bf16 for the two contractions over experts and
+ * tokens, which read bf16(z) and R2 with fp32 accumulation; the dtop terms use fp32 z; dx and
+ * dR1t read dz as a bf16 hi/lo pair.  Every sum runs in a fixed order, so a shape gives the
+ * same bits on every run.  Errors: MORE_ERR_INVALID_ARG (NULL or misaligned pointers, negative
+ * sizes), MORE_ERR_UNSUPPORTED (r outside {16, 32, 64}, h not a multiple of 16, k > MORE_K_MAX),
+ * MORE_ERR_WORKSPACE; nothing is enqueued on an error.
+ */
+more_status more_route_lowrank_backward(const uint16_t* x, const uint16_t* R1t,
+                                        const uint16_t* R2t, int64_t T, int32_t h, int32_t r,
+                                        int32_t M, int32_t k, const int32_t* idx,
+                                        const float* dtop, const float* pbar, const float* m,
+                                        const float* Z, float* dx, float* dR1t, float* dR2t,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+more_status more_route_lowrank_backward_workspace_size(int64_t T, int32_t h, int32_t r,
+                                                       int32_t M, int32_t k, int32_t balance,
+                                                       size_t* bytes);
+
+/*
  * Full-rank (standard) router, the baseline (Section "Preliminaries": softmax(TopK(R x)) with
  * R in R^{M x h}).  The logits x W^T are formed with a hipBLASLt GEMM into the workspace
  * (fp32 when logit_bits == 32, bf16 when logit_bits == 16) and a row top-k kernel then

@@ -32,6 +32,10 @@ SIGNATURES = {
     "more_route_lowrank_train": (_I32, [_P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P,
                                         _P, _P, _P, _P, _P, _SZ, _P]),
     "more_route_lowrank_train_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _I32, _PSZ]),
+    "more_route_lowrank_backward": (_I32, [_P, _P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P,
+                                           _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "more_route_lowrank_backward_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _I32, _I32,
+                                                          _PSZ]),
     "more_route_fullrank": (_I32, [_P, _P, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P, _SZ,
                                    _P]),
     "more_route_fullrank_workspace_size": (_I32, [_I64, _I32, _I32, _I32, _I32, _PSZ]),

@@ -1,0 +1,921 @@
+// Training backward pass of the low-rank router for gfx950 (Appendix "Pseudocode", backward
+// pass: eqs. app_chain, app_jac, app_kernelgrad and the backward algorithm with recompute).
+// With l = z R2, z = x R1, P_te = exp(l_te - m_t) / Z_t from the saved statistics, the gradient
+// dtop of the loss with respect to the selected logits and pbar with respect to psum:
+//   g_t     = sum_e pbar_e P_te                       (one scalar per token)
+//   ybar_te = P_te (pbar_e - g_t) + dtop at the selected experts
+//   dz      = ybar R2^T,  dR2 = z^T ybar,  dx = dz R1^T,  dR1 = x^T dz
+// and no T x M matrix is written: the logits are recomputed tile by tile on the matrix cores.
+//
+// Kernels of one call (the balancing kernels run only when pbar is given):
+//   zonly           z = x R1 (fp32, the z pass of the routing call)
+//   bwd_prep        z' = z log2(e) as bf16 hi/lo rows, bf16(z) rows, the token bias
+//                   -(m log2(e) + log2 Z), and R1 transposed to [h][r]
+//   bwd_tok<false>  sweep 1, token-major: per (expert split, token) sum_e pbar_e P_te
+//   bwd_sum         g = the split sums in split order
+//   bwd_tok<true>   sweep 2, token-major: ybar tile by tile, dz partials per expert split
+//   bwd_dz          dz = partials in order + the selected experts' dtop R2 rows; dz as bf16
+//                   hi/lo rows [T][2r] and as transposed hi/lo rows [2][r][T]
+//   bwd_exp         sweep 2 again, expert-major: ybar tile by tile, dR2 partials per token split
+//   dispatch        the selections sorted by expert (Sort + Count kernels)
+//   bwd_dr2         dR2 = partials in order + dtop z of each expert's selections in order
+//   bwd_dx          dx = dz R1^T (dz as hi + lo)
+//   bwd_dr1 + sum   dR1 = x^T dz over token splits, summed in split order
+// The paper's algorithm computes dz and dR2 in one sweep per token block and lets token blocks
+// add into dR2; here two sweeps (one token-major, one expert-major) each own their output, so
+// nothing is added atomically and every sum runs in a fixed order: a shape gives the same bits
+// on every run.
+//
+// Numerics.  The logits are recomputed as in the training forward pass (z' as bf16 hi + lo on
+// the matrix cores, the bias entering through the accumulator input, 2^x by v_exp_f32).  The
+// dense logit gradient P (pbar - g) is rounded to bf16 for the two contractions, which also
+// read bf16(z) (dR2) and the bf16 rows of R2 (dz), with fp32 accumulation; the sparse dtop
+// terms use fp32 z and fp32 dtop; dx and dR1 read dz as bf16 hi + lo (about 16 significant
+// bits) and the exact bf16 x and R1.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "device_common.h"
+#include "lowrank.h"
+
+namespace more {
+
+namespace {
+
+constexpr float kBwLog2e = 1.44269504088896340736f;
+constexpr float kBwNoToken = -0x1p100f;  // bias of rows past T: 2^(finite + this) = 0
+
+constexpr int kBwWaves = 8;
+constexpr int kBwThreads = 64 * kBwWaves;
+// 32-token groups per wave in the token-major sweeps (one for the r = 64 dz sweep, whose
+// accumulators would not fit two waves per SIMD otherwise)
+template <int RC, bool DZ>
+constexpr int bw_tpw() { return (RC == 4 && DZ) ? 1 : 2; }
+constexpr int kBwStageE = 128;   // experts per LDS stage of the token-major sweeps
+constexpr int kBwNE = 2;         // 32-expert tiles per wave in the expert-major sweep
+constexpr int kBwStageT = 128;   // tokens per LDS stage of the expert-major sweep
+
+__device__ __forceinline__ float bw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// eight fp32 -> bf16x8 (round to nearest even)
+__device__ __forceinline__ bf16x8 pack_bf16x8(const float* v) {
+    bf16x8 o;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] = (__bf16)v[i];
+    return o;
+}
+
+// Two 8-byte LDS pieces (four bf16 each) as one operand.
+__device__ __forceinline__ bf16x8 lds_two_quads(const uint16_t* p0, const uint16_t* p1) {
+    const uint2 a = *reinterpret_cast<const uint2*>(p0);
+    const uint2 b = *reinterpret_cast<const uint2*>(p1);
+    return __builtin_bit_cast(bf16x8, u32x4{a.x, a.y, b.x, b.y});
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------------ prep
+// One thread per element of z [T][r]: zhl [T][2r] = bf16(z'), bf16(z' - bf16(z')) with
+// z' = z log2(e); zb [T][r] = bf16(z); bias[t] = -(m log2(e) + log2 Z) (when m is given).
+__global__ __launch_bounds__(256) void bwd_prep_kernel(const float* __restrict__ z,
+                                                       const float* __restrict__ m,
+                                                       const float* __restrict__ Z, int32_t T,
+                                                       int32_t r, uint16_t* __restrict__ zhl,
+                                                       uint16_t* __restrict__ zb,
+                                                       float* __restrict__ bias) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)T * r) return;
+    const int64_t t = i / r;
+    const int32_t j = (int32_t)(i - t * r);
+    const float zv = z[i];
+    const float v = zv * kBwLog2e;
+    const __bf16 hb = (__bf16)v;
+    const __bf16 lb = (__bf16)(v - (float)hb);
+    zhl[t * 2 * r + j] = __builtin_bit_cast(uint16_t, hb);
+    zhl[t * 2 * r + r + j] = __builtin_bit_cast(uint16_t, lb);
+    zb[i] = __builtin_bit_cast(uint16_t, (__bf16)zv);
+    if (m && j == 0) bias[t] = -(m[t] * kBwLog2e + log2f(Z[t]));
+}
+
+// R1 [h][r] from R1t [r][h].
+__global__ __launch_bounds__(256) void bwd_r1_transpose_kernel(const uint16_t* __restrict__ R1t,
+                                                               int32_t h, int32_t r,
+                                                               uint16_t* __restrict__ R1) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;  // index into R1
+    if (i >= (int64_t)h * r) return;
+    const int64_t c = i / r;
+    const int32_t j = (int32_t)(i - c * r);
+    R1[i] = R1t[(int64_t)j * h + c];
+}
+
+// ------------------------------------------------------------------------------ token-major
+// Workgroup (token block, expert split); the block's tokens are WT slots of TPW x 32 tokens, and
+// the waves of a slot (WE = 8 / WT of them) take the expert tiles of each stage in turn.  A
+// wave holds z'_hi and z'_lo of its tokens as B operands (token columns) and reads the expert
+// rows of R2t from LDS as A operands, so a lane owns one token column and sixteen expert rows
+// of each 32 x 32 logit tile; the token's bias enters through the accumulator input.
+//   DZ = false: per lane sum_e pbar_e 2^(l' + bias) -> gpart[(split WE + we)][t]
+//   DZ = true : ybar = P (pbar_e - g_t) as bf16 A operands (token rows, expert K order as the
+//               accumulator holds them) against R2^T pieces read from a transposed LDS copy
+//               with the same K order -> dz partials dzpart[(split WE + we)][t][r]
+template <int RC>
+struct TokCfg {
+    static constexpr int R = 16 * RC;
+    static constexpr int RB = (R + 31) / 32;       // 32-row blocks of the rank axis
+    static constexpr int RP = R + 8;               // LDS pitch of an expert row (bf16)
+    static constexpr int CP = kBwStageE + 8;       // LDS pitch of a transposed row (bf16)
+    static constexpr int PIECES = kBwStageE * R / 8;  // 16-byte pieces of R2t per stage
+    static constexpr int PPT = (PIECES + kBwThreads - 1) / kBwThreads;
+};
+
+template <int RC, bool DZ>
+__global__ __launch_bounds__(kBwThreads, 1) void bwd_tok_kernel(
+    const uint16_t* __restrict__ zhl, const float* __restrict__ bias,
+    const float* __restrict__ gtok, const float* __restrict__ pbar,
+    const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t WT, int32_t splits,
+    float* __restrict__ out) {
+    using C = TokCfg<RC>;
+    constexpr int R = C::R, RB = C::RB, RP = C::RP, CP = C::CP, TPW = bw_tpw<RC, DZ>();
+    constexpr int TILES = kBwStageE / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t rows[2][kBwStageE * RP];
+    __shared__ __attribute__((aligned(16))) uint16_t rowsT[DZ ? 2 : 1][DZ ? R * CP : 8];
+    __shared__ __attribute__((aligned(16))) float pbs[2][kBwStageE];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 31, half = lane >> 5;
+    const int WE = kBwWaves / WT;
+    const int wt = w % WT, we = w / WT;
+    const int32_t split = (int32_t)(blockIdx.x % (unsigned)splits);
+    const int64_t tb = blockIdx.x / (unsigned)splits;
+    const int32_t Mt = (M + 31) / 32;
+    const int32_t tile0 = (int32_t)((int64_t)Mt * split / splits);
+    const int32_t tile1 = (int32_t)((int64_t)Mt * (split + 1) / splits);
+    const int nstages = (tile1 - tile0 + TILES - 1) / TILES;
+    const int64_t first = (tb * WT + wt) * (32 * TPW);  // first token of this wave
+
+    // the wave's tokens as B operands, its bias and g
+    bf16x8 zh[TPW][RC], zl[TPW][RC];
+    float bt[TPW], gt[TPW];
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) {
+        const int64_t t = first + 32 * g + n;
+        const bool ok = t < T;
+        const uint16_t* zr = zhl + (ok ? t : 0) * (2 * R) + 8 * half;
+#pragma unroll
+        for (int c = 0; c < RC; ++c) {
+            const bf16x8 hv = load_bf16x8(zr + 16 * c);
+            const bf16x8 lv = load_bf16x8(zr + R + 16 * c);
+            zh[g][c] = ok ? hv : zero_bf16x8();
+            zl[g][c] = ok ? lv : zero_bf16x8();
+        }
+        bt[g] = ok ? bias[t] : kBwNoToken;
+        gt[g] = (DZ && ok) ? gtok[t] : 0.0f;
+    }
+
+    // stage loads: piece p = expert p / (R / 8) of the stage, rank piece p % (R / 8)
+    u32x4 rg[C::PPT];
+    float rp = 0.0f;
+    auto gload = [&](int st) __attribute__((always_inline)) {
+        const int64_t e0 = (int64_t)(tile0 + st * TILES) * 32;
+#pragma unroll
+        for (int i = 0; i < C::PPT; ++i) {
+            const int p = tid + i * kBwThreads;
+            int64_t e = e0 + p / (R / 8);
+            e = e < M ? e : M - 1;  // rows past M: masked out of the sums below
+            if (p < C::PIECES)
+                rg[i] = *reinterpret_cast<const u32x4*>(R2t + e * R + 8 * (p % (R / 8)));
+        }
+        if (tid < kBwStageE) {
+            const int64_t e = e0 + tid;
+            rp = e < M ? pbar[e] : 0.0f;
+        }
+    };
+    auto stash = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < C::PPT; ++i) {
+            const int p = tid + i * kBwThreads;
+            if (p < C::PIECES) {
+                const int el = p / (R / 8), q = p % (R / 8);
+                *reinterpret_cast<u32x4*>(&rows[buf][el * RP + 8 * q]) = rg[i];
+                if constexpr (DZ) {
+                    const uint16_t* v = reinterpret_cast<const uint16_t*>(&rg[i]);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) rowsT[buf][(8 * q + u) * CP + el] = v[u];
+                }
+            }
+        }
+        if (tid < kBwStageE) pbs[buf][tid] = rp;
+    };
+
+    float gs[TPW];
+    f32x16 dz[TPW][RB];
+#pragma unroll
+    for (int g = 0; g < TPW; ++g) {
+        gs[g] = 0.0f;
+#pragma unroll
+        for (int b = 0; b < RB; ++b) dz[g][b] = zero_f32x16();
+    }
+    const bool active = first < T;  // wave-uniform; idle waves still stage experts
+    if (nstages > 0) {              // workgroup-uniform
+        gload(0);
+        stash(0);
+        if (nstages > 1) gload(1);
+        __syncthreads();
+        for (int st = 0; st < nstages; ++st) {
+            const int buf = st & 1;
+            if (active) {
+                for (int tl = we; tl < TILES; tl += WE) {
+                    const int32_t tile = tile0 + st * TILES + tl;
+                    if (tile >= tile1) break;
+                    bf16x8 a[RC];
+                    const uint16_t* ar = &rows[buf][(tl * 32 + n) * RP + 8 * half];
+#pragma unroll
+                    for (int c = 0; c < RC; ++c) a[c] = load_bf16x8(ar + 16 * c);
+                    // rows past M in the last tile: no probability
+                    const bool ragged = (tile + 1) * 32 > M;
+                    bf16x8 rt[2][RB];
+                    if constexpr (DZ) {
+#pragma unroll
+                        for (int q2 = 0; q2 < 2; ++q2)
+#pragma unroll
+                            for (int b = 0; b < RB; ++b) {
+                                int j = 32 * b + n;
+                                j = j < R ? j : R - 1;  // columns past r: never stored
+                                const uint16_t* pr = &rowsT[buf][j * CP + tl * 32 + 16 * q2 + 4 * half];
+                                rt[q2][b] = lds_two_quads(pr, pr + 8);
+                            }
+                    }
+#pragma unroll
+                    for (int g = 0; g < TPW; ++g) {
+                        f32x16 acc;
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) acc[i] = bt[g];
+#pragma unroll
+                        for (int c = 0; c < RC; ++c) acc = mfma_32x32x16(a[c], zh[g][c], acc);
+#pragma unroll
+                        for (int c = 0; c < RC; ++c) acc = mfma_32x32x16(a[c], zl[g][c], acc);
+                        // pbar of this lane's expert rows (re-read per group: fewer live registers)
+                        float pb[16];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            const f32x4 v = *reinterpret_cast<const f32x4*>(
+                                &pbs[buf][tl * 32 + 8 * q + 4 * half]);
+#pragma unroll
+                            for (int u = 0; u < 4; ++u) pb[4 * q + u] = v[u];
+                        }
+                        float p[16];
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) p[i] = bw_exp2(acc[i]);
+                        if (ragged) {
+#pragma unroll
+                            for (int i = 0; i < 16; ++i)
+                                p[i] = tile * 32 + acc_row(i, half) < M ? p[i] : 0.0f;
+                        }
+                        if constexpr (!DZ) {
+                            float s = 0.0f;
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) s += pb[i] * p[i];
+                            gs[g] += s;
+                        } else {
+                            float y[16];
+#pragma unroll
+                            for (int i = 0; i < 16; ++i) y[i] = p[i] * (pb[i] - gt[g]);
+                            const bf16x8 y0 = pack_bf16x8(y), y1 = pack_bf16x8(y + 8);
+#pragma unroll
+                            for (int b = 0; b < RB; ++b) {
+                                dz[g][b] = mfma_32x32x16(y0, rt[0][b], dz[g][b]);
+                                dz[g][b] = mfma_32x32x16(y1, rt[1][b], dz[g][b]);
+                            }
+                        }
+                    }
+                }
+            }
+            if (st + 1 < nstages) stash(buf ^ 1);
+            if (st + 2 < nstages) gload(st + 2);
+            __syncthreads();
+        }
+    }
+    const int64_t slot = (int64_t)split * WE + we;
+    if constexpr (!DZ) {
+#pragma unroll
+        for (int g = 0; g < TPW; ++g) {
+            const float tot = sum_pair32(gs[g]);  // the two lane halves hold disjoint rows
+            const int64_t t = first + 32 * g + n;
+            if (half == 0 && t < T) out[slot * T + t] = tot;
+        }
+    } else {
+        // lane: rank column 32 b + n, token rows acc_row(i, half) of group g
+#pragma unroll
+        for (int g = 0; g < TPW; ++g)
+#pragma unroll
+            for (int b = 0; b < RB; ++b) {
+                const int j = 32 * b + n;
+                if (j < R) {
+#pragma unroll
+                    for (int i = 0; i < 16; ++i) {
+                        const int64_t t = first + 32 * g + acc_row(i, half);
+                        if (t < T) out[(slot * T + t) * R + j] = dz[g][b][i];
+                    }
+                }
+            }
+    }
+}
+
+// out[j] = sum over p < P of in[p N + j], in order of p (0 when P == 0).
+__global__ __launch_bounds__(256) void bwd_sum_kernel(const float* __restrict__ in, int32_t P,
+                                                      int64_t N, float* __restrict__ out) {
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j >= N) return;
+    float s = 0.0f;
+    for (int32_t p = 0; p < P; ++p) s += in[(int64_t)p * N + j];
+    out[j] = s;
+}
+
+// ------------------------------------------------------------------------------ dz
+// One workgroup per 64 tokens: dz[t][j] = the P partials in order, then dtop[t][q] R2t[e][j]
+// for the token's selections q = 0 .. k-1 with e = idx[t][q] in [0, M).  Writes dz as bf16 hi/lo
+// rows dzhl [T][2r] and, through LDS, as transposed rows dzT [2][r][Tp] (Tp = T rounded up to
+// 64; the columns past T are zero).
+__global__ __launch_bounds__(256) void bwd_dz_kernel(const float* __restrict__ part, int32_t P,
+                                                     const int32_t* __restrict__ idx,
+                                                     const float* __restrict__ dtop, int32_t k,
+                                                     const uint16_t* __restrict__ R2t, int32_t T,
+                                                     int32_t r, int32_t M, int64_t Tp,
+                                                     uint16_t* __restrict__ dzhl,
+                                                     uint16_t* __restrict__ dzT) {
+    __shared__ uint16_t sh[2][64 * 65];  // [hi/lo][j][token] with 65 columns per row
+    const int64_t t0 = (int64_t)blockIdx.x * 64;
+    const int n = 64 * r;
+    for (int q = threadIdx.x; q < n; q += 256) {
+        const int tl = q / r, j = q % r;
+        const int64_t t = t0 + tl;
+        float s = 0.0f;
+        if (t < T) {
+            for (int32_t p = 0; p < P; ++p) s += part[((int64_t)p * T + t) * r + j];
+            for (int32_t u = 0; u < k; ++u) {
+                const int32_t e = idx[t * k + u];
+                if (e >= 0 && e < M)
+                    s += dtop[t * k + u] * bf16_bits_to_f32(R2t[(int64_t)e * r + j]);
+            }
+        }
+        const __bf16 hb = (__bf16)s;
+        const __bf16 lb = (__bf16)(s - (float)hb);
+        const uint16_t hv = __builtin_bit_cast(uint16_t, hb), lv = __builtin_bit_cast(uint16_t, lb);
+        if (t < T) {
+            dzhl[t * 2 * r + j] = hv;
+            dzhl[t * 2 * r + r + j] = lv;
+        }
+        sh[0][j * 65 + tl] = hv;
+        sh[1][j * 65 + tl] = lv;
+    }
+    __syncthreads();
+    for (int q = threadIdx.x; q < n; q += 256) {
+        const int j = q / 64, tl = q % 64;
+        dzT[(int64_t)j * Tp + t0 + tl] = sh[0][j * 65 + tl];
+        dzT[((int64_t)r + j) * Tp + t0 + tl] = sh[1][j * 65 + tl];
+    }
+}
+
+// ------------------------------------------------------------------------------ expert-major
+// Workgroup (expert block, token split): wave w owns NE expert tiles of the block, held as B
+// operands (expert columns) in registers, and the workgroup streams the 32-token tiles of its
+// split through LDS (z'_hi/z'_lo rows, bias and g of each token, and bf16(z) transposed), stages
+// of 128 tokens, double buffered.  A lane owns one expert column and sixteen token rows of each
+// logit tile; ybar = P (pbar_e - g_t) is then an A operand (expert rows, token K order as the
+// accumulator holds them) against bf16(z) pieces read from the transposed copy in the same K
+// order, accumulating dR2^T rows: part[split][e][r].  Rows past M are computed and not stored;
+// rows past T have bias kBwNoToken (P = 0) and zero z.
+template <int RC>
+struct ExpCfg {
+    static constexpr int R = 16 * RC;
+    static constexpr int RB = (R + 31) / 32;
+    static constexpr int ROW = 2 * R + 8;                  // LDS pitch of a z'_hi|z'_lo row
+    static constexpr int ZP = kBwStageT + 8;               // LDS pitch of a transposed z row
+    static constexpr int ZH_PIECES = kBwStageT * 2 * R / 8;
+    static constexpr int ZB_PIECES = kBwStageT * R / 8;
+    static constexpr int ZH_PPT = ZH_PIECES / kBwThreads;
+    static constexpr int ZB_PPT = (ZB_PIECES + kBwThreads - 1) / kBwThreads;
+    static constexpr int EXPERTS = 32 * kBwNE * kBwWaves;  // experts per workgroup
+    static_assert(ZH_PIECES % kBwThreads == 0, "whole pieces per thread");
+};
+
+template <int RC>
+__global__ __launch_bounds__(kBwThreads, 1) void bwd_exp_kernel(
+    const uint16_t* __restrict__ zhl, const uint16_t* __restrict__ zb,
+    const float* __restrict__ bias, const float* __restrict__ gtok,
+    const float* __restrict__ pbar, const uint16_t* __restrict__ R2t, int32_t T, int32_t M,
+    int32_t eblocks, int32_t splits, float* __restrict__ part) {
+    using C = ExpCfg<RC>;
+    constexpr int R = C::R, RB = C::RB, ROW = C::ROW, ZP = C::ZP, NE = kBwNE;
+    constexpr int TILES = kBwStageT / 32;
+    __shared__ __attribute__((aligned(16))) uint16_t zs[2][kBwStageT * ROW];
+    __shared__ __attribute__((aligned(16))) uint16_t zt[2][R * ZP];
+    __shared__ __attribute__((aligned(16))) float bs[2][kBwStageT];
+    __shared__ __attribute__((aligned(16))) float gss[2][kBwStageT];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 31, half = lane >> 5;
+    const int32_t eb = (int32_t)(blockIdx.x % (unsigned)eblocks);
+    const int32_t split = (int32_t)(blockIdx.x / (unsigned)eblocks);
+    const int64_t Tt = ((int64_t)T + 31) / 32;
+    const int64_t tt0 = Tt * split / splits, tt1 = Tt * (split + 1) / splits;
+    const int ntiles = (int)(tt1 - tt0);
+    const int nstages = (ntiles + TILES - 1) / TILES;
+    const int32_t Mt = (M + 31) / 32;
+    const int32_t etile0 = (eb * kBwWaves + w) * NE;
+    const bool active = etile0 < Mt;  // wave-uniform; idle waves still stage tokens
+    bf16x8 b[NE][RC];
+    float pb[NE];
+#pragma unroll
+    for (int j = 0; j < NE; ++j) {
+        int64_t e = (int64_t)32 * (etile0 + j) + n;
+        const bool ok = e < M;
+        e = ok ? e : M - 1;  // columns past M: never stored
+#pragma unroll
+        for (int c = 0; c < RC; ++c) b[j][c] = load_bf16x8(R2t + e * R + 16 * c + 8 * half);
+        pb[j] = ok ? pbar[e] : 0.0f;
+    }
+    u32x4 rh[C::ZH_PPT], rz[C::ZB_PPT];
+    float rb = 0.0f, rgv = 0.0f;
+    auto gload = [&](int st) __attribute__((always_inline)) {
+        const int64_t tok0 = (tt0 + (int64_t)st * TILES) * 32;
+#pragma unroll
+        for (int i = 0; i < C::ZH_PPT; ++i) {
+            const int p = tid + i * kBwThreads;
+            int64_t t = tok0 + p / (2 * R / 8);
+            t = t < T ? t : T - 1;  // rows past T: bias kBwNoToken below
+            rh[i] = *reinterpret_cast<const u32x4*>(zhl + t * (2 * R) + 8 * (p % (2 * R / 8)));
+        }
+#pragma unroll
+        for (int i = 0; i < C::ZB_PPT; ++i) {
+            const int p = tid + i * kBwThreads;
+            const int64_t t = tok0 + p / (R / 8);
+            const int64_t tc = t < T ? t : T - 1;
+            u32x4 v = u32x4{0u, 0u, 0u, 0u};
+            if (p < C::ZB_PIECES) v = *reinterpret_cast<const u32x4*>(zb + tc * R + 8 * (p % (R / 8)));
+            rz[i] = t < T ? v : u32x4{0u, 0u, 0u, 0u};
+        }
+        if (tid < kBwStageT) {
+            const int64_t t = tok0 + tid;
+            const int64_t tc = t < T ? t : T - 1;
+            const float bv = bias[tc], gv = gtok[tc];
+            rb = t < T ? bv : kBwNoToken;
+            rgv = t < T ? gv : 0.0f;
+        }
+    };
+    auto stash = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < C::ZH_PPT; ++i) {
+            const int p = tid + i * kBwThreads;
+            *reinterpret_cast<u32x4*>(&zs[buf][(p / (2 * R / 8)) * ROW + 8 * (p % (2 * R / 8))]) =
+                rh[i];
+        }
+#pragma unroll
+        for (int i = 0; i < C::ZB_PPT; ++i) {
+            const int p = tid + i * kBwThreads;
+            if (p < C::ZB_PIECES) {
+                const int tl = p / (R / 8), q = p % (R / 8);
+                const uint16_t* v = reinterpret_cast<const uint16_t*>(&rz[i]);
+#pragma unroll
+                for (int u = 0; u < 8; ++u) zt[buf][(8 * q + u) * ZP + tl] = v[u];
+            }
+        }
+        if (tid < kBwStageT) {
+            bs[buf][tid] = rb;
+            gss[buf][tid] = rgv;
+        }
+    };
+    f32x16 dr[NE][RB];
+#pragma unroll
+    for (int j = 0; j < NE; ++j)
+#pragma unroll
+        for (int q = 0; q < RB; ++q) dr[j][q] = zero_f32x16();
+    if (nstages > 0) {  // workgroup-uniform
+        gload(0);
+        stash(0);
+        if (nstages > 1) gload(1);
+        __syncthreads();
+        for (int st = 0; st < nstages; ++st) {
+            const int buf = st & 1;
+            const int cnt = min(TILES, ntiles - st * TILES);
+            if (active) {
+                for (int tl = 0; tl < cnt; ++tl) {
+                    const uint16_t* zr = &zs[buf][(tl * 32 + n) * ROW + 8 * half];
+                    bf16x8 a[2 * RC];
+#pragma unroll
+                    for (int c = 0; c < 2 * RC; ++c) a[c] = load_bf16x8(zr + 16 * c);
+                    f32x16 cin;
+                    float gv[16];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const f32x4 v =
+                            *reinterpret_cast<const f32x4*>(&bs[buf][tl * 32 + 8 * q + 4 * half]);
+                        const f32x4 u =
+                            *reinterpret_cast<const f32x4*>(&gss[buf][tl * 32 + 8 * q + 4 * half]);
+#pragma unroll
+                        for (int p = 0; p < 4; ++p) {
+                            cin[4 * q + p] = v[p];
+                            gv[4 * q + p] = u[p];
+                        }
+                    }
+                    bf16x8 zf[2][RB];
+#pragma unroll
+                    for (int q2 = 0; q2 < 2; ++q2)
+#pragma unroll
+                        for (int q = 0; q < RB; ++q) {
+                            int jr = 32 * q + n;
+                            jr = jr < R ? jr : R - 1;  // columns past r: never stored
+                            const uint16_t* pr = &zt[buf][jr * ZP + tl * 32 + 16 * q2 + 4 * half];
+                            zf[q2][q] = lds_two_quads(pr, pr + 8);
+                        }
+#pragma unroll
+                    for (int j = 0; j < NE; ++j) {
+                        f32x16 acc = mfma_32x32x16(a[0], b[j][0], cin);
+#pragma unroll
+                        for (int c = 1; c < RC; ++c) acc = mfma_32x32x16(a[c], b[j][c], acc);
+#pragma unroll
+                        for (int c = 0; c < RC; ++c) acc = mfma_32x32x16(a[RC + c], b[j][c], acc);
+                        float y[16];
+#pragma unroll
+                        for (int i = 0; i < 16; ++i) y[i] = bw_exp2(acc[i]) * (pb[j] - gv[i]);
+                        const bf16x8 y0 = pack_bf16x8(y), y1 = pack_bf16x8(y + 8);
+#pragma unroll
+                        for (int q = 0; q < RB; ++q) {
+                            dr[j][q] = mfma_32x32x16(y0, zf[0][q], dr[j][q]);
+                            dr[j][q] = mfma_32x32x16(y1, zf[1][q], dr[j][q]);
+                        }
+                    }
+                }
+            }
+            if (st + 1 < nstages) stash(buf ^ 1);
+            if (st + 2 < nstages) gload(st + 2);
+            __syncthreads();
+        }
+    }
+    // lane: rank column 32 q + n, expert rows acc_row(i, half) of tile j
+#pragma unroll
+    for (int j = 0; j < NE; ++j) {
+        if (etile0 + j >= Mt) break;
+#pragma unroll
+        for (int q = 0; q < RB; ++q) {
+            const int jr = 32 * q + n;
+            if (jr < R) {
+#pragma unroll
+                for (int i = 0; i < 16; ++i) {
+                    const int64_t e = (int64_t)32 * (etile0 + j) + acc_row(i, half);
+                    if (e < M) part[((int64_t)split * M + e) * R + jr] = dr[j][q][i];
+                }
+            }
+        }
+    }
+}
+
+// dR2t[e][j] = the P partials in order, then dtop[p] z[p / k][j] for the expert's selections p
+// in increasing order (offsets / sorted of the dispatch bookkeeping).  One thread per element.
+__global__ __launch_bounds__(256) void bwd_dr2_kernel(const float* __restrict__ part, int32_t P,
+                                                      const int32_t* __restrict__ offsets,
+                                                      const int32_t* __restrict__ sorted,
+                                                      const float* __restrict__ dtop, int32_t k,
+                                                      const float* __restrict__ z, int32_t M,
+                                                      int32_t r, float* __restrict__ dR2t) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= (int64_t)M * r) return;
+    const int64_t e = i / r;
+    const int32_t j = (int32_t)(i - e * r);
+    const int64_t N = (int64_t)M * r;
+    float s = 0.0f;
+    for (int32_t p = 0; p < P; ++p) s += part[(int64_t)p * N + i];
+    const int32_t q0 = offsets[e], q1 = offsets[e + 1];
+    for (int32_t q = q0; q < q1; ++q) {
+        const int32_t p = sorted[q];
+        s += dtop[p] * z[(int64_t)(p / k) * r + j];
+    }
+    dR2t[i] = s;
+}
+
+// ------------------------------------------------------------------------------ dx
+// dx [T][h] = dz R1^T with dz = hi + lo: a wave takes 32 tokens (A operands: dz rows) and
+// kBwDxTiles 32-column tiles (B operands: rows of R1 [h][r]); a lane stores one column.
+constexpr int kBwDxTiles = 4;
+
+template <int RC>
+__global__ __launch_bounds__(256) void bwd_dx_kernel(const uint16_t* __restrict__ dzhl,
+                                                     const uint16_t* __restrict__ R1, int32_t T,
+                                                     int32_t h, int32_t ctiles_per_wg,
+                                                     float* __restrict__ dx) {
+    constexpr int R = 16 * RC;
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int n = lane & 31, half = lane >> 5;
+    const int32_t Ct = (h + 31) / 32;
+    const int32_t cgroups = (Ct + ctiles_per_wg - 1) / ctiles_per_wg;
+    const int64_t tt = blockIdx.x / (unsigned)cgroups;
+    const int32_t cg = (int32_t)(blockIdx.x % (unsigned)cgroups);
+    const int64_t t = tt * 32 + n;
+    const bool tok_ok = t < T;
+    bf16x8 ah[RC], al[RC];
+    const uint16_t* dr = dzhl + (tok_ok ? t : 0) * (2 * R) + 8 * half;
+#pragma unroll
+    for (int c = 0; c < RC; ++c) {
+        const bf16x8 hv = load_bf16x8(dr + 16 * c), lv = load_bf16x8(dr + R + 16 * c);
+        ah[c] = tok_ok ? hv : zero_bf16x8();
+        al[c] = tok_ok ? lv : zero_bf16x8();
+    }
+    const int32_t ct_end = min(Ct, (cg + 1) * ctiles_per_wg);
+    for (int32_t ct = cg * ctiles_per_wg + w; ct < ct_end; ct += 4) {
+        int64_t col = (int64_t)ct * 32 + n;
+        const bool col_ok = col < h;
+        const uint16_t* br = R1 + (col_ok ? col : h - 1) * R + 8 * half;
+        f32x16 acc = zero_f32x16();
+#pragma unroll
+        for (int c = 0; c < RC; ++c) {
+            const bf16x8 bv = load_bf16x8(br + 16 * c);
+            acc = mfma_32x32x16(ah[c], bv, acc);
+            acc = mfma_32x32x16(al[c], bv, acc);
+        }
+        if (col_ok) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int64_t tr = tt * 32 + acc_row(i, half);
+                if (tr < T) dx[tr * h + col] = acc[i];
+            }
+        }
+    }
+}
+
+// ------------------------------------------------------------------------------ dR1
+// part[s][j][c] = sum over the tokens of split s of dz[t][j] x[t][c]: a workgroup of 4 waves
+// takes 128 columns (wave w: columns 32 w ..) and stages 64-token slices of x through LDS; the
+// A operands are dz^T rows (hi and lo) read from dzT, the B operands eight x values of one
+// column read down the LDS slice.
+constexpr int kBwR1Tok = 64;
+constexpr int kBwR1Cols = 128;
+constexpr int kBwR1Pitch = kBwR1Cols + 8;
+
+template <int RC>
+__global__ __launch_bounds__(256) void bwd_dr1_kernel(const uint16_t* __restrict__ x,
+                                                      const uint16_t* __restrict__ dzT,
+                                                      int64_t Tp, int32_t T, int32_t h,
+                                                      int32_t splits, float* __restrict__ part) {
+    constexpr int R = 16 * RC, RB = (R + 31) / 32;
+    constexpr int PIECES = kBwR1Tok * kBwR1Cols / 8;  // 1024
+    constexpr int PPT = PIECES / 256;
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][kBwR1Tok * kBwR1Pitch];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    const int n = lane & 31, half = lane >> 5;
+    const int32_t cblocks = (h + kBwR1Cols - 1) / kBwR1Cols;
+    const int32_t cb = (int32_t)(blockIdx.x % (unsigned)cblocks);
+    const int32_t split = (int32_t)(blockIdx.x / (unsigned)cblocks);
+    const int64_t Ts = Tp / kBwR1Tok;  // 64-token slices
+    const int64_t s0 = Ts * split / splits, s1 = Ts * (split + 1) / splits;
+    const int nst = (int)(s1 - s0);
+    const int64_t c0 = (int64_t)cb * kBwR1Cols;
+    u32x4 rg[PPT];
+    auto gload = [&](int st) __attribute__((always_inline)) {
+        const int64_t tok0 = (s0 + st) * kBwR1Tok;
+#pragma unroll
+        for (int i = 0; i < PPT; ++i) {
+            const int p = tid + i * 256;
+            const int64_t t = tok0 + p / (kBwR1Cols / 8);
+            const int64_t c = c0 + 8 * (p % (kBwR1Cols / 8));
+            const bool ok = t < T && c < h;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(x + (ok ? t * h + c : 0));
+            rg[i] = ok ? v : u32x4{0u, 0u, 0u, 0u};
+        }
+    };
+    auto stash = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < PPT; ++i) {
+            const int p = tid + i * 256;
+            *reinterpret_cast<u32x4*>(
+                &xs[buf][(p / (kBwR1Cols / 8)) * kBwR1Pitch + 8 * (p % (kBwR1Cols / 8))]) = rg[i];
+        }
+    };
+    f32x16 acc[RB];
+#pragma unroll
+    for (int q = 0; q < RB; ++q) acc[q] = zero_f32x16();
+    if (nst > 0) {
+        gload(0);
+        stash(0);
+        if (nst > 1) gload(1);
+        __syncthreads();
+        for (int st = 0; st < nst; ++st) {
+            const int buf = st & 1;
+            const int64_t tok0 = (s0 + st) * kBwR1Tok;
+#pragma unroll
+            for (int ks = 0; ks < kBwR1Tok / 16; ++ks) {
+                bf16x8 bx;
+                const uint16_t* xp = &xs[buf][(16 * ks + 8 * half) * kBwR1Pitch + 32 * w + n];
+#pragma unroll
+                for (int u = 0; u < 8; ++u)
+                    bx[u] = __builtin_bit_cast(__bf16, xp[u * kBwR1Pitch]);
+#pragma unroll
+                for (int q = 0; q < RB; ++q) {
+                    int jr = 32 * q + n;
+                    jr = jr < R ? jr : R - 1;  // rows past r: never stored
+                    const int64_t off = tok0 + 16 * ks + 8 * half;
+                    const bf16x8 ahv = load_bf16x8(dzT + (int64_t)jr * Tp + off);
+                    const bf16x8 alv = load_bf16x8(dzT + ((int64_t)R + jr) * Tp + off);
+                    acc[q] = mfma_32x32x16(ahv, bx, acc[q]);
+                    acc[q] = mfma_32x32x16(alv, bx, acc[q]);
+                }
+            }
+            if (st + 1 < nst) stash(buf ^ 1);
+            if (st + 2 < nst) gload(st + 2);
+            __syncthreads();
+        }
+    }
+    const int64_t c = c0 + 32 * w + n;
+    if (c < h) {
+#pragma unroll
+        for (int q = 0; q < RB; ++q)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int jr = 32 * q + acc_row(i, half);
+                if (jr < R) part[((int64_t)split * R + jr) * h + c] = acc[q][i];
+            }
+    }
+}
+
+// ------------------------------------------------------------------------------ host side
+namespace {
+
+size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+}  // namespace
+
+bool backward_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, bool balance,
+                        BackwardPlan* out) {
+    if (T < 0 || M <= 0 || k < 1 || (r != 16 && r != 32 && r != 64) || h <= 0 || h % 16 != 0)
+        return false;
+    BackwardPlan q{};
+    q.RC = r / 16;
+    q.balance = balance ? 1 : 0;
+    const int64_t Mt = ((int64_t)M + 31) / 32;
+    const int64_t Tt = (T + 31) / 32;
+    // token-major sweeps: WT token slots per workgroup, about 256 workgroups
+    auto tok_grid = [&](int tpw, TokGrid* g) {
+        const int64_t slot = 32 * tpw;
+        const int64_t slots_needed = (T + slot - 1) / slot;
+        int32_t WT = 8;
+        while (WT > 2 && (int64_t)WT / 2 >= slots_needed) WT /= 2;
+        g->WT = WT;
+        g->ntb = (T + WT * slot - 1) / (WT * slot);
+        int64_t S = (256 + g->ntb - 1) / (g->ntb > 0 ? g->ntb : 1);
+        const int64_t stages = (Mt + kBwStageE / 32 - 1) / (kBwStageE / 32);
+        if (S > stages) S = stages;
+        if (S < 1) S = 1;
+        g->splits = (int32_t)S;
+        g->parts = (int32_t)(S * (kBwWaves / WT));
+    };
+    switch (q.RC) {
+        case 1: tok_grid(bw_tpw<1, false>(), &q.gsweep); tok_grid(bw_tpw<1, true>(), &q.dzsweep); break;
+        case 2: tok_grid(bw_tpw<2, false>(), &q.gsweep); tok_grid(bw_tpw<2, true>(), &q.dzsweep); break;
+        default: tok_grid(bw_tpw<4, false>(), &q.gsweep); tok_grid(bw_tpw<4, true>(), &q.dzsweep); break;
+    }
+    // expert-major sweep: expert blocks of 32 NE waves tiles, about 512 workgroups
+    const int64_t per_block = 32 * kBwNE * kBwWaves;
+    q.eblocks = (int32_t)((M + per_block - 1) / per_block);
+    int64_t P = (512 + q.eblocks - 1) / q.eblocks;
+    if (P > Tt) P = Tt;
+    if (P < 1) P = 1;
+    q.esplits = (int32_t)P;
+    // dR1: 128-column blocks x token splits, about 512 workgroups
+    q.Tp = ((T + 63) / 64) * 64;
+    const int64_t cblocks = (h + kBwR1Cols - 1) / kBwR1Cols;
+    int64_t S3 = (512 + cblocks - 1) / cblocks;
+    if (S3 > q.Tp / 64) S3 = q.Tp / 64;
+    if (S3 < 1) S3 = 1;
+    q.r1splits = (int32_t)S3;
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += al256(bytes);
+        return at;
+    };
+    q.off_z = take((size_t)T * r * 4);
+    q.off_zscratch = take(zonly_workspace_bytes(T > 0 ? T : 1, h, r));
+    q.off_zhl = take((size_t)T * 2 * r * 2);
+    q.off_zb = take((size_t)T * r * 2);
+    q.off_bias = take((size_t)T * 4);
+    q.off_g = take((size_t)T * 4);
+    q.off_gpart = balance ? take((size_t)q.gsweep.parts * T * 4) : take(0);
+    q.off_dzpart = balance ? take((size_t)q.dzsweep.parts * T * r * 4) : take(0);
+    q.off_dzhl = take((size_t)T * 2 * r * 2);
+    q.off_dzT = take((size_t)2 * r * q.Tp * 2);
+    q.off_r1 = take((size_t)h * r * 2);
+    q.off_r2part = balance ? take((size_t)q.esplits * M * r * 4) : take(0);
+    q.off_r1part = take((size_t)q.r1splits * r * h * 4);
+    q.off_offsets = take(((size_t)M + 1) * 4);
+    q.off_sorted = take((size_t)T * k * 4);
+    q.off_dispatch = take(dispatch_workspace_bytes(T * k));
+    q.workspace_bytes = o;
+    *out = q;
+    return true;
+}
+
+template <int RC>
+static void launch_balance(const BackwardPlan& p, const BackwardArgs& a, char* ws,
+                           hipStream_t st) {
+    const uint16_t* zhl = reinterpret_cast<const uint16_t*>(ws + p.off_zhl);
+    const uint16_t* zb = reinterpret_cast<const uint16_t*>(ws + p.off_zb);
+    const float* bias = reinterpret_cast<const float*>(ws + p.off_bias);
+    float* g = reinterpret_cast<float*>(ws + p.off_g);
+    float* gpart = reinterpret_cast<float*>(ws + p.off_gpart);
+    float* dzpart = reinterpret_cast<float*>(ws + p.off_dzpart);
+    float* r2part = reinterpret_cast<float*>(ws + p.off_r2part);
+    const TokGrid& G = p.gsweep;
+    const TokGrid& D = p.dzsweep;
+    hipLaunchKernelGGL((bwd_tok_kernel<RC, false>), dim3((unsigned)(G.ntb * G.splits)),
+                       dim3(kBwThreads), 0, st, zhl, bias, nullptr, a.pbar, a.R2t, a.T, a.M, G.WT,
+                       G.splits, gpart);
+    hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)((a.T + 255) / 256)), dim3(256), 0, st,
+                       gpart, G.parts, (int64_t)a.T, g);
+    hipLaunchKernelGGL((bwd_tok_kernel<RC, true>), dim3((unsigned)(D.ntb * D.splits)),
+                       dim3(kBwThreads), 0, st, zhl, bias, g, a.pbar, a.R2t, a.T, a.M, D.WT,
+                       D.splits, dzpart);
+    hipLaunchKernelGGL((bwd_exp_kernel<RC>), dim3((unsigned)((int64_t)p.eblocks * p.esplits)),
+                       dim3(kBwThreads), 0, st, zhl, zb, bias, g, a.pbar, a.R2t, a.T, a.M,
+                       p.eblocks, p.esplits, r2part);
+}
+
+template <int RC>
+static void launch_phase3(const BackwardPlan& p, const BackwardArgs& a, char* ws,
+                          hipStream_t st) {
+    const uint16_t* dzhl = reinterpret_cast<const uint16_t*>(ws + p.off_dzhl);
+    const uint16_t* dzT = reinterpret_cast<const uint16_t*>(ws + p.off_dzT);
+    const uint16_t* R1 = reinterpret_cast<const uint16_t*>(ws + p.off_r1);
+    float* r1part = reinterpret_cast<float*>(ws + p.off_r1part);
+    const int32_t Ct = (a.h + 31) / 32;
+    const int32_t per_wg = 4 * kBwDxTiles;
+    const int64_t cgroups = (Ct + per_wg - 1) / per_wg;
+    const int64_t Tt = ((int64_t)a.T + 31) / 32;
+    if (Tt > 0)
+        hipLaunchKernelGGL((bwd_dx_kernel<RC>), dim3((unsigned)(Tt * cgroups)), dim3(256), 0, st,
+                           dzhl, R1, a.T, a.h, per_wg, a.dx);
+    const int64_t cblocks = (a.h + kBwR1Cols - 1) / kBwR1Cols;
+    hipLaunchKernelGGL((bwd_dr1_kernel<RC>), dim3((unsigned)(cblocks * p.r1splits)), dim3(256), 0,
+                       st, a.x, dzT, p.Tp, a.T, a.h, p.r1splits, r1part);
+    const int64_t N = (int64_t)a.r * a.h;
+    hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, st,
+                       r1part, p.r1splits, N, a.dR1t);
+}
+
+hipError_t backward_launch(const BackwardPlan& p, const BackwardArgs& a, void* workspace,
+                           hipStream_t st) {
+    char* ws = static_cast<char*>(workspace);
+    const int32_t r = a.r;
+    if (a.T == 0) {  // no tokens: zero weight gradients
+        hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)(((int64_t)r * a.h + 255) / 256)),
+                           dim3(256), 0, st, nullptr, 0, (int64_t)r * a.h, a.dR1t);
+        hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)(((int64_t)a.M * r + 255) / 256)),
+                           dim3(256), 0, st, nullptr, 0, (int64_t)a.M * r, a.dR2t);
+        return hipGetLastError();
+    }
+    float* z = reinterpret_cast<float*>(ws + p.off_z);
+    hipError_t e = zonly_launch(a.x, a.R1t, a.T, a.h, r, z, ws + p.off_zscratch, st);
+    if (e != hipSuccess) return e;
+    const int64_t nz = (int64_t)a.T * r;
+    hipLaunchKernelGGL(bwd_prep_kernel, dim3((unsigned)((nz + 255) / 256)), dim3(256), 0, st, z,
+                       p.balance ? a.m : nullptr, a.Z, a.T, r,
+                       reinterpret_cast<uint16_t*>(ws + p.off_zhl),
+                       reinterpret_cast<uint16_t*>(ws + p.off_zb),
+                       reinterpret_cast<float*>(ws + p.off_bias));
+    const int64_t nr1 = (int64_t)a.h * r;
+    hipLaunchKernelGGL(bwd_r1_transpose_kernel, dim3((unsigned)((nr1 + 255) / 256)), dim3(256), 0,
+                       st, a.R1t, a.h, r, reinterpret_cast<uint16_t*>(ws + p.off_r1));
+    if (p.balance) {
+        switch (p.RC) {
+            case 1: launch_balance<1>(p, a, ws, st); break;
+            case 2: launch_balance<2>(p, a, ws, st); break;
+            case 4: launch_balance<4>(p, a, ws, st); break;
+            default: return hipErrorInvalidValue;
+        }
+    }
+    const int32_t P1 = p.balance ? p.dzsweep.parts : 0;
+    hipLaunchKernelGGL(bwd_dz_kernel, dim3((unsigned)(p.Tp / 64)), dim3(256), 0, st,
+                       reinterpret_cast<const float*>(ws + p.off_dzpart), P1, a.idx, a.dtop, a.k,
+                       a.R2t, a.T, r, a.M, p.Tp, reinterpret_cast<uint16_t*>(ws + p.off_dzhl),
+                       reinterpret_cast<uint16_t*>(ws + p.off_dzT));
+    int32_t* offsets = reinterpret_cast<int32_t*>(ws + p.off_offsets);
+    int32_t* sorted = reinterpret_cast<int32_t*>(ws + p.off_sorted);
+    e = dispatch_launch(a.idx, (int64_t)a.T * a.k, a.M, offsets, sorted, ws + p.off_dispatch, st);
+    if (e != hipSuccess) return e;
+    const int64_t nr2 = (int64_t)a.M * r;
+    hipLaunchKernelGGL(bwd_dr2_kernel, dim3((unsigned)((nr2 + 255) / 256)), dim3(256), 0, st,
+                       reinterpret_cast<const float*>(ws + p.off_r2part),
+                       p.balance ? p.esplits : 0, offsets, sorted, a.dtop, a.k, z, a.M, r, a.dR2t);
+    switch (p.RC) {
+        case 1: launch_phase3<1>(p, a, ws, st); break;
+        case 2: launch_phase3<2>(p, a, ws, st); break;
+        case 4: launch_phase3<4>(p, a, ws, st); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace more

@@ -214,6 +214,63 @@ more_status more_route_lowrank_train(const uint16_t* x, const uint16_t* R1t, con
     return from_hip(more::stats_launch(sp, a, sws, st));
 }
 
+more_status more_route_lowrank_backward_workspace_size(int64_t T, int32_t h, int32_t r,
+                                                       int32_t M, int32_t k, int32_t balance,
+                                                       size_t* bytes) {
+    if (!bytes || r <= 0) return MORE_ERR_INVALID_ARG;
+    more_status s = check_common(T, h, M, k);
+    if (s != MORE_OK) return s;
+    if (!rank_supported(r)) return MORE_ERR_UNSUPPORTED;
+    if (T == 0) {
+        *bytes = 0;
+        return MORE_OK;
+    }
+    more::BackwardPlan p;
+    if (!more::backward_make_plan(T, h, r, M, k, balance != 0, &p)) return MORE_ERR_INVALID_ARG;
+    *bytes = p.workspace_bytes;
+    return MORE_OK;
+}
+
+more_status more_route_lowrank_backward(const uint16_t* x, const uint16_t* R1t,
+                                        const uint16_t* R2t, int64_t T, int32_t h, int32_t r,
+                                        int32_t M, int32_t k, const int32_t* idx,
+                                        const float* dtop, const float* pbar, const float* m,
+                                        const float* Z, float* dx, float* dR1t, float* dR2t,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+    if (!R1t || !R2t || !dR1t || !dR2t || (T != 0 && (!x || !idx || !dtop || !dx)) ||
+        (T != 0 && pbar && (!m || !Z)))
+        return MORE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(R1t, 16) || !aligned(R2t, 16) || !aligned(idx, 4) ||
+        !aligned(dtop, 4) || !aligned(pbar, 4) || !aligned(m, 4) || !aligned(Z, 4) ||
+        !aligned(dx, 4) || !aligned(dR1t, 4) || !aligned(dR2t, 4) || !aligned(workspace, 256))
+        return MORE_ERR_INVALID_ARG;
+    if (r <= 0) return MORE_ERR_INVALID_ARG;
+    more_status s = check_common(T, h, M, k);
+    if (s != MORE_OK) return s;
+    if (!rank_supported(r)) return MORE_ERR_UNSUPPORTED;
+    more::BackwardPlan p;
+    if (!more::backward_make_plan(T, h, r, M, k, pbar != nullptr, &p)) return MORE_ERR_INVALID_ARG;
+    if (T != 0 && (!workspace || workspace_bytes < p.workspace_bytes)) return MORE_ERR_WORKSPACE;
+    more::BackwardArgs a;
+    a.x = x;
+    a.R1t = R1t;
+    a.R2t = R2t;
+    a.T = (int32_t)T;
+    a.h = h;
+    a.r = r;
+    a.M = M;
+    a.k = k;
+    a.idx = idx;
+    a.dtop = dtop;
+    a.pbar = pbar;
+    a.m = m;
+    a.Z = Z;
+    a.dx = dx;
+    a.dR1t = dR1t;
+    a.dR2t = dR2t;
+    return from_hip(more::backward_launch(p, a, workspace, static_cast<hipStream_t>(stream)));
+}
+
 more_status more_route_fullrank_workspace_size(int64_t T, int32_t h, int32_t M, int32_t k,
                                                int32_t logit_bits, size_t* bytes) {
     if (!bytes) return MORE_ERR_INVALID_ARG;

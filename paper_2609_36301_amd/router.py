@@ -222,6 +222,94 @@ def route_lowrank_train(x: torch.Tensor, R1t: torch.Tensor, R2t: torch.Tensor, k
     return router(x, R1t, R2t)
 
 
+@dataclasses.dataclass
+class Gradients:
+    """Gradients of the training backward pass (float32)."""
+    dx: torch.Tensor    # [T][h]
+    dR1t: torch.Tensor  # [r][h]
+    dR2t: torch.Tensor  # [M][r]
+
+
+def lowrank_backward_workspace_size(T: int, h: int, r: int, M: int, k: int,
+                                    balance: bool = True) -> int:
+    n = ctypes.c_size_t(0)
+    _lib.check(_lib.load().more_route_lowrank_backward_workspace_size(T, h, r, M, k, int(balance),
+                                                                      ctypes.byref(n)),
+               "more_route_lowrank_backward_workspace_size")
+    return n.value
+
+
+def _check_dev(name: str, t: torch.Tensor, dtype, shape):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch.Tensor" % name)
+    if t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous tensor of shape %s, got %s"
+                         % (name, tuple(shape), tuple(t.shape)))
+    if t.device.type != "cuda":
+        raise ValueError("%s must be on a GPU device" % name)
+
+
+class LowrankBackward:
+    """Pre-allocated gradients and workspace for repeated backward calls with one shape
+    (more_route_lowrank_backward); balance=False leaves out the psum term (pbar)."""
+
+    def __init__(self, T: int, h: int, r: int, M: int, k: int, *, balance: bool = True,
+                 device=None):
+        self.shape = (T, h, r, M, k)
+        self.balance = balance
+        dev = torch.device(device or "cuda")
+        f32 = torch.float32
+        self.out = Gradients(dx=torch.empty((T, h), dtype=f32, device=dev),
+                             dR1t=torch.empty((r, h), dtype=f32, device=dev),
+                             dR2t=torch.empty((M, r), dtype=f32, device=dev))
+        nbytes = lowrank_backward_workspace_size(T, h, r, M, k, balance)
+        self.workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+        self.workspace_bytes = nbytes
+
+    def __call__(self, x, R1t, R2t, idx, dtop, pbar=None, m=None, Z=None) -> Gradients:
+        T, h, r, M, k = self.shape
+        _check_bf16("x", x, 2)
+        _check_bf16("R1t", R1t, 2)
+        _check_bf16("R2t", R2t, 2)
+        if tuple(x.shape) != (T, h) or tuple(R1t.shape) != (r, h) or tuple(R2t.shape) != (M, r):
+            raise ValueError("shapes %s %s %s do not match (T=%d, h=%d, r=%d, M=%d)"
+                             % (tuple(x.shape), tuple(R1t.shape), tuple(R2t.shape), T, h, r, M))
+        _check_dev("idx", idx, torch.int32, (T, k))
+        _check_dev("dtop", dtop, torch.float32, (T, k))
+        if (pbar is not None) != self.balance:
+            raise ValueError("pbar must be given exactly when the backward was set up with "
+                             "balance=True")
+        if pbar is not None:
+            _check_dev("pbar", pbar, torch.float32, (M,))
+            _check_dev("m", m, torch.float32, (T,))
+            _check_dev("Z", Z, torch.float32, (T,))
+        o = self.out
+        ws = _ptr(self.workspace) if self.workspace_bytes else None
+        st = _lib.load().more_route_lowrank_backward(
+            _ptr(x), _ptr(R1t), _ptr(R2t), T, h, r, M, k, _ptr(idx), _ptr(dtop), _ptr(pbar),
+            _ptr(m), _ptr(Z), _ptr(o.dx), _ptr(o.dR1t), _ptr(o.dR2t), ws, self.workspace_bytes,
+            _stream(x.device))
+        _lib.check(st, "more_route_lowrank_backward")
+        return o
+
+
+def route_lowrank_backward(x, R1t, R2t, idx, dtop, pbar=None, m=None, Z=None) -> Gradients:
+    """Training backward pass of the low-rank router: the gradients of x, R1t and R2t given the
+    gradient dtop [T][k] with respect to the selected logits and, optionally, pbar [M] with
+    respect to psum (then m and Z [T] are the statistics of the training forward pass)."""
+    _check_bf16("x", x, 2)
+    _check_bf16("R1t", R1t, 2)
+    _check_bf16("R2t", R2t, 2)
+    T, h = x.shape
+    r = R1t.shape[0]
+    M = R2t.shape[0]
+    k = idx.shape[1] if idx.dim() == 2 else 0
+    return LowrankBackward(T, h, r, M, k, balance=pbar is not None, device=x.device)(
+        x, R1t, R2t, idx, dtop, pbar, m, Z)
+
+
 class FullrankRouter:
     """Pre-allocated outputs and workspace (logits + GEMM scratch) for the full-rank router."""
 

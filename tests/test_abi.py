@@ -289,6 +289,64 @@ def test_fullrank_fused_validation(lib):
     assert call(T=0, x=None, idx=None, gate=None) == _lib.OK
 
 
+def backward(lib, T=64, h=64, r=16, M=64, k=4, x=FAKE, idx=FAKE, dtop=FAKE, pbar=FAKE, m=FAKE,
+             Z=FAKE, dx=FAKE, dR1t=FAKE, dR2t=FAKE, ws=FAKE, wsb=1 << 30):
+    return lib.more_route_lowrank_backward(x, FAKE, FAKE, T, h, r, M, k, idx, dtop, pbar, m, Z,
+                                           dx, dR1t, dR2t, ws, wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(x=None), _lib.ERR_INVALID_ARG),
+    (dict(idx=None), _lib.ERR_INVALID_ARG),
+    (dict(dtop=None), _lib.ERR_INVALID_ARG),
+    (dict(dx=None), _lib.ERR_INVALID_ARG),
+    (dict(dR1t=None), _lib.ERR_INVALID_ARG),
+    (dict(dR2t=None), _lib.ERR_INVALID_ARG),
+    (dict(m=None), _lib.ERR_INVALID_ARG),          # pbar given: the statistics are required
+    (dict(Z=None), _lib.ERR_INVALID_ARG),
+    (dict(dtop=ODD), _lib.ERR_INVALID_ARG),
+    (dict(ws=ctypes.c_void_p(0x10010)), _lib.ERR_INVALID_ARG),
+    (dict(T=-1), _lib.ERR_INVALID_ARG),
+    (dict(k=0), _lib.ERR_INVALID_ARG),
+    (dict(k=65), _lib.ERR_INVALID_ARG),            # k > M
+    (dict(M=100, k=33), _lib.ERR_UNSUPPORTED),
+    (dict(r=48), _lib.ERR_UNSUPPORTED),
+    (dict(h=72), _lib.ERR_UNSUPPORTED),
+    (dict(ws=None, wsb=0), _lib.ERR_WORKSPACE),
+    (dict(wsb=1000), _lib.ERR_WORKSPACE),
+])
+def test_backward_validation(lib, kw, status):
+    assert backward(lib, **kw) == status
+
+
+def test_backward_workspace_size(lib):
+    n, nb = ctypes.c_size_t(7), ctypes.c_size_t(0)
+    assert lib.more_route_lowrank_backward_workspace_size(0, 512, 32, 4096, 8, 1,
+                                                          ctypes.byref(n)) == _lib.OK
+    assert n.value == 0
+    assert lib.more_route_lowrank_backward_workspace_size(16, 512, 32, 4096, 8, 1,
+                                                          None) == _lib.ERR_INVALID_ARG
+    for T, h, r, M, k in [(256, 512, 16, 256, 8), (16384, 512, 32, 4096, 8),
+                          (32768, 2048, 64, 16384, 8), (16384, 4096, 64, 65536, 8),
+                          (128, 4096, 64, 262144, 16)]:
+        assert lib.more_route_lowrank_backward_workspace_size(T, h, r, M, k, 1,
+                                                              ctypes.byref(n)) == _lib.OK
+        assert lib.more_route_lowrank_backward_workspace_size(T, h, r, M, k, 0,
+                                                              ctypes.byref(nb)) == _lib.OK
+        # z, z' hi/lo, dz hi/lo twice, the transposed R1 and the sorted selections at least;
+        # the softmax sweeps add their partials of g, dz and dR2
+        base = T * r * 4 + T * r * 4 + 2 * T * r * 4 + h * r * 2 + T * k * 4
+        assert nb.value >= base
+        assert n.value >= nb.value + T * 4 + T * r * 4 + M * r * 4
+    # without pbar the statistics may be NULL
+    assert lib.more_route_lowrank_backward_workspace_size(64, 64, 16, 64, 4, 0,
+                                                          ctypes.byref(nb)) == 0
+    assert backward(lib, pbar=None, m=None, Z=None, wsb=nb.value - 1) == _lib.ERR_WORKSPACE
+    assert lib.more_route_lowrank_backward_workspace_size(64, 64, 16, 64, 4, 1,
+                                                          ctypes.byref(n)) == 0
+    assert backward(lib, wsb=n.value - 1) == _lib.ERR_WORKSPACE
+
+
 def test_binding_rejects_bad_tensors():
     import torch
     from paper_2609_36301_amd import router
