@@ -304,7 +304,31 @@ def main():
                            "unit": "TFLOP/s", "frac": round(sach / PEAK_BF16_TFLOPS, 4),
                            "algorithmic_flops": sflops,
                            "exp_per_s": round(2 * w.T * w.M / stats_s, 1)}}
-    del trr
+    # Training backward pass on the same batches (more_route_lowrank_backward): the selection
+    # and statistics of one training forward call, dtop ~ N(0, 1), pbar = (M / T) f.
+    # Algorithmic flops of the paper's algorithm: the logits in both sweeps, the two gradient
+    # contractions dz = ybar R2^T and dR2 = z^T ybar (2 T r M each), plus z, dx and dR1
+    # (2 T r h each); the balancing term is dense in M, so all of it is on the matrix cores.
+    tro = trr(*bufs[0])
+    gen = torch.Generator(device=dev).manual_seed(11)
+    dtop = torch.randn((w.T, w.k), device=dev, generator=gen)
+    pbar = (torch.bincount(tro.idx.flatten().long(), minlength=w.M).float()
+            * (w.M / (w.T * w.k))).contiguous()
+    bwd = router.LowrankBackward(w.T, w.h, w.r, w.M, w.k, device=dev)
+    sel = (tro.idx.clone(), tro.m.clone(), tro.Z.clone())
+    bt = timed_graph(lambda i: bwd(*bufs[i % nbuf], sel[0], dtop, pbar, sel[1], sel[2]),
+                     args.steps, args.warmup)
+    bflops = 8 * w.T * w.r * w.M + 6 * w.T * w.r * w.h
+    bach = bflops / bt["mean_s"] / 1e12
+    result["backward"] = {
+        "op": "training backward (more_route_lowrank_backward): dx, dR1, dR2 with the balancing "
+              "term, logits recomputed",
+        "ms": round(bt["mean_s"] * 1e3, 5), "tokens_per_s": round(w.T / bt["mean_s"], 1),
+        "roofline": {"bound": "mfma", "achieved": round(bach, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(bach / PEAK_BF16_TFLOPS, 4),
+                     "algorithmic_flops": bflops, "executed_flops": 16 * w.T * w.r * w.M
+                     + 6 * w.T * w.r * w.h}}
+    del trr, tro, bwd, sel
     torch.cuda.empty_cache()
 
     if not args.no_fullrank:

@@ -322,58 +322,103 @@ __global__ __launch_bounds__(kBwThreads, 1) void bwd_tok_kernel(
     }
 }
 
-// out[j] = sum over p < P of in[p N + j], in order of p (0 when P == 0).
-__global__ __launch_bounds__(256) void bwd_sum_kernel(const float* __restrict__ in, int32_t P,
-                                                      int64_t N, float* __restrict__ out) {
-    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (j >= N) return;
+// out[j] = sum over p < P of in[p N + j] in a fixed order (0 when P == 0): G threads per output
+// (blocks of 256 / G consecutive outputs, so that loads coalesce); thread q sums p = q, q + G, ...
+// in increasing order with eight loads in flight, and the G partials are added in order of q.
+__global__ __launch_bounds__(256) void bwd_colsum_kernel(const float* __restrict__ in, int32_t P,
+                                                         int64_t N, int32_t G,
+                                                         float* __restrict__ out) {
+    __shared__ float red[256];
+    const int per = 256 / G;
+    const int q = threadIdx.x / per, jj = threadIdx.x % per;
+    const int64_t j = (int64_t)blockIdx.x * per + jj;
     float s = 0.0f;
-    for (int32_t p = 0; p < P; ++p) s += in[(int64_t)p * N + j];
-    out[j] = s;
+    if (j < N) {
+        int32_t p = q;
+        for (; p + 7 * G < P; p += 8 * G) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = in[(int64_t)(p + u * G) * N + j];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; p < P; p += G) s += in[(int64_t)p * N + j];
+    }
+    red[threadIdx.x] = s;
+    __syncthreads();
+    if (q == 0 && j < N) {
+        float t = red[jj];
+        for (int qq = 1; qq < G; ++qq) t += red[qq * per + jj];
+        out[j] = t;
+    }
 }
 
 // ------------------------------------------------------------------------------ dz
-// One workgroup per 64 tokens: dz[t][j] = the P partials in order, then dtop[t][q] R2t[e][j]
-// for the token's selections q = 0 .. k-1 with e = idx[t][q] in [0, M).  Writes dz as bf16 hi/lo
-// rows dzhl [T][2r] and, through LDS, as transposed rows dzT [2][r][Tp] (Tp = T rounded up to
-// 64; the columns past T are zero).
-__global__ __launch_bounds__(256) void bwd_dz_kernel(const float* __restrict__ part, int32_t P,
+// One workgroup per 32 tokens, eight threads per token, each owning VPT = r / 8 consecutive rank
+// columns: dz[t][j] = dzsum[t][j] (the dense part, when given), then dtop[t][q] R2t[e][j] for the
+// token's selections q = 0 .. k-1 with e = idx[t][q] in [0, M) (one VPT-wide gather each).
+// Writes dz as bf16 hi/lo rows dzhl [T][2r] and, through LDS, as transposed rows dzT [2][r][Tp]
+// (Tp = T rounded up to 64; the columns past T are zero).
+template <int RC>
+__global__ __launch_bounds__(256) void bwd_dz_kernel(const float* __restrict__ dzsum,
                                                      const int32_t* __restrict__ idx,
                                                      const float* __restrict__ dtop, int32_t k,
                                                      const uint16_t* __restrict__ R2t, int32_t T,
-                                                     int32_t r, int32_t M, int64_t Tp,
+                                                     int32_t M, int64_t Tp,
                                                      uint16_t* __restrict__ dzhl,
                                                      uint16_t* __restrict__ dzT) {
-    __shared__ uint16_t sh[2][64 * 65];  // [hi/lo][j][token] with 65 columns per row
-    const int64_t t0 = (int64_t)blockIdx.x * 64;
-    const int n = 64 * r;
-    for (int q = threadIdx.x; q < n; q += 256) {
-        const int tl = q / r, j = q % r;
-        const int64_t t = t0 + tl;
-        float s = 0.0f;
-        if (t < T) {
-            for (int32_t p = 0; p < P; ++p) s += part[((int64_t)p * T + t) * r + j];
-            for (int32_t u = 0; u < k; ++u) {
-                const int32_t e = idx[t * k + u];
-                if (e >= 0 && e < M)
-                    s += dtop[t * k + u] * bf16_bits_to_f32(R2t[(int64_t)e * r + j]);
+    constexpr int R = 16 * RC, VPT = R / 8;
+    __shared__ uint16_t sh[2][R * 33];  // [hi/lo][j][token] with 33 columns per row
+    const int tl = threadIdx.x >> 3, jg = threadIdx.x & 7;
+    const int64_t t0 = (int64_t)blockIdx.x * 32;
+    const int64_t t = t0 + tl;
+    const int j0 = jg * VPT;
+    float s[VPT];
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) s[v] = 0.0f;
+    if (t < T) {
+        if (dzsum) {
+#pragma unroll
+            for (int v = 0; v < VPT; ++v) s[v] = dzsum[t * R + j0 + v];
+        }
+        for (int32_t u = 0; u < k; ++u) {
+            const int32_t e = idx[t * k + u];
+            if (e >= 0 && e < M) {
+                const float d = dtop[t * k + u];
+                const uint16_t* row = R2t + (int64_t)e * R + j0;
+                uint16_t w[VPT];
+                if constexpr (VPT == 8) {
+                    const u32x4 q = *reinterpret_cast<const u32x4*>(row);
+                    __builtin_memcpy(w, &q, sizeof w);
+                } else if constexpr (VPT == 4) {
+                    const uint2 q = *reinterpret_cast<const uint2*>(row);
+                    __builtin_memcpy(w, &q, sizeof w);
+                } else {
+                    const uint32_t q = *reinterpret_cast<const uint32_t*>(row);
+                    __builtin_memcpy(w, &q, sizeof w);
+                }
+#pragma unroll
+                for (int v = 0; v < VPT; ++v) s[v] += d * bf16_bits_to_f32(w[v]);
             }
         }
-        const __bf16 hb = (__bf16)s;
-        const __bf16 lb = (__bf16)(s - (float)hb);
+    }
+#pragma unroll
+    for (int v = 0; v < VPT; ++v) {
+        const __bf16 hb = (__bf16)s[v];
+        const __bf16 lb = (__bf16)(s[v] - (float)hb);
         const uint16_t hv = __builtin_bit_cast(uint16_t, hb), lv = __builtin_bit_cast(uint16_t, lb);
         if (t < T) {
-            dzhl[t * 2 * r + j] = hv;
-            dzhl[t * 2 * r + r + j] = lv;
+            dzhl[t * 2 * R + j0 + v] = hv;
+            dzhl[t * 2 * R + R + j0 + v] = lv;
         }
-        sh[0][j * 65 + tl] = hv;
-        sh[1][j * 65 + tl] = lv;
+        sh[0][(j0 + v) * 33 + tl] = hv;
+        sh[1][(j0 + v) * 33 + tl] = lv;
     }
     __syncthreads();
-    for (int q = threadIdx.x; q < n; q += 256) {
-        const int j = q / 64, tl = q % 64;
-        dzT[(int64_t)j * Tp + t0 + tl] = sh[0][j * 65 + tl];
-        dzT[((int64_t)r + j) * Tp + t0 + tl] = sh[1][j * 65 + tl];
+    for (int q = threadIdx.x; q < 32 * R; q += 256) {
+        const int j = q / 32, c = q % 32;
+        dzT[(int64_t)j * Tp + t0 + c] = sh[0][j * 33 + c];
+        dzT[((int64_t)R + j) * Tp + t0 + c] = sh[1][j * 33 + c];
     }
 }
 
@@ -572,13 +617,69 @@ __global__ __launch_bounds__(kBwThreads, 1) void bwd_exp_kernel(
     }
 }
 
-// dR2t[e][j] = the P partials in order, then dtop[p] z[p / k][j] for the expert's selections p
-// in increasing order (offsets / sorted of the dispatch bookkeeping).  One thread per element.
+// The dtop terms of dR2, sum over the selections p of expert e of dtop[p] z[p / k][:], as a
+// segmented sum over the sorted selections: one wave per chunk of kBwChunk consecutive sorted
+// entries (lane j < r holds rank column j) walks its entries in order and sums each run of one
+// expert.  An expert whose entries lie in one chunk gets its sum written to dR2t[e][:] (read
+// back, after the dense part, by bwd_dr2); for an expert spanning chunks c0 < c1 each chunk
+// stores its run in bpart[c][s][:], with s = 1 in c0 (the chunk's last run) and s = 0 in the
+// others (the chunk's first run), and bwd_dr2 adds them in chunk order.
+constexpr int kBwChunk = 64;
+
+__global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restrict__ sorted,
+                                                         const int32_t* __restrict__ offsets,
+                                                         const int32_t* __restrict__ idx,
+                                                         const float* __restrict__ dtop,
+                                                         const float* __restrict__ z, int32_t k,
+                                                         int32_t r, int32_t M, int64_t nchunks,
+                                                         float* __restrict__ dR2t,
+                                                         float* __restrict__ bpart) {
+    const int lane = threadIdx.x & 63;
+    const int64_t c = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (c >= nchunks) return;  // wave-uniform
+    const int64_t nv = offsets[M];  // entries with a valid id
+    const int64_t q0 = c * kBwChunk;
+    const int cnt = (int)min((int64_t)kBwChunk, nv - q0);
+    if (cnt <= 0) return;  // wave-uniform
+    int32_t pl = 0, el = 0;
+    float vl = 0.0f;
+    if (lane < cnt) {
+        pl = sorted[q0 + lane];
+        el = idx[pl];
+        vl = dtop[pl];
+    }
+    auto flush = [&](int32_t e, float acc) __attribute__((always_inline)) {
+        const int64_t o0 = offsets[e], o1 = offsets[e + 1];
+        const int64_t c0 = o0 / kBwChunk, c1 = (o1 - 1) / kBwChunk;
+        if (lane < r) {
+            if (c0 == c1)
+                dR2t[(int64_t)e * r + lane] = acc;
+            else
+                bpart[(c * 2 + (c == c0 ? 1 : 0)) * r + lane] = acc;
+        }
+    };
+    int32_t cur = __builtin_amdgcn_readfirstlane(el);
+    float acc = 0.0f;
+    for (int u = 0; u < cnt; ++u) {
+        const int32_t e = __builtin_amdgcn_readlane(el, u);
+        const int32_t p = __builtin_amdgcn_readlane(pl, u);
+        const float v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
+                                                      __builtin_bit_cast(int32_t, vl), u));
+        if (e != cur) {
+            flush(cur, acc);
+            cur = e;
+            acc = 0.0f;
+        }
+        if (lane < r) acc += v * z[(int64_t)(p / k) * r + lane];
+    }
+    flush(cur, acc);
+}
+
+// dR2t[e][j] = the P partials in order, then the dtop terms of bwd_sparse (in chunk order for an
+// expert spanning chunks).  One thread per element.
 __global__ __launch_bounds__(256) void bwd_dr2_kernel(const float* __restrict__ part, int32_t P,
                                                       const int32_t* __restrict__ offsets,
-                                                      const int32_t* __restrict__ sorted,
-                                                      const float* __restrict__ dtop, int32_t k,
-                                                      const float* __restrict__ z, int32_t M,
+                                                      const float* __restrict__ bpart, int32_t M,
                                                       int32_t r, float* __restrict__ dR2t) {
     const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (i >= (int64_t)M * r) return;
@@ -586,11 +687,24 @@ __global__ __launch_bounds__(256) void bwd_dr2_kernel(const float* __restrict__ 
     const int32_t j = (int32_t)(i - e * r);
     const int64_t N = (int64_t)M * r;
     float s = 0.0f;
-    for (int32_t p = 0; p < P; ++p) s += part[(int64_t)p * N + i];
-    const int32_t q0 = offsets[e], q1 = offsets[e + 1];
-    for (int32_t q = q0; q < q1; ++q) {
-        const int32_t p = sorted[q];
-        s += dtop[p] * z[(int64_t)(p / k) * r + j];
+    int32_t p = 0;
+    for (; p + 8 <= P; p += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(p + u) * N + i];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; p < P; ++p) s += part[(int64_t)p * N + i];
+    const int64_t o0 = offsets[e], o1 = offsets[e + 1];
+    if (o1 > o0) {
+        const int64_t c0 = o0 / kBwChunk, c1 = (o1 - 1) / kBwChunk;
+        if (c0 == c1) {
+            s += dR2t[i];
+        } else {
+            s += bpart[(c0 * 2 + 1) * r + j];
+            for (int64_t c = c0 + 1; c <= c1; ++c) s += bpart[(c * 2) * r + j];
+        }
     }
     dR2t[i] = s;
 }
@@ -746,6 +860,20 @@ namespace {
 
 size_t al256(size_t b) { return (b + 255) & ~(size_t)255; }
 
+// Threads per output of bwd_colsum for P partials: about eight partials per thread, at most 16.
+int32_t colsum_group(int64_t P) {
+    int32_t G = 1;
+    while (G < 16 && (int64_t)G * 8 < P) G *= 2;
+    return G;
+}
+
+void launch_colsum(const float* in, int32_t P, int64_t N, float* out, hipStream_t st) {
+    const int32_t G = colsum_group(P);
+    const int64_t per = 256 / G;
+    hipLaunchKernelGGL(bwd_colsum_kernel, dim3((unsigned)((N + per - 1) / per)), dim3(256), 0, st,
+                       in, P, N, G, out);
+}
+
 }  // namespace
 
 bool backward_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, bool balance,
@@ -805,6 +933,7 @@ bool backward_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, b
     q.off_g = take((size_t)T * 4);
     q.off_gpart = balance ? take((size_t)q.gsweep.parts * T * 4) : take(0);
     q.off_dzpart = balance ? take((size_t)q.dzsweep.parts * T * r * 4) : take(0);
+    q.off_dzsum = balance ? take((size_t)T * r * 4) : take(0);
     q.off_dzhl = take((size_t)T * 2 * r * 2);
     q.off_dzT = take((size_t)2 * r * q.Tp * 2);
     q.off_r1 = take((size_t)h * r * 2);
@@ -813,6 +942,8 @@ bool backward_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, b
     q.off_offsets = take(((size_t)M + 1) * 4);
     q.off_sorted = take((size_t)T * k * 4);
     q.off_dispatch = take(dispatch_workspace_bytes(T * k));
+    q.nchunks = (T * k + kBwChunk - 1) / kBwChunk;
+    q.off_bpart = take((size_t)q.nchunks * 2 * r * 4);
     q.workspace_bytes = o;
     *out = q;
     return true;
@@ -828,16 +959,17 @@ static void launch_balance(const BackwardPlan& p, const BackwardArgs& a, char* w
     float* gpart = reinterpret_cast<float*>(ws + p.off_gpart);
     float* dzpart = reinterpret_cast<float*>(ws + p.off_dzpart);
     float* r2part = reinterpret_cast<float*>(ws + p.off_r2part);
+    float* dzsum = reinterpret_cast<float*>(ws + p.off_dzsum);
     const TokGrid& G = p.gsweep;
     const TokGrid& D = p.dzsweep;
     hipLaunchKernelGGL((bwd_tok_kernel<RC, false>), dim3((unsigned)(G.ntb * G.splits)),
                        dim3(kBwThreads), 0, st, zhl, bias, nullptr, a.pbar, a.R2t, a.T, a.M, G.WT,
                        G.splits, gpart);
-    hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)((a.T + 255) / 256)), dim3(256), 0, st,
-                       gpart, G.parts, (int64_t)a.T, g);
+    launch_colsum(gpart, G.parts, a.T, g, st);
     hipLaunchKernelGGL((bwd_tok_kernel<RC, true>), dim3((unsigned)(D.ntb * D.splits)),
                        dim3(kBwThreads), 0, st, zhl, bias, g, a.pbar, a.R2t, a.T, a.M, D.WT,
                        D.splits, dzpart);
+    launch_colsum(dzpart, D.parts, (int64_t)a.T * a.r, dzsum, st);
     hipLaunchKernelGGL((bwd_exp_kernel<RC>), dim3((unsigned)((int64_t)p.eblocks * p.esplits)),
                        dim3(kBwThreads), 0, st, zhl, zb, bias, g, a.pbar, a.R2t, a.T, a.M,
                        p.eblocks, p.esplits, r2part);
@@ -850,6 +982,12 @@ static void launch_phase3(const BackwardPlan& p, const BackwardArgs& a, char* ws
     const uint16_t* dzT = reinterpret_cast<const uint16_t*>(ws + p.off_dzT);
     const uint16_t* R1 = reinterpret_cast<const uint16_t*>(ws + p.off_r1);
     float* r1part = reinterpret_cast<float*>(ws + p.off_r1part);
+    // dz = the dense sum (when pbar is given) plus the dtop rows of R2, as hi/lo rows and transposed
+    hipLaunchKernelGGL((bwd_dz_kernel<RC>), dim3((unsigned)(p.Tp / 32)), dim3(256), 0, st,
+                       p.balance ? reinterpret_cast<const float*>(ws + p.off_dzsum) : nullptr,
+                       a.idx, a.dtop, a.k, a.R2t, a.T, a.M, p.Tp,
+                       reinterpret_cast<uint16_t*>(ws + p.off_dzhl),
+                       reinterpret_cast<uint16_t*>(ws + p.off_dzT));
     const int32_t Ct = (a.h + 31) / 32;
     const int32_t per_wg = 4 * kBwDxTiles;
     const int64_t cgroups = (Ct + per_wg - 1) / per_wg;
@@ -860,9 +998,7 @@ static void launch_phase3(const BackwardPlan& p, const BackwardArgs& a, char* ws
     const int64_t cblocks = (a.h + kBwR1Cols - 1) / kBwR1Cols;
     hipLaunchKernelGGL((bwd_dr1_kernel<RC>), dim3((unsigned)(cblocks * p.r1splits)), dim3(256), 0,
                        st, a.x, dzT, p.Tp, a.T, a.h, p.r1splits, r1part);
-    const int64_t N = (int64_t)a.r * a.h;
-    hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)((N + 255) / 256)), dim3(256), 0, st,
-                       r1part, p.r1splits, N, a.dR1t);
+    launch_colsum(r1part, p.r1splits, (int64_t)a.r * a.h, a.dR1t, st);
 }
 
 hipError_t backward_launch(const BackwardPlan& p, const BackwardArgs& a, void* workspace,
@@ -870,10 +1006,8 @@ hipError_t backward_launch(const BackwardPlan& p, const BackwardArgs& a, void* w
     char* ws = static_cast<char*>(workspace);
     const int32_t r = a.r;
     if (a.T == 0) {  // no tokens: zero weight gradients
-        hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)(((int64_t)r * a.h + 255) / 256)),
-                           dim3(256), 0, st, nullptr, 0, (int64_t)r * a.h, a.dR1t);
-        hipLaunchKernelGGL(bwd_sum_kernel, dim3((unsigned)(((int64_t)a.M * r + 255) / 256)),
-                           dim3(256), 0, st, nullptr, 0, (int64_t)a.M * r, a.dR2t);
+        launch_colsum(nullptr, 0, (int64_t)r * a.h, a.dR1t, st);
+        launch_colsum(nullptr, 0, (int64_t)a.M * r, a.dR2t, st);
         return hipGetLastError();
     }
     float* z = reinterpret_cast<float*>(ws + p.off_z);
@@ -896,19 +1030,17 @@ hipError_t backward_launch(const BackwardPlan& p, const BackwardArgs& a, void* w
             default: return hipErrorInvalidValue;
         }
     }
-    const int32_t P1 = p.balance ? p.dzsweep.parts : 0;
-    hipLaunchKernelGGL(bwd_dz_kernel, dim3((unsigned)(p.Tp / 64)), dim3(256), 0, st,
-                       reinterpret_cast<const float*>(ws + p.off_dzpart), P1, a.idx, a.dtop, a.k,
-                       a.R2t, a.T, r, a.M, p.Tp, reinterpret_cast<uint16_t*>(ws + p.off_dzhl),
-                       reinterpret_cast<uint16_t*>(ws + p.off_dzT));
     int32_t* offsets = reinterpret_cast<int32_t*>(ws + p.off_offsets);
     int32_t* sorted = reinterpret_cast<int32_t*>(ws + p.off_sorted);
     e = dispatch_launch(a.idx, (int64_t)a.T * a.k, a.M, offsets, sorted, ws + p.off_dispatch, st);
     if (e != hipSuccess) return e;
+    float* bpart = reinterpret_cast<float*>(ws + p.off_bpart);
+    hipLaunchKernelGGL(bwd_sparse_kernel, dim3((unsigned)((p.nchunks + 3) / 4)), dim3(256), 0, st,
+                       sorted, offsets, a.idx, a.dtop, z, a.k, r, a.M, p.nchunks, a.dR2t, bpart);
     const int64_t nr2 = (int64_t)a.M * r;
     hipLaunchKernelGGL(bwd_dr2_kernel, dim3((unsigned)((nr2 + 255) / 256)), dim3(256), 0, st,
                        reinterpret_cast<const float*>(ws + p.off_r2part),
-                       p.balance ? p.esplits : 0, offsets, sorted, a.dtop, a.k, z, a.M, r, a.dR2t);
+                       p.balance ? p.esplits : 0, offsets, bpart, a.M, r, a.dR2t);
     switch (p.RC) {
         case 1: launch_phase3<1>(p, a, ws, st); break;
         case 2: launch_phase3<2>(p, a, ws, st); break;

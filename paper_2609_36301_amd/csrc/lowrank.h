@@ -144,8 +144,10 @@ struct BackwardPlan {
     int32_t esplits;     //   x token splits
     int64_t Tp;          // T rounded up to 64
     int32_t r1splits;    // token splits of dR1
+    int64_t nchunks;     // chunks of the sorted selections in the segmented dtop sum of dR2
     size_t off_z, off_zscratch, off_zhl, off_zb, off_bias, off_g, off_gpart, off_dzpart,
-        off_dzhl, off_dzT, off_r1, off_r2part, off_r1part, off_offsets, off_sorted, off_dispatch;
+        off_dzsum, off_dzhl, off_dzT, off_r1, off_r2part, off_r1part, off_offsets, off_sorted,
+        off_dispatch, off_bpart;
     size_t workspace_bytes;
 };
 
