@@ -248,13 +248,16 @@ __global__ __launch_bounds__(kBwThreads, 1) void bwd_tok_kernel(
                     }
 #pragma unroll
                     for (int g = 0; g < TPW; ++g) {
-                        f32x16 acc;
+                        // two independent chains (z'_hi with the bias, z'_lo), added at the end
+                        f32x16 acc, acl = zero_f32x16();
 #pragma unroll
                         for (int i = 0; i < 16; ++i) acc[i] = bt[g];
 #pragma unroll
-                        for (int c = 0; c < RC; ++c) acc = mfma_32x32x16(a[c], zh[g][c], acc);
-#pragma unroll
-                        for (int c = 0; c < RC; ++c) acc = mfma_32x32x16(a[c], zl[g][c], acc);
+                        for (int c = 0; c < RC; ++c) {
+                            acc = mfma_32x32x16(a[c], zh[g][c], acc);
+                            acl = mfma_32x32x16(a[c], zl[g][c], acl);
+                        }
+                        acc += acl;
                         // pbar of this lane's expert rows (re-read per group: fewer live registers)
                         float pb[16];
 #pragma unroll
@@ -577,11 +580,21 @@ __global__ __launch_bounds__(kBwThreads, 1) void bwd_exp_kernel(
                         }
 #pragma unroll
                     for (int j = 0; j < NE; ++j) {
-                        f32x16 acc = mfma_32x32x16(a[0], b[j][0], cin);
+                        f32x16 acc = cin;
+                        if constexpr (RC < 4) {
+                            // two independent chains (z'_hi with the bias, z'_lo), added at the
+                            // end (at r = 64 the NE tiles' chains suffice and registers are short)
+                            f32x16 acl = zero_f32x16();
 #pragma unroll
-                        for (int c = 1; c < RC; ++c) acc = mfma_32x32x16(a[c], b[j][c], acc);
+                            for (int c = 0; c < RC; ++c) {
+                                acc = mfma_32x32x16(a[c], b[j][c], acc);
+                                acl = mfma_32x32x16(a[RC + c], b[j][c], acl);
+                            }
+                            acc += acl;
+                        } else {
 #pragma unroll
-                        for (int c = 0; c < RC; ++c) acc = mfma_32x32x16(a[RC + c], b[j][c], acc);
+                            for (int c = 0; c < 2 * RC; ++c) acc = mfma_32x32x16(a[c], b[j][c % RC], acc);
+                        }
                         float y[16];
 #pragma unroll
                         for (int i = 0; i < 16; ++i) y[i] = bw_exp2(acc[i]) * (pb[j] - gv[i]);
@@ -660,17 +673,30 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
     };
     int32_t cur = __builtin_amdgcn_readfirstlane(el);
     float acc = 0.0f;
-    for (int u = 0; u < cnt; ++u) {
-        const int32_t e = __builtin_amdgcn_readlane(el, u);
-        const int32_t p = __builtin_amdgcn_readlane(pl, u);
-        const float v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(
-                                                      __builtin_bit_cast(int32_t, vl), u));
-        if (e != cur) {
-            flush(cur, acc);
-            cur = e;
-            acc = 0.0f;
+    const int32_t vbits = __builtin_bit_cast(int32_t, vl);
+    for (int u0 = 0; u0 < cnt; u0 += 8) {
+        // the z rows of eight entries in flight, then the entries in order
+        int32_t ev[8];
+        float vv[8], zv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int u = min(u0 + q, cnt - 1);
+            ev[q] = __builtin_amdgcn_readlane(el, u);
+            const int32_t p = __builtin_amdgcn_readlane(pl, u);
+            vv[q] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(vbits, u));
+            zv[q] = lane < r ? z[(int64_t)(p / k) * r + lane] : 0.0f;
         }
-        if (lane < r) acc += v * z[(int64_t)(p / k) * r + lane];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            if (u0 + q < cnt) {
+                if (ev[q] != cur) {
+                    flush(cur, acc);
+                    cur = ev[q];
+                    acc = 0.0f;
+                }
+                acc += vv[q] * zv[q];
+            }
+        }
     }
     flush(cur, acc);
 }
