@@ -194,6 +194,34 @@ def cpu_baseline_and_parity(w, inp, out, budget_s=40.0):
     return base, par
 
 
+def backward_leg(w, dev, router, trr, bufs, nbuf, args):
+    """Training backward pass on the rotating batches (more_route_lowrank_backward): the
+    selection and statistics of one training forward call, dtop ~ N(0, 1), pbar = (M / T) f.
+    Algorithmic flops of the paper's algorithm: the logits in both sweeps, the two gradient
+    contractions dz = ybar R2^T and dR2 = z^T ybar (2 T r M each), plus z, dx and dR1
+    (2 T r h each); the balancing term is dense in M, so all of it is on the matrix cores."""
+    import torch
+    tro = trr(*bufs[0])
+    gen = torch.Generator(device=dev).manual_seed(11)
+    dtop = torch.randn((w.T, w.k), device=dev, generator=gen)
+    pbar = (torch.bincount(tro.idx.flatten().long(), minlength=w.M).float()
+            * (w.M / (w.T * w.k))).contiguous()
+    bwd = router.LowrankBackward(w.T, w.h, w.r, w.M, w.k, device=dev)
+    sel = (tro.idx.clone(), tro.m.clone(), tro.Z.clone())
+    bt = timed_graph(lambda i: bwd(*bufs[i % nbuf], sel[0], dtop, pbar, sel[1], sel[2]),
+                     args.steps, args.warmup)
+    bflops = 8 * w.T * w.r * w.M + 6 * w.T * w.r * w.h
+    bach = bflops / bt["mean_s"] / 1e12
+    return {
+        "op": "training backward (more_route_lowrank_backward): dx, dR1, dR2 with the balancing "
+              "term, logits recomputed",
+        "ms": round(bt["mean_s"] * 1e3, 5), "tokens_per_s": round(w.T / bt["mean_s"], 1),
+        "roofline": {"bound": "mfma", "achieved": round(bach, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(bach / PEAK_BF16_TFLOPS, 4),
+                     "algorithmic_flops": bflops,
+                     "executed_flops": 16 * w.T * w.r * w.M + 6 * w.T * w.r * w.h}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -203,6 +231,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip the oracle leg (CPU baseline and parity counts)")
     ap.add_argument("--no-fullrank", action="store_true")
+    ap.add_argument("--no-backward", action="store_true", help="skip the training backward leg")
+    ap.add_argument("--backward-only", action="store_true",
+                    help="time only the training backward pass (one JSON line of its own)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain copy kernel of BYTES (counter calibration) and exit")
     args = ap.parse_args()
@@ -239,6 +270,13 @@ def main():
                      torch.roll(r1, shifts=b, dims=1).contiguous(),
                      torch.roll(r2, shifts=b * 13, dims=0).contiguous()))
     torch.cuda.synchronize()
+
+    if args.backward_only:
+        trr = router.LowrankTrainRouter(w.T, w.h, w.r, w.M, w.k, device=dev)
+        print(json.dumps({"workload": w.name, "steps": args.steps, "warmup": args.warmup,
+                          "backward": backward_leg(w, dev, router, trr, bufs, nbuf, args)}),
+              flush=True)
+        return
 
     lr = router.LowrankRouter(w.T, w.h, w.r, w.M, w.k, device=dev, histogram=w.histogram)
 
@@ -304,31 +342,9 @@ def main():
                            "unit": "TFLOP/s", "frac": round(sach / PEAK_BF16_TFLOPS, 4),
                            "algorithmic_flops": sflops,
                            "exp_per_s": round(2 * w.T * w.M / stats_s, 1)}}
-    # Training backward pass on the same batches (more_route_lowrank_backward): the selection
-    # and statistics of one training forward call, dtop ~ N(0, 1), pbar = (M / T) f.
-    # Algorithmic flops of the paper's algorithm: the logits in both sweeps, the two gradient
-    # contractions dz = ybar R2^T and dR2 = z^T ybar (2 T r M each), plus z, dx and dR1
-    # (2 T r h each); the balancing term is dense in M, so all of it is on the matrix cores.
-    tro = trr(*bufs[0])
-    gen = torch.Generator(device=dev).manual_seed(11)
-    dtop = torch.randn((w.T, w.k), device=dev, generator=gen)
-    pbar = (torch.bincount(tro.idx.flatten().long(), minlength=w.M).float()
-            * (w.M / (w.T * w.k))).contiguous()
-    bwd = router.LowrankBackward(w.T, w.h, w.r, w.M, w.k, device=dev)
-    sel = (tro.idx.clone(), tro.m.clone(), tro.Z.clone())
-    bt = timed_graph(lambda i: bwd(*bufs[i % nbuf], sel[0], dtop, pbar, sel[1], sel[2]),
-                     args.steps, args.warmup)
-    bflops = 8 * w.T * w.r * w.M + 6 * w.T * w.r * w.h
-    bach = bflops / bt["mean_s"] / 1e12
-    result["backward"] = {
-        "op": "training backward (more_route_lowrank_backward): dx, dR1, dR2 with the balancing "
-              "term, logits recomputed",
-        "ms": round(bt["mean_s"] * 1e3, 5), "tokens_per_s": round(w.T / bt["mean_s"], 1),
-        "roofline": {"bound": "mfma", "achieved": round(bach, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(bach / PEAK_BF16_TFLOPS, 4),
-                     "algorithmic_flops": bflops, "executed_flops": 16 * w.T * w.r * w.M
-                     + 6 * w.T * w.r * w.h}}
-    del trr, tro, bwd, sel
+    if not args.no_backward:
+        result["backward"] = backward_leg(w, dev, router, trr, bufs, nbuf, args)
+    del trr
     torch.cuda.empty_cache()
 
     if not args.no_fullrank:
