@@ -654,15 +654,19 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
     const int64_t q0 = c * kBwChunk;
     const int cnt = (int)min((int64_t)kBwChunk, nv - q0);
     if (cnt <= 0) return;  // wave-uniform
-    int32_t pl = 0, el = 0;
+    int32_t pl = 0, el = 0, o0l = 0, o1l = 1;
     float vl = 0.0f;
     if (lane < cnt) {
         pl = sorted[q0 + lane];
         el = idx[pl];
         vl = dtop[pl];
+        o0l = offsets[el];  // the entry's expert range, loaded for all entries at once
+        o1l = offsets[el + 1];
     }
-    auto flush = [&](int32_t e, float acc) __attribute__((always_inline)) {
-        const int64_t o0 = offsets[e], o1 = offsets[e + 1];
+    // run ending at entry u (its expert's range read from lane u)
+    auto flush = [&](int32_t e, int u, float acc) __attribute__((always_inline)) {
+        const int64_t o0 = __builtin_amdgcn_readlane(o0l, u);
+        const int64_t o1 = __builtin_amdgcn_readlane(o1l, u);
         const int64_t c0 = o0 / kBwChunk, c1 = (o1 - 1) / kBwChunk;
         if (lane < r) {
             if (c0 == c1)
@@ -690,7 +694,7 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
         for (int q = 0; q < 8; ++q) {
             if (u0 + q < cnt) {
                 if (ev[q] != cur) {
-                    flush(cur, acc);
+                    flush(cur, u0 + q - 1, acc);
                     cur = ev[q];
                     acc = 0.0f;
                 }
@@ -698,7 +702,7 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
             }
         }
     }
-    flush(cur, acc);
+    flush(cur, cnt - 1, acc);
 }
 
 // dR2t[e][j] = the P partials in order, then the dtop terms of bwd_sparse (in chunk order for an
