@@ -37,6 +37,7 @@
 
 #include "device_common.h"
 #include "lowrank.h"
+#include "backward.h"
 
 namespace more {
 

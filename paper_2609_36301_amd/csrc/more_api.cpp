@@ -6,6 +6,7 @@
 
 #include "more.h"
 #include "lowrank.h"
+#include "backward.h"
 
 namespace {
 
