@@ -48,8 +48,11 @@ constexpr float kBwNoToken = -0x1p100f;  // bias of rows past T: 2^(finite + thi
 
 constexpr int kBwWaves = 8;
 constexpr int kBwThreads = 64 * kBwWaves;
-// 32-token groups per wave in the token-major sweeps (one for the r = 64 dz sweep, whose
-// accumulators would not fit two waves per SIMD otherwise)
+// Waves per workgroup and 32-token groups per wave in the token-major sweeps.  The r = 64 dz
+// sweep holds one token group per wave: two would not fit two waves per SIMD, and one wave per
+// SIMD with two groups (four waves per workgroup, up to 512 registers each) measured 45% slower.
+template <int RC, bool DZ>
+constexpr int bw_waves() { return 8; }
 template <int RC, bool DZ>
 constexpr int bw_tpw() { return (RC == 4 && DZ) ? 1 : 2; }
 constexpr int kBwStageE = 128;   // experts per LDS stage of the token-major sweeps
@@ -119,24 +122,27 @@ __global__ __launch_bounds__(256) void bwd_r1_transpose_kernel(const uint16_t* _
 //   DZ = true : ybar = P (pbar_e - g_t) as bf16 A operands (token rows, expert K order as the
 //               accumulator holds them) against R2^T pieces read from a transposed LDS copy
 //               with the same K order -> dz partials dzpart[(split WE + we)][t][r]
-template <int RC>
+template <int RC, int NW>
 struct TokCfg {
+    static constexpr int THREADS = 64 * NW;
     static constexpr int R = 16 * RC;
     static constexpr int RB = (R + 31) / 32;       // 32-row blocks of the rank axis
     static constexpr int RP = R + 8;               // LDS pitch of an expert row (bf16)
     static constexpr int CP = kBwStageE + 8;       // LDS pitch of a transposed row (bf16)
     static constexpr int PIECES = kBwStageE * R / 8;  // 16-byte pieces of R2t per stage
-    static constexpr int PPT = (PIECES + kBwThreads - 1) / kBwThreads;
+    static constexpr int PPT = (PIECES + THREADS - 1) / THREADS;
 };
 
 template <int RC, bool DZ>
-__global__ __launch_bounds__(kBwThreads, 1) void bwd_tok_kernel(
+__global__ __launch_bounds__((64 * bw_waves<RC, DZ>()), 1) void bwd_tok_kernel(
     const uint16_t* __restrict__ zhl, const float* __restrict__ bias,
     const float* __restrict__ gtok, const float* __restrict__ pbar,
     const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t WT, int32_t splits,
     float* __restrict__ out) {
-    using C = TokCfg<RC>;
+    constexpr int NW = bw_waves<RC, DZ>();
+    using C = TokCfg<RC, NW>;
     constexpr int R = C::R, RB = C::RB, RP = C::RP, CP = C::CP, TPW = bw_tpw<RC, DZ>();
+    constexpr int NT = C::THREADS;
     constexpr int TILES = kBwStageE / 32;
     __shared__ __attribute__((aligned(16))) uint16_t rows[2][kBwStageE * RP];
     __shared__ __attribute__((aligned(16))) uint16_t rowsT[DZ ? 2 : 1][DZ ? R * CP : 8];
@@ -145,7 +151,7 @@ __global__ __launch_bounds__(kBwThreads, 1) void bwd_tok_kernel(
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int n = lane & 31, half = lane >> 5;
-    const int WE = kBwWaves / WT;
+    const int WE = NW / WT;
     const int wt = w % WT, we = w / WT;
     const int32_t split = (int32_t)(blockIdx.x % (unsigned)splits);
     const int64_t tb = blockIdx.x / (unsigned)splits;
@@ -181,7 +187,7 @@ __global__ __launch_bounds__(kBwThreads, 1) void bwd_tok_kernel(
         const int64_t e0 = (int64_t)(tile0 + st * TILES) * 32;
 #pragma unroll
         for (int i = 0; i < C::PPT; ++i) {
-            const int p = tid + i * kBwThreads;
+            const int p = tid + i * NT;
             int64_t e = e0 + p / (R / 8);
             e = e < M ? e : M - 1;  // rows past M: masked out of the sums below
             if (p < C::PIECES)
@@ -195,7 +201,7 @@ __global__ __launch_bounds__(kBwThreads, 1) void bwd_tok_kernel(
     auto stash = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
         for (int i = 0; i < C::PPT; ++i) {
-            const int p = tid + i * kBwThreads;
+            const int p = tid + i * NT;
             if (p < C::PIECES) {
                 const int el = p / (R / 8), q = p % (R / 8);
                 *reinterpret_cast<u32x4*>(&rows[buf][el * RP + 8 * q]) = rg[i];
@@ -917,11 +923,11 @@ bool backward_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, b
     const int64_t Mt = ((int64_t)M + 31) / 32;
     const int64_t Tt = (T + 31) / 32;
     // token-major sweeps: WT token slots per workgroup, about 256 workgroups
-    auto tok_grid = [&](int tpw, TokGrid* g) {
+    auto tok_grid = [&](int nw, int tpw, TokGrid* g) {
         const int64_t slot = 32 * tpw;
         const int64_t slots_needed = (T + slot - 1) / slot;
-        int32_t WT = 8;
-        while (WT > 2 && (int64_t)WT / 2 >= slots_needed) WT /= 2;
+        int32_t WT = nw;  // token slots per workgroup; the WE = nw / WT waves of a slot (<= 4)
+        while (WT > nw / 4 && (int64_t)WT / 2 >= slots_needed) WT /= 2;
         g->WT = WT;
         g->ntb = (T + WT * slot - 1) / (WT * slot);
         int64_t S = (256 + g->ntb - 1) / (g->ntb > 0 ? g->ntb : 1);
@@ -929,12 +935,21 @@ bool backward_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, b
         if (S > stages) S = stages;
         if (S < 1) S = 1;
         g->splits = (int32_t)S;
-        g->parts = (int32_t)(S * (kBwWaves / WT));
+        g->parts = (int32_t)(S * (nw / WT));
     };
     switch (q.RC) {
-        case 1: tok_grid(bw_tpw<1, false>(), &q.gsweep); tok_grid(bw_tpw<1, true>(), &q.dzsweep); break;
-        case 2: tok_grid(bw_tpw<2, false>(), &q.gsweep); tok_grid(bw_tpw<2, true>(), &q.dzsweep); break;
-        default: tok_grid(bw_tpw<4, false>(), &q.gsweep); tok_grid(bw_tpw<4, true>(), &q.dzsweep); break;
+        case 1:
+            tok_grid(bw_waves<1, false>(), bw_tpw<1, false>(), &q.gsweep);
+            tok_grid(bw_waves<1, true>(), bw_tpw<1, true>(), &q.dzsweep);
+            break;
+        case 2:
+            tok_grid(bw_waves<2, false>(), bw_tpw<2, false>(), &q.gsweep);
+            tok_grid(bw_waves<2, true>(), bw_tpw<2, true>(), &q.dzsweep);
+            break;
+        default:
+            tok_grid(bw_waves<4, false>(), bw_tpw<4, false>(), &q.gsweep);
+            tok_grid(bw_waves<4, true>(), bw_tpw<4, true>(), &q.dzsweep);
+            break;
     }
     // expert-major sweep: expert blocks of 32 NE waves tiles, about 512 workgroups
     const int64_t per_block = 32 * kBwNE * kBwWaves;
@@ -994,11 +1009,11 @@ static void launch_balance(const BackwardPlan& p, const BackwardArgs& a, char* w
     const TokGrid& G = p.gsweep;
     const TokGrid& D = p.dzsweep;
     hipLaunchKernelGGL((bwd_tok_kernel<RC, false>), dim3((unsigned)(G.ntb * G.splits)),
-                       dim3(kBwThreads), 0, st, zhl, bias, nullptr, a.pbar, a.R2t, a.T, a.M, G.WT,
+                       dim3(64 * bw_waves<RC, false>()), 0, st, zhl, bias, nullptr, a.pbar, a.R2t, a.T, a.M, G.WT,
                        G.splits, gpart);
     launch_colsum(gpart, G.parts, a.T, g, st);
     hipLaunchKernelGGL((bwd_tok_kernel<RC, true>), dim3((unsigned)(D.ntb * D.splits)),
-                       dim3(kBwThreads), 0, st, zhl, bias, g, a.pbar, a.R2t, a.T, a.M, D.WT,
+                       dim3(64 * bw_waves<RC, true>()), 0, st, zhl, bias, g, a.pbar, a.R2t, a.T, a.M, D.WT,
                        D.splits, dzpart);
     launch_colsum(dzpart, D.parts, (int64_t)a.T * a.r, dzsum, st);
     hipLaunchKernelGGL((bwd_exp_kernel<RC>), dim3((unsigned)((int64_t)p.eblocks * p.esplits)),
