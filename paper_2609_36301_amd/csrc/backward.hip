@@ -685,28 +685,25 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
     int32_t cur = __builtin_amdgcn_readfirstlane(el);
     float acc = 0.0f;
     const int32_t vbits = __builtin_bit_cast(int32_t, vl);
-    for (int u0 = 0; u0 < cnt; u0 += 8) {
-        // the z rows of eight entries in flight, then the entries in order
-        int32_t ev[8];
-        float vv[8], zv[8];
+    // the z rows of all the chunk's entries in flight at once (lane j < r: column j), then the
+    // entries in order
+    float zv[kBwChunk];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int u = min(u0 + q, cnt - 1);
-            ev[q] = __builtin_amdgcn_readlane(el, u);
-            const int32_t p = __builtin_amdgcn_readlane(pl, u);
-            vv[q] = __builtin_bit_cast(float, __builtin_amdgcn_readlane(vbits, u));
-            zv[q] = lane < r ? z[(int64_t)(p / k) * r + lane] : 0.0f;
-        }
+    for (int u = 0; u < kBwChunk; ++u) {
+        const int32_t p = __builtin_amdgcn_readlane(pl, u);  // 0 past cnt: a valid row
+        zv[u] = lane < r ? z[(int64_t)(p / k) * r + lane] : 0.0f;
+    }
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            if (u0 + q < cnt) {
-                if (ev[q] != cur) {
-                    flush(cur, u0 + q - 1, acc);
-                    cur = ev[q];
-                    acc = 0.0f;
-                }
-                acc += vv[q] * zv[q];
+    for (int u = 0; u < kBwChunk; ++u) {
+        if (u < cnt) {
+            const int32_t e = __builtin_amdgcn_readlane(el, u);
+            const float v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(vbits, u));
+            if (e != cur) {
+                flush(cur, u - 1, acc);
+                cur = e;
+                acc = 0.0f;
             }
+            acc += v * zv[u];
         }
     }
     flush(cur, cnt - 1, acc);
