@@ -152,6 +152,7 @@ SHAPES = [
     (128, 256, 64, 9000, 16),    # decode-like: two token slots per workgroup
     (130, 128, 64, 2100, 8),     # one token past a slot boundary
     (2000, 128, 64, 20000, 8),   # many expert splits
+    (300, 64, 32, 500, 32),      # k = 32 (the backward's limit)
 ]
 
 
@@ -253,3 +254,40 @@ def test_backward_full_workload_sampled(wl):
     print("[backward] %s trace identity: %.6g %.6g %.6g (bound %.3g)" % (wl, tx_, t1, t2, bound),
           flush=True)
     assert abs(tx_ - t1) <= bound and abs(tx_ - t2) <= bound
+
+
+def test_backward_graph_replays_match_eager():
+    """Two backward calls (with and without the balancing term) captured in one HIP graph; every
+    replay, with the outputs scribbled over and eager work in between, equals the eager result."""
+    torch = require_gpu()
+    from paper_2609_36301_amd import router
+    cases = []
+    for T, h, r, M, k, bal in [(700, 256, 64, 5000, 8, True), (300, 128, 32, 3000, 4, False)]:
+        inp = make_inputs(T, h, r, M, seed=T + 1)
+        idx, dtop, pbar, m, Z = _grad_inputs(inp, k, seed=T, balance=bal)
+        R1t, R2t = transposed_factors(inp)
+        dev = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(a)).cuda()
+        args = (to_dev(inp.x), to_dev(R1t), to_dev(R2t), dev(idx), dev(dtop), dev(pbar), dev(m),
+                dev(Z))
+        b = router.LowrankBackward(T, h, r, M, k, balance=bal)
+        announce("backward graph eager T=%d M=%d balance=%d" % (T, M, bal))
+        o = b(*args)
+        torch.cuda.synchronize()
+        cases.append((b, args, [t.clone() for t in (o.dx, o.dR1t, o.dR2t)]))
+    announce("backward graph capture")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for b, args, _ in cases:
+            b(*args)
+    for rep in range(3):
+        for b, _, _ in cases:
+            for t in (b.out.dx, b.out.dR1t, b.out.dR2t):
+                t.fill_(-7.0)
+        torch.cuda.synchronize()
+        announce("backward graph replay %d" % rep)
+        g.replay()
+        torch.cuda.synchronize()
+        for b, _, ref in cases:
+            for got, want in zip((b.out.dx, b.out.dR1t, b.out.dR2t), ref):
+                assert torch.equal(got, want), "replay %d differs from eager" % rep
+        _ = torch.ones(1000, device="cuda").sum().item()  # eager work between replays
