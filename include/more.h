@@ -12,6 +12,12 @@
  * of the M experts; the softmax runs over those k logits only.  The T x M logit matrix is
  * never written to memory (Appendix "Pseudocode", inference algorithm).
  *
+ * Calls: the routing (more_route_lowrank and its variants), the training forward pass with the
+ * softmax statistics (more_route_lowrank_train), the training backward pass
+ * (more_route_lowrank_backward), the full-rank baselines (more_route_fullrank,
+ * more_route_fullrank_fused), the per-expert histogram and the dispatch bookkeeping
+ * (more_dispatch_sort).
+ *
  * Conventions shared by every call
  * --------------------------------
  *  - Element types: bfloat16 inputs are passed as uint16_t bit patterns.  Accumulation is
@@ -30,8 +36,9 @@
  *    execution surface at the caller's next synchronisation.
  *  - Arguments are validated on the host before anything is launched; an error status means
  *    nothing was enqueued.  T == 0 returns MORE_OK without launching (apart from clearing
- *    the per-expert outputs counts and psum); the token-sized pointers (x, idx, gate, topval,
- *    m, Z) may then be NULL.
+ *    the per-expert outputs counts and psum, and the weight gradients dR1t and dR2t of the
+ *    backward pass); the token-sized pointers (x, idx, gate, topval, m, Z, dtop, dx) may then
+ *    be NULL.
  *  - Selection order: experts are ranked by logit, larger first; equal logits are ranked by
  *    expert id, smaller first.  idx[t][0..k-1] lists the selected experts in that order.
  *    (The paper's buffer leaves both the slot order and tie handling open; this total
