@@ -8,19 +8,21 @@
 // and no T x M matrix is written: the logits are recomputed tile by tile on the matrix cores.
 //
 // Kernels of one call (the balancing kernels run only when pbar is given):
-//   zonly           z = x R1 (fp32, the z pass of the routing call)
-//   bwd_prep        z' = z log2(e) as bf16 hi/lo rows, bf16(z) rows, the token bias
-//                   -(m log2(e) + log2 Z), and R1 transposed to [h][r]
-//   bwd_tok<false>  sweep 1, token-major: per (expert split, token) sum_e pbar_e P_te
-//   bwd_sum         g = the split sums in split order
-//   bwd_tok<true>   sweep 2, token-major: ybar tile by tile, dz partials per expert split
-//   bwd_dz          dz = partials in order + the selected experts' dtop R2 rows; dz as bf16
-//                   hi/lo rows [T][2r] and as transposed hi/lo rows [2][r][T]
-//   bwd_exp         sweep 2 again, expert-major: ybar tile by tile, dR2 partials per token split
-//   dispatch        the selections sorted by expert (Sort + Count kernels)
-//   bwd_dr2         dR2 = partials in order + dtop z of each expert's selections in order
-//   bwd_dx          dx = dz R1^T (dz as hi + lo)
-//   bwd_dr1 + sum   dR1 = x^T dz over token splits, summed in split order
+//   zonly            z = x R1 (fp32, the z pass of the routing call)
+//   bwd_prep         z' = z log2(e) as bf16 hi/lo rows, bf16(z) rows and the token bias
+//                    -(m log2(e) + log2 Z); bwd_r1_transpose: R1 as [h][r]
+//   bwd_tok<false>   sweep 1, token-major: per (expert split, token) sum_e pbar_e P_te
+//   bwd_colsum       g = the split sums in split order
+//   bwd_tok<true>    sweep 2, token-major: ybar tile by tile, dz partials per expert split,
+//                    summed by bwd_colsum
+//   bwd_exp          sweep 2 again, expert-major: ybar tile by tile, dR2 partials per token split
+//   dispatch         the selections sorted by expert (Sort + Count kernels)
+//   bwd_sparse       the dtop z terms of dR2, a segmented sum over chunks of the sorted selections
+//   bwd_dr2          dR2 = partials in order + the dtop terms
+//   bwd_dz           dz = the dense sum + the selected experts' dtop R2 rows; dz as bf16 hi/lo rows
+//                    [T][2r] and as transposed hi/lo rows [2][r][T]
+//   bwd_dx           dx = dz R1^T (dz as hi + lo)
+//   bwd_dr1          dR1 = x^T dz over token splits, summed by bwd_colsum in split order
 // The paper's algorithm computes dz and dR2 in one sweep per token block and lets token blocks
 // add into dR2; here two sweeps (one token-major, one expert-major) each own their output, so
 // nothing is added atomically and every sum runs in a fixed order: a shape gives the same bits
