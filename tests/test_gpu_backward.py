@@ -225,35 +225,73 @@ def test_backward_full_workload(wl):
     _check_full(inp, *ins, got, wl)
 
 
+def _dr2_tolerance_cols(inp, cols, idx, dtop, pbar, m, Z, g):
+    """The dR2 bound of the module docstring for the expert columns `cols` over all tokens, with
+    A_t and S_t both replaced by their upper bound sum_i |z_ti| max_e |u_ie| (no T x M work)."""
+    T, h, r, M = inp.shape
+    k = idx.shape[1]
+    xf, R1, R2 = f64(inp.x), f64(inp.R1), f64(inp.R2)
+    tol = np.zeros((r, cols.size))
+    colpos = {int(e): c for c, e in enumerate(cols)}
+    umax = np.abs(R2).max(axis=1)
+    for t0 in range(0, T, 2048):
+        z = xf[t0:t0 + 2048] @ R1
+        az = np.abs(z)
+        Sb = az @ umax
+        mm, ZZ = m[t0:t0 + 2048].astype(np.float64), Z[t0:t0 + 2048].astype(np.float64)
+        d = (1e-4 * (1 + Sb) + 2.0 ** -18 * Sb + (2 * r + 1) * 2.0 ** -24 * 2 * Sb
+             + 2.0 ** -21 * (np.abs(mm) + np.abs(np.log(ZZ)) + 1))
+        D = np.expm1(d) + 2.0 ** -22
+        lg = z @ R2[:, cols]
+        P = np.exp(lg - mm[:, None]) / ZZ[:, None]
+        dev_ = pbar.astype(np.float64)[cols][None, :] - g[t0:t0 + 2048][:, None]
+        # |dg_t| needs G_t = sum_e |pbar_e| P_te over all experts; sum_e P_te = 1 bounds it
+        G = np.abs(pbar).max() * np.ones_like(Sb)
+        dg = 1.01 * (D + 2.0 ** -24 * (M + k + 1100)) * G
+        yd = P * dev_
+        E = P * (np.abs(dev_) * (D + 2.0 ** -8)[:, None] + 1.02 * dg[:, None])
+        y = yd.copy()
+        for q in range(k):
+            e = idx[t0:t0 + 2048, q]
+            for row in np.nonzero(np.isin(e, cols))[0]:
+                y[row, colpos[int(e[row])]] += float(dtop[t0 + row, q])
+        ez = (h + 64) * 2.0 ** -24 * (np.abs(xf[t0:t0 + 2048]) @ np.abs(R1))
+        tol += (az.T @ (E * (1 + 2.0 ** -8) + 2.0 ** -8 * np.abs(yd)) + ez.T @ np.abs(y)
+                + 1.1 * 2.0 ** -24 * (T + 1100) * (az.T @ np.abs(y)))
+    return tol
+
+
 @pytest.mark.parametrize("wl", ["mid", "fine_grained"])
 def test_backward_full_workload_sampled(wl):
-    """dx on sampled tokens (the oracle on those tokens alone: every per-token quantity depends
-    on the token's own row only), and the trace identity <dx, x> = <dR1, R1> = <dR2, R2> over
-    the whole batch, bounded by 2^-6 sum_t A_t (2 max |pbar| + sum_j |dtop_tj|)."""
+    """The oracle on the whole batch; dx on 64 sampled tokens and dR2 on 64 sampled experts
+    (first, last and the most selected among them) element by element, and the trace identity
+    <dx, x> = <dR1, R1> = <dR2, R2> over the whole batch, bounded by
+    2^-6 sum_t A_t (2 max |pbar| + sum_j |dtop_tj|)."""
     inp = make_workload_inputs(wl)
     T, h, r, M = inp.shape
     k = WORKLOADS[wl].k
     idx, dtop, pbar, m, Z = _grad_inputs(inp, k, seed=8, selection="synthetic")
     got = _run(inp, idx, dtop, pbar, m, Z, tag=wl)
+    f = lambda a: a.astype(np.float64)
+    ref = oracle.route_backward(inp.x, inp.R1, inp.R2, idx, f(dtop), f(pbar), f(m), f(Z))
     rng = np.random.default_rng(9)
     rows = np.unique(np.concatenate([[0, T - 1], rng.integers(0, T, 62)]))
-    sub = make_inputs(rows.size, h, r, M, seed=0)
-    sub.x, sub.R1, sub.R2 = inp.x[rows], inp.R1, inp.R2
-    f = lambda a: a.astype(np.float64)
-    ref = oracle.route_backward(sub.x, sub.R1, sub.R2, idx[rows], f(dtop[rows]), f(pbar),
-                                f(m[rows]), f(Z[rows]))
-    tx, _, _ = _tolerances(sub, idx[rows], dtop[rows], pbar, m[rows], Z[rows], ref.g, ref.dz)
-    _compare("dx (sampled rows)", got["dx"][rows], ref.dx, tx, wl)
+    tx, _, _ = _tolerances(inp, idx, dtop, pbar, m, Z, ref.g, ref.dz, rows=rows)
+    _compare("dx (sampled rows)", got["dx"][rows], ref.dx[rows], tx, wl)
+    hot = int(np.bincount(idx.ravel(), minlength=M).argmax())
+    cols = np.unique(np.concatenate([[0, M - 1, hot], rng.integers(0, M, 61)]))
+    t2 = _dr2_tolerance_cols(inp, cols, idx, dtop, pbar, m, Z, ref.g)
+    _compare("dR2 (sampled experts)", got["dR2t"][cols].T, ref.dR2[:, cols], t2, wl)
     xf, R1, R2 = f64(inp.x), f64(inp.R1), f64(inp.R2)
     tx_ = np.sum(got["dx"] * xf)
     t1 = np.sum(got["dR1t"].T * R1)
-    t2 = np.sum(got["dR2t"].T * R2)
+    t2s = np.sum(got["dR2t"].T * R2)
     z = xf @ R1
     A = np.abs(z) @ np.abs(R2).max(axis=1)
     bound = 2.0 ** -6 * np.sum(A * (2 * np.abs(pbar).max() + np.abs(dtop).sum(axis=1)))
-    print("[backward] %s trace identity: %.6g %.6g %.6g (bound %.3g)" % (wl, tx_, t1, t2, bound),
+    print("[backward] %s trace identity: %.6g %.6g %.6g (bound %.3g)" % (wl, tx_, t1, t2s, bound),
           flush=True)
-    assert abs(tx_ - t1) <= bound and abs(tx_ - t2) <= bound
+    assert abs(tx_ - t1) <= bound and abs(tx_ - t2s) <= bound
 
 
 def test_backward_graph_replays_match_eager():
