@@ -14,7 +14,8 @@
 //                         digits (a 256-wide scan in LDS) plus the digit's block prefix.
 // dsort_offsets_kernel derives offsets from the sorted keys: offsets[e] = the first slot whose
 // key is at least e.  Up to 4096 entries (decode-sized batches) one workgroup runs all passes in
-// LDS instead (dsort_small_kernel).
+// LDS instead (dsort_small_kernel); with at most 8191 experts one counting pass replaces the
+// radix passes (dsort_whist, dsort_scan, dsort_wscatter).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -155,6 +156,103 @@ __global__ __launch_bounds__(kDsThreads) void dsort_scatter_kernel(
             if (keys_out) keys_out[dest] = key[r];
             vals_out[dest] = val[r];
         }
+    }
+}
+
+// ------------------------------------------------------------------------------ one pass
+// Keys 0 .. M with M + 1 <= kDsWideBins (up to 8191 experts) need one counting pass instead of two
+// radix passes: per-block key counts, the scan of each key's block counts (dsort_scan_kernel
+// with one workgroup per key), and a scatter that also writes the offsets.
+constexpr int kDsWideBins = 8192;
+constexpr int kDsWideBits = 13;
+
+// Key counts of block b: hist[key * nblocks + b].
+__global__ __launch_bounds__(kDsThreads) void dsort_whist_kernel(const int32_t* __restrict__ idx,
+                                                                 int64_t N, int32_t M,
+                                                                 int32_t* __restrict__ hist) {
+    __shared__ int32_t cnt[kDsWideBins];
+    const int tid = threadIdx.x;
+    const int D = M + 1;
+    for (int i = tid; i < D; i += kDsThreads) cnt[i] = 0;
+    __syncthreads();
+    const int64_t b0 = (int64_t)blockIdx.x * kDsBlock;
+    for (int r = 0; r < kDsRounds; ++r) {
+        const int64_t g = b0 + r * kDsThreads + tid;
+        if (g < N) atomicAdd(&cnt[ds_key(idx[g], M)], 1);
+    }
+    __syncthreads();
+    for (int i = tid; i < D; i += kDsThreads) hist[(int64_t)i * gridDim.x + blockIdx.x] = cnt[i];
+}
+
+// Block b: base[key] = entries with a smaller key (the exclusive scan of the key totals, in LDS;
+// block 0 writes it as the offsets) plus the block's prefix of the key (start, scanned per key),
+// then one wave places the block's entries in entry order: in each group of 64, a lane's rank
+// among the lanes with its key (13 ballots) is added to base[key], and the group's first lane of
+// each key advances base[key] by the group's count of that key.
+__global__ __launch_bounds__(kDsThreads) void dsort_wscatter_kernel(
+    const int32_t* __restrict__ idx, int64_t N, int32_t M, const int32_t* __restrict__ start,
+    const int32_t* __restrict__ total, int32_t* __restrict__ sorted,
+    int32_t* __restrict__ offsets) {
+    constexpr int PER = kDsWideBins / kDsThreads;  // keys per thread in the scan
+    __shared__ int32_t base[kDsWideBins];
+    __shared__ int32_t part[kDsThreads];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int D = M + 1;
+    int32_t v[PER];
+    int32_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        const int key = PER * tid + i;
+        v[i] = key < D ? total[key] : 0;
+        sum += v[i];
+    }
+    part[tid] = sum;
+    __syncthreads();
+    for (int d = 1; d < kDsThreads; d <<= 1) {  // inclusive scan of the threads' sums
+        const int32_t u = tid >= d ? part[tid - d] : 0;
+        __syncthreads();
+        part[tid] += u;
+        __syncthreads();
+    }
+    int32_t run = part[tid] - sum;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+        base[PER * tid + i] = run;
+        run += v[i];
+    }
+    __syncthreads();
+    if (blockIdx.x == 0)
+        for (int e = tid; e <= M; e += kDsThreads) offsets[e] = base[e];
+    for (int key = tid; key < D; key += kDsThreads)
+        base[key] += start[(int64_t)key * gridDim.x + blockIdx.x];
+    __syncthreads();
+    if (tid >= 64) return;  // wave-uniform: wave 0 places the entries
+    constexpr int NG = kDsBlock / 64;
+    const int64_t b0 = (int64_t)blockIdx.x * kDsBlock;
+    const uint64_t below = (1ull << lane) - 1ull;
+    int32_t keys[NG];
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {
+        const int64_t g = b0 + gi * 64 + lane;
+        keys[gi] = g < N ? ds_key(idx[g], M) : 0;
+    }
+#pragma unroll
+    for (int gi = 0; gi < NG; ++gi) {
+        const int64_t g = b0 + gi * 64 + lane;
+        const bool ok = g < N;
+        const int d = keys[gi];
+        uint64_t peers = __ballot(ok);
+#pragma unroll
+        for (int bit = 0; bit < kDsWideBits; ++bit) {
+            const uint64_t m = __ballot((d >> bit) & 1);
+            peers &= ((d >> bit) & 1) ? m : ~m;
+        }
+        const uint64_t before = peers & below;
+        // every lane reads base[d] before the group's first lane of each key advances it (one
+        // wave: its LDS operations complete in order)
+        const int32_t slot = base[d] + __popcll(before);
+        if (ok && before == 0) base[d] += __popcll(peers);
+        if (ok && slot < N) sorted[slot] = (int32_t)g;
     }
 }
 
@@ -302,7 +400,8 @@ size_t dispatch_workspace_bytes(int64_t N) {
     if (N == 0) return 0;
     const int64_t nblocks = (N + kDsBlock - 1) / kDsBlock;
     auto al = [](size_t b) { return (b + 255) & ~(size_t)255; };
-    return 4 * al((size_t)N * 4) + al((size_t)nblocks * kDsDigits * 4) + al(kDsDigits * 4);
+    // room for the key counts of the one-pass sort (kDsWideBins >= kDsDigits)
+    return 4 * al((size_t)N * 4) + al((size_t)nblocks * kDsWideBins * 4) + al(kDsWideBins * 4);
 }
 
 hipError_t dispatch_launch(const int32_t* idx, int64_t N, int32_t M, int32_t* offsets,
@@ -323,6 +422,18 @@ hipError_t dispatch_launch(const int32_t* idx, int64_t N, int32_t M, int32_t* of
                            (int32_t)N, M, dispatch_passes(M), keys, sorted);
         hipLaunchKernelGGL(dsort_offsets_kernel, dim3(oblocks), dim3(256), 0, st, keys, N, M,
                            offsets);
+        return hipGetLastError();
+    }
+    if ((int64_t)M + 1 <= kDsWideBins) {  // one counting pass: three launches
+        int32_t* hist = reinterpret_cast<int32_t*>(ws + 4 * al((size_t)N * 4));
+        int32_t* total = reinterpret_cast<int32_t*>(ws + 4 * al((size_t)N * 4) +
+                                                    al((size_t)nblocks * kDsWideBins * 4));
+        hipLaunchKernelGGL(dsort_whist_kernel, dim3((unsigned)nblocks), dim3(kDsThreads), 0, st,
+                           idx, N, M, hist);
+        hipLaunchKernelGGL(dsort_scan_kernel, dim3((unsigned)(M + 1)), dim3(kDsThreads), 0, st,
+                           hist, nblocks, total);
+        hipLaunchKernelGGL(dsort_wscatter_kernel, dim3((unsigned)nblocks), dim3(kDsThreads), 0, st,
+                           idx, N, M, hist, total, sorted, offsets);
         return hipGetLastError();
     }
     int32_t* keys[2] = {reinterpret_cast<int32_t*>(ws), reinterpret_cast<int32_t*>(ws + al((size_t)N * 4))};

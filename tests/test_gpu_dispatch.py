@@ -43,7 +43,10 @@ def _skewed(T, k, M, seed):
 
 
 @pytest.mark.parametrize("T,k,M", [(256, 8, 200), (256, 8, 256), (1001, 3, 5000),
-                                   (4096, 4, 70000)],
+                                   (4096, 4, 70000),
+                                   # one counting pass (more than 4096 entries, M + 1 <= 8192)
+                                   (16384, 8, 4096), (3000, 7, 8191), (20000, 3, 1),
+                                   (1100, 4, 300), (5000, 2, 8192)],
                          ids=lambda v: str(v))
 def test_random_ids(T, k, M):
     rng = np.random.default_rng(T + M)
@@ -55,6 +58,17 @@ def test_ids_outside_the_range_go_last():
     idx = rng.integers(-5, 120, size=(777, 5)).astype(np.int32)
     idx[::7, 0] = 2 ** 31 - 1
     _check(idx, 100, "invalid ids")
+
+
+def test_ids_outside_the_range_go_last_one_pass():
+    rng = np.random.default_rng(4)
+    idx = rng.integers(-3, 2000, size=(3000, 6)).astype(np.int32)
+    idx[::5, 2] = 2 ** 31 - 1
+    _check(idx, 1990, "outside, one pass")
+
+
+def test_teaser_sized_skew_one_pass():
+    _check(_skewed(16384, 8, 4096, seed=5), 4096, "skewed teaser")
 
 
 def test_one_expert_takes_every_entry():
