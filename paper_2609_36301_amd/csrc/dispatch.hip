@@ -185,19 +185,28 @@ __global__ __launch_bounds__(kDsThreads) void dsort_whist_kernel(const int32_t* 
 }
 
 // Block b: base[key] = entries with a smaller key (the exclusive scan of the key totals, in LDS;
-// block 0 writes it as the offsets) plus the block's prefix of the key (start, scanned per key),
-// then one wave places the block's entries in entry order: in each group of 64, a lane's rank
-// among the lanes with its key (13 ballots) is added to base[key], and the group's first lane of
-// each key advances base[key] by the group's count of that key.
+// block 0 writes it as the offsets) plus the block's prefix of the key (start, scanned per key).
+// Wave w then places entries 256 w .. 256 w + 255 of the block in entry order.  The waves' counts
+// of each key, 16-bit fields packed two to a word (waves 0 and 1 in wc[0], 2 and 3 in wc[1]), are
+// turned into each wave's exclusive prefix over the earlier waves; in each group of 64 a lane's
+// slot is base[key] + its wave's field + its rank among the group's lanes with that key (13
+// ballots), and the group's first lane of each key advances the wave's field by the group's count
+// of that key (an atomic add on the word, so the other half is never overwritten).
 __global__ __launch_bounds__(kDsThreads) void dsort_wscatter_kernel(
     const int32_t* __restrict__ idx, int64_t N, int32_t M, const int32_t* __restrict__ start,
     const int32_t* __restrict__ total, int32_t* __restrict__ sorted,
     int32_t* __restrict__ offsets) {
     constexpr int PER = kDsWideBins / kDsThreads;  // keys per thread in the scan
+    constexpr int WG = kDsRounds;                  // groups of 64 per wave (256 entries)
     __shared__ int32_t base[kDsWideBins];
+    __shared__ uint32_t wc[2][kDsWideBins];
     __shared__ int32_t part[kDsThreads];
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int D = M + 1;
+    for (int i = tid; i < D; i += kDsThreads) {
+        wc[0][i] = 0u;
+        wc[1][i] = 0u;
+    }
     int32_t v[PER];
     int32_t sum = 0;
 #pragma unroll
@@ -225,19 +234,28 @@ __global__ __launch_bounds__(kDsThreads) void dsort_wscatter_kernel(
         for (int e = tid; e <= M; e += kDsThreads) offsets[e] = base[e];
     for (int key = tid; key < D; key += kDsThreads)
         base[key] += start[(int64_t)key * gridDim.x + blockIdx.x];
-    __syncthreads();
-    if (tid >= 64) return;  // wave-uniform: wave 0 places the entries
-    constexpr int NG = kDsBlock / 64;
-    const int64_t b0 = (int64_t)blockIdx.x * kDsBlock;
-    const uint64_t below = (1ull << lane) - 1ull;
-    int32_t keys[NG];
+    // the wave's keys, and its count of each key
+    const int64_t b0 = (int64_t)blockIdx.x * kDsBlock + (int64_t)w * 64 * WG;
+    const uint32_t one = 1u << (16 * (w & 1));
+    int32_t keys[WG];
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {
+    for (int gi = 0; gi < WG; ++gi) {
         const int64_t g = b0 + gi * 64 + lane;
         keys[gi] = g < N ? ds_key(idx[g], M) : 0;
+        if (g < N) atomicAdd(&wc[w >> 1][keys[gi]], one);
     }
+    __syncthreads();
+    for (int key = tid; key < D; key += kDsThreads) {  // per wave: the counts of earlier waves
+        const uint32_t a = wc[0][key], c = wc[1][key];
+        const uint32_t c0 = a & 0xFFFFu, c1 = a >> 16, c2 = c & 0xFFFFu;
+        wc[0][key] = (c0 << 16);
+        wc[1][key] = (c0 + c1) | ((c0 + c1 + c2) << 16);
+    }
+    __syncthreads();
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int sh = 16 * (w & 1);
 #pragma unroll
-    for (int gi = 0; gi < NG; ++gi) {
+    for (int gi = 0; gi < WG; ++gi) {
         const int64_t g = b0 + gi * 64 + lane;
         const bool ok = g < N;
         const int d = keys[gi];
@@ -248,10 +266,12 @@ __global__ __launch_bounds__(kDsThreads) void dsort_wscatter_kernel(
             peers &= ((d >> bit) & 1) ? m : ~m;
         }
         const uint64_t before = peers & below;
-        // every lane reads base[d] before the group's first lane of each key advances it (one
-        // wave: its LDS operations complete in order)
-        const int32_t slot = base[d] + __popcll(before);
-        if (ok && before == 0) base[d] += __popcll(peers);
+        // every lane reads its wave's field before the group's first lane of each key advances
+        // it (one wave: its LDS operations complete in order; the other wave of the word only
+        // adds to its own field)
+        const int32_t slot =
+            base[d] + (int32_t)((wc[w >> 1][d] >> sh) & 0xFFFFu) + __popcll(before);
+        if (ok && before == 0) atomicAdd(&wc[w >> 1][d], (uint32_t)__popcll(peers) << sh);
         if (ok && slot < N) sorted[slot] = (int32_t)g;
     }
 }
