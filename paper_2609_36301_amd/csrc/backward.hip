@@ -654,6 +654,7 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
                                                          const float* __restrict__ dtop,
                                                          const float* __restrict__ z, int32_t k,
                                                          int32_t r, int32_t M, int64_t nchunks,
+                                                         int32_t accumulate,
                                                          float* __restrict__ dR2t,
                                                          float* __restrict__ bpart) {
     const int lane = threadIdx.x & 63;
@@ -678,9 +679,10 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
         const int64_t o1 = __builtin_amdgcn_readlane(o1l, u);
         const int64_t c0 = o0 / kBwChunk, c1 = (o1 - 1) / kBwChunk;
         if (lane < r) {
-            if (c0 == c1)
-                dR2t[(int64_t)e * r + lane] = acc;
-            else
+            if (c0 == c1) {
+                float* o = dR2t + (int64_t)e * r + lane;
+                *o = accumulate ? *o + acc : acc;
+            } else
                 bpart[(c * 2 + (c == c0 ? 1 : 0)) * r + lane] = acc;
         }
     };
@@ -712,7 +714,10 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
 }
 
 // dR2t[e][j] = the P partials in order, then the dtop terms of bwd_sparse (in chunk order for an
-// expert spanning chunks).  One thread per element.
+// expert spanning chunks).  One thread per element.  With one token split the expert-major sweep
+// writes dR2t itself and bwd_sparse adds the sums of the experts inside one chunk to it
+// (accumulate = 1); bwd_dr2_fix then adds the chunk sums of the experts spanning chunks, in the
+// same order of operations.
 __global__ __launch_bounds__(256) void bwd_dr2_kernel(const float* __restrict__ part, int32_t P,
                                                       const int32_t* __restrict__ offsets,
                                                       const float* __restrict__ bpart, int32_t M,
@@ -743,6 +748,24 @@ __global__ __launch_bounds__(256) void bwd_dr2_kernel(const float* __restrict__ 
         }
     }
     dR2t[i] = s;
+}
+
+__global__ __launch_bounds__(256) void bwd_dr2_fix_kernel(const int32_t* __restrict__ offsets,
+                                                          const float* __restrict__ bpart,
+                                                          int32_t M, int32_t r,
+                                                          float* __restrict__ dR2t) {
+    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;  // one thread per expert
+    if (e >= M) return;
+    const int64_t o0 = offsets[e], o1 = offsets[e + 1];
+    if (o1 <= o0) return;
+    const int64_t c0 = o0 / kBwChunk, c1 = (o1 - 1) / kBwChunk;
+    if (c0 == c1) return;  // added by bwd_sparse
+    for (int32_t j = 0; j < r; ++j) {  // rare: experts whose selections span chunks
+        float s = dR2t[e * r + j];
+        s += bpart[(c0 * 2 + 1) * r + j];
+        for (int64_t c = c0 + 1; c <= c1; ++c) s += bpart[(c * 2) * r + j];
+        dR2t[e * r + j] = s;
+    }
 }
 
 // ------------------------------------------------------------------------------ dx
@@ -982,7 +1005,7 @@ bool backward_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, b
     q.off_dzhl = take((size_t)T * 2 * r * 2);
     q.off_dzT = take((size_t)2 * r * q.Tp * 2);
     q.off_r1 = take((size_t)h * r * 2);
-    q.off_r2part = balance ? take((size_t)q.esplits * M * r * 4) : take(0);
+    q.off_r2part = (balance && q.esplits > 1) ? take((size_t)q.esplits * M * r * 4) : take(0);
     q.off_r1part = take((size_t)q.r1splits * r * h * 4);
     q.off_offsets = take(((size_t)M + 1) * 4);
     q.off_sorted = take((size_t)T * k * 4);
@@ -1015,9 +1038,10 @@ static void launch_balance(const BackwardPlan& p, const BackwardArgs& a, char* w
                        dim3(64 * bw_waves<RC, true>()), 0, st, zhl, bias, g, a.pbar, a.R2t, a.T, a.M, D.WT,
                        D.splits, dzpart);
     launch_colsum(dzpart, D.parts, (int64_t)a.T * a.r, dzsum, st);
+    // one token split: the sweep's partials are dR2's dense part, written in place
     hipLaunchKernelGGL((bwd_exp_kernel<RC>), dim3((unsigned)((int64_t)p.eblocks * p.esplits)),
                        dim3(kBwThreads), 0, st, zhl, zb, bias, g, a.pbar, a.R2t, a.T, a.M,
-                       p.eblocks, p.esplits, r2part);
+                       p.eblocks, p.esplits, p.esplits == 1 ? a.dR2t : r2part);
 }
 
 template <int RC>
@@ -1080,12 +1104,18 @@ hipError_t backward_launch(const BackwardPlan& p, const BackwardArgs& a, void* w
     e = dispatch_launch(a.idx, (int64_t)a.T * a.k, a.M, offsets, sorted, ws + p.off_dispatch, st);
     if (e != hipSuccess) return e;
     float* bpart = reinterpret_cast<float*>(ws + p.off_bpart);
+    const bool direct = p.balance && p.esplits == 1;  // dR2t holds the dense part already
     hipLaunchKernelGGL(bwd_sparse_kernel, dim3((unsigned)((p.nchunks + 3) / 4)), dim3(256), 0, st,
-                       sorted, offsets, a.idx, a.dtop, z, a.k, r, a.M, p.nchunks, a.dR2t, bpart);
+                       sorted, offsets, a.idx, a.dtop, z, a.k, r, a.M, p.nchunks,
+                       direct ? 1 : 0, a.dR2t, bpart);
     const int64_t nr2 = (int64_t)a.M * r;
-    hipLaunchKernelGGL(bwd_dr2_kernel, dim3((unsigned)((nr2 + 255) / 256)), dim3(256), 0, st,
-                       reinterpret_cast<const float*>(ws + p.off_r2part),
-                       p.balance ? p.esplits : 0, offsets, bpart, a.M, r, a.dR2t);
+    if (direct)
+        hipLaunchKernelGGL(bwd_dr2_fix_kernel, dim3((unsigned)(((int64_t)a.M + 255) / 256)),
+                           dim3(256), 0, st, offsets, bpart, a.M, r, a.dR2t);
+    else
+        hipLaunchKernelGGL(bwd_dr2_kernel, dim3((unsigned)((nr2 + 255) / 256)), dim3(256), 0, st,
+                           reinterpret_cast<const float*>(ws + p.off_r2part),
+                           p.balance ? p.esplits : 0, offsets, bpart, a.M, r, a.dR2t);
     switch (p.RC) {
         case 1: launch_phase3<1>(p, a, ws, st); break;
         case 2: launch_phase3<2>(p, a, ws, st); break;

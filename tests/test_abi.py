@@ -334,10 +334,10 @@ def test_backward_workspace_size(lib):
         assert lib.more_route_lowrank_backward_workspace_size(T, h, r, M, k, 0,
                                                               ctypes.byref(nb)) == _lib.OK
         # z, z' hi/lo, dz hi/lo twice, the transposed R1 and the sorted selections at least;
-        # the softmax sweeps add their partials of g, dz and dR2
+        # the softmax sweeps add their partials of g and dz (and of dR2 with several token splits)
         base = T * r * 4 + T * r * 4 + 2 * T * r * 4 + h * r * 2 + T * k * 4
         assert nb.value >= base
-        assert n.value >= nb.value + T * 4 + T * r * 4 + M * r * 4
+        assert n.value >= nb.value + T * 4 + T * r * 4
     # without pbar the statistics may be NULL
     assert lib.more_route_lowrank_backward_workspace_size(64, 64, 16, 64, 4, 0,
                                                           ctypes.byref(nb)) == 0

@@ -153,6 +153,8 @@ SHAPES = [
     (130, 128, 64, 2100, 8),     # one token past a slot boundary
     (2000, 128, 64, 20000, 8),   # many expert splits
     (300, 64, 32, 500, 32),      # k = 32 (the backward's limit)
+    (20, 64, 32, 3000, 4),       # one token tile: dR2 written in place by the expert sweep
+    (32, 128, 64, 40000, 8),     # the same with many expert blocks
 ]
 
 
