@@ -673,16 +673,16 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
         o0l = offsets[el];  // the entry's expert range, loaded for all entries at once
         o1l = offsets[el + 1];
     }
-    // run ending at entry u (its expert's range read from lane u)
-    auto flush = [&](int32_t e, int u, float acc) __attribute__((always_inline)) {
+    // run ending at entry u (its expert's range read from lane u; dense: its dR2 row's value when
+    // accumulating)
+    auto flush = [&](int32_t e, int u, float acc, float dense) __attribute__((always_inline)) {
         const int64_t o0 = __builtin_amdgcn_readlane(o0l, u);
         const int64_t o1 = __builtin_amdgcn_readlane(o1l, u);
         const int64_t c0 = o0 / kBwChunk, c1 = (o1 - 1) / kBwChunk;
         if (lane < r) {
-            if (c0 == c1) {
-                float* o = dR2t + (int64_t)e * r + lane;
-                *o = accumulate ? *o + acc : acc;
-            } else
+            if (c0 == c1)
+                dR2t[(int64_t)e * r + lane] = accumulate ? dense + acc : acc;
+            else
                 bpart[(c * 2 + (c == c0 ? 1 : 0)) * r + lane] = acc;
         }
     };
@@ -697,20 +697,27 @@ __global__ __launch_bounds__(256) void bwd_sparse_kernel(const int32_t* __restri
         const int32_t p = __builtin_amdgcn_readlane(pl, u);  // 0 past cnt: a valid row
         zv[u] = lane < r ? z[(int64_t)(p / k) * r + lane] : 0.0f;
     }
+    // accumulating: the dense dR2 rows of the entries' experts, also all in flight at once
+    float dv[kBwChunk];
+#pragma unroll
+    for (int u = 0; u < kBwChunk; ++u) {
+        const int32_t e = __builtin_amdgcn_readlane(el, u);  // 0 past cnt: a valid row
+        dv[u] = (accumulate && lane < r) ? dR2t[(int64_t)e * r + lane] : 0.0f;
+    }
 #pragma unroll
     for (int u = 0; u < kBwChunk; ++u) {
         if (u < cnt) {
             const int32_t e = __builtin_amdgcn_readlane(el, u);
             const float v = __builtin_bit_cast(float, __builtin_amdgcn_readlane(vbits, u));
             if (e != cur) {
-                flush(cur, u - 1, acc);
+                flush(cur, u - 1, acc, dv[u > 0 ? u - 1 : 0]);
                 cur = e;
                 acc = 0.0f;
             }
             acc += v * zv[u];
+            if (u == cnt - 1) flush(cur, u, acc, dv[u]);
         }
     }
-    flush(cur, cnt - 1, acc);
 }
 
 // dR2t[e][j] = the P partials in order, then the dtop terms of bwd_sparse (in chunk order for an
@@ -754,17 +761,29 @@ __global__ __launch_bounds__(256) void bwd_dr2_fix_kernel(const int32_t* __restr
                                                           const float* __restrict__ bpart,
                                                           int32_t M, int32_t r,
                                                           float* __restrict__ dR2t) {
-    const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;  // one thread per expert
-    if (e >= M) return;
-    const int64_t o0 = offsets[e], o1 = offsets[e + 1];
-    if (o1 <= o0) return;
-    const int64_t c0 = o0 / kBwChunk, c1 = (o1 - 1) / kBwChunk;
-    if (c0 == c1) return;  // added by bwd_sparse
-    for (int32_t j = 0; j < r; ++j) {  // rare: experts whose selections span chunks
-        float s = dR2t[e * r + j];
-        s += bpart[(c0 * 2 + 1) * r + j];
-        for (int64_t c = c0 + 1; c <= c1; ++c) s += bpart[(c * 2) * r + j];
-        dR2t[e * r + j] = s;
+    // lane l of a wave checks expert 64 w + l; the wave then fixes each spanning one, lane = column
+    const int lane = threadIdx.x & 63;
+    const int64_t e0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * 64;
+    const int64_t e = e0 + lane;
+    int64_t o0 = 0, o1 = 0;
+    if (e < M) {
+        o0 = offsets[e];
+        o1 = offsets[e + 1];
+    }
+    const bool span = o1 > o0 && o0 / kBwChunk != (o1 - 1) / kBwChunk;
+    uint64_t m = __ballot(span);
+    while (m) {  // wave-uniform
+        const int src = __builtin_ctzll(m);
+        m &= m - 1;
+        const int64_t ee = e0 + src;
+        const int64_t c0 = (int64_t)__builtin_amdgcn_readlane((int32_t)o0, src) / kBwChunk;
+        const int64_t c1 = ((int64_t)__builtin_amdgcn_readlane((int32_t)o1, src) - 1) / kBwChunk;
+        if (lane < r) {
+            float s = dR2t[ee * r + lane];
+            s += bpart[(c0 * 2 + 1) * r + lane];
+            for (int64_t c = c0 + 1; c <= c1; ++c) s += bpart[(c * 2) * r + lane];
+            dR2t[ee * r + lane] = s;
+        }
     }
 }
 
@@ -1111,7 +1130,7 @@ hipError_t backward_launch(const BackwardPlan& p, const BackwardArgs& a, void* w
     const int64_t nr2 = (int64_t)a.M * r;
     if (direct)
         hipLaunchKernelGGL(bwd_dr2_fix_kernel, dim3((unsigned)(((int64_t)a.M + 255) / 256)),
-                           dim3(256), 0, st, offsets, bpart, a.M, r, a.dR2t);
+                           dim3(256), 0, st, offsets, bpart, a.M, r, a.dR2t);  // 64 experts a wave
     else
         hipLaunchKernelGGL(bwd_dr2_kernel, dim3((unsigned)((nr2 + 255) / 256)), dim3(256), 0, st,
                            reinterpret_cast<const float*>(ws + p.off_r2part),
