@@ -393,24 +393,35 @@ __global__ __launch_bounds__(256) void bwd_dz_kernel(const float* __restrict__ d
 #pragma unroll
             for (int v = 0; v < VPT; ++v) s[v] = dzsum[t * R + j0 + v];
         }
-        for (int32_t u = 0; u < k; ++u) {
-            const int32_t e = idx[t * k + u];
-            if (e >= 0 && e < M) {
-                const float d = dtop[t * k + u];
-                const uint16_t* row = R2t + (int64_t)e * R + j0;
-                uint16_t w[VPT];
-                if constexpr (VPT == 8) {
-                    const u32x4 q = *reinterpret_cast<const u32x4*>(row);
-                    __builtin_memcpy(w, &q, sizeof w);
-                } else if constexpr (VPT == 4) {
-                    const uint2 q = *reinterpret_cast<const uint2*>(row);
-                    __builtin_memcpy(w, &q, sizeof w);
-                } else {
-                    const uint32_t q = *reinterpret_cast<const uint32_t*>(row);
-                    __builtin_memcpy(w, &q, sizeof w);
-                }
+        for (int32_t u0 = 0; u0 < k; u0 += 8) {  // eight selections' rows in flight, added in order
+            int32_t ee[8];
+            float dd[8];
+            uint16_t w[8][VPT];
 #pragma unroll
-                for (int v = 0; v < VPT; ++v) s[v] += d * bf16_bits_to_f32(w[v]);
+            for (int q = 0; q < 8; ++q) {
+                const int32_t u = u0 + q;
+                const int32_t e = u < k ? idx[t * k + u] : -1;
+                const bool ok = e >= 0 && e < M;
+                ee[q] = ok ? e : -1;
+                dd[q] = ok ? dtop[t * k + u] : 0.0f;
+                const uint16_t* row = R2t + (int64_t)(ok ? e : 0) * R + j0;
+                if constexpr (VPT == 8) {
+                    const u32x4 v = *reinterpret_cast<const u32x4*>(row);
+                    __builtin_memcpy(w[q], &v, sizeof w[q]);
+                } else if constexpr (VPT == 4) {
+                    const uint2 v = *reinterpret_cast<const uint2*>(row);
+                    __builtin_memcpy(w[q], &v, sizeof w[q]);
+                } else {
+                    const uint32_t v = *reinterpret_cast<const uint32_t*>(row);
+                    __builtin_memcpy(w[q], &v, sizeof w[q]);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                if (ee[q] >= 0) {
+#pragma unroll
+                    for (int v = 0; v < VPT; ++v) s[v] += dd[q] * bf16_bits_to_f32(w[q][v]);
+                }
             }
         }
     }
