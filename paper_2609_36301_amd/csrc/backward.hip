@@ -60,6 +60,7 @@ constexpr int bw_tpw() { return (RC == 4 && DZ) ? 1 : 2; }
 constexpr int kBwStageE = 128;   // experts per LDS stage of the token-major sweeps
 constexpr int kBwNE = 2;         // 32-expert tiles per wave in the expert-major sweep
 constexpr int kBwStageT = 128;   // tokens per LDS stage of the expert-major sweep
+constexpr int kBwFoldParts = 16; // at most this many partials: summed by their consumers
 
 __device__ __forceinline__ float bw_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -138,7 +139,8 @@ struct TokCfg {
 template <int RC, bool DZ>
 __global__ __launch_bounds__((64 * bw_waves<RC, DZ>()), 1) void bwd_tok_kernel(
     const uint16_t* __restrict__ zhl, const float* __restrict__ bias,
-    const float* __restrict__ gtok, const float* __restrict__ pbar,
+    const float* __restrict__ gtok, const float* __restrict__ gpart, int32_t gparts,
+    float* gsummed, const float* __restrict__ pbar,
     const uint16_t* __restrict__ R2t, int32_t T, int32_t M, int32_t WT, int32_t splits,
     float* __restrict__ out) {
     constexpr int NW = bw_waves<RC, DZ>();
@@ -179,7 +181,18 @@ __global__ __launch_bounds__((64 * bw_waves<RC, DZ>()), 1) void bwd_tok_kernel(
             zl[g][c] = ok ? lv : zero_bf16x8();
         }
         bt[g] = ok ? bias[t] : kBwNoToken;
-        gt[g] = (DZ && ok) ? gtok[t] : 0.0f;
+        // g: the summed array, or (few partials) their sum in order, which the first expert
+        // split's first wave column stores for the expert-major sweep
+        float gsum = 0.0f;
+        if (DZ && ok) {
+            if (gparts > 0) {
+                for (int32_t p = 0; p < gparts; ++p) gsum += gpart[(int64_t)p * T + t];
+                if (split == 0 && we == 0 && half == 0) gsummed[t] = gsum;
+            } else {
+                gsum = gtok[t];
+            }
+        }
+        gt[g] = gsum;
     }
 
     // stage loads: piece p = expert p / (R / 8) of the stage, rank piece p % (R / 8)
@@ -367,12 +380,15 @@ __global__ __launch_bounds__(256) void bwd_colsum_kernel(const float* __restrict
 
 // ------------------------------------------------------------------------------ dz
 // One workgroup per 32 tokens, eight threads per token, each owning VPT = r / 8 consecutive rank
-// columns: dz[t][j] = dzsum[t][j] (the dense part, when given), then dtop[t][q] R2t[e][j] for the
+// columns: dz[t][j] = the dense part (dzsum, or the dz sweep's partials summed here in order when
+// there are few), then dtop[t][q] R2t[e][j] for the
 // token's selections q = 0 .. k-1 with e = idx[t][q] in [0, M) (one VPT-wide gather each).
 // Writes dz as bf16 hi/lo rows dzhl [T][2r] and, through LDS, as transposed rows dzT [2][r][Tp]
 // (Tp = T rounded up to 64; the columns past T are zero).
 template <int RC>
 __global__ __launch_bounds__(256) void bwd_dz_kernel(const float* __restrict__ dzsum,
+                                                     const float* __restrict__ dzpart,
+                                                     int32_t dzparts,
                                                      const int32_t* __restrict__ idx,
                                                      const float* __restrict__ dtop, int32_t k,
                                                      const uint16_t* __restrict__ R2t, int32_t T,
@@ -389,7 +405,12 @@ __global__ __launch_bounds__(256) void bwd_dz_kernel(const float* __restrict__ d
 #pragma unroll
     for (int v = 0; v < VPT; ++v) s[v] = 0.0f;
     if (t < T) {
-        if (dzsum) {
+        if (dzparts > 0) {  // the dz sweep's partials in order (few), else their sum
+            for (int32_t p = 0; p < dzparts; ++p) {
+#pragma unroll
+                for (int v = 0; v < VPT; ++v) s[v] += dzpart[((int64_t)p * T + t) * R + j0 + v];
+            }
+        } else if (dzsum) {
 #pragma unroll
             for (int v = 0; v < VPT; ++v) s[v] = dzsum[t * R + j0 + v];
         }
@@ -1061,13 +1082,15 @@ static void launch_balance(const BackwardPlan& p, const BackwardArgs& a, char* w
     const TokGrid& G = p.gsweep;
     const TokGrid& D = p.dzsweep;
     hipLaunchKernelGGL((bwd_tok_kernel<RC, false>), dim3((unsigned)(G.ntb * G.splits)),
-                       dim3(64 * bw_waves<RC, false>()), 0, st, zhl, bias, nullptr, a.pbar, a.R2t, a.T, a.M, G.WT,
-                       G.splits, gpart);
-    launch_colsum(gpart, G.parts, a.T, g, st);
+                       dim3(64 * bw_waves<RC, false>()), 0, st, zhl, bias, nullptr, nullptr, 0,
+                       nullptr, a.pbar, a.R2t, a.T, a.M, G.WT, G.splits, gpart);
+    // few partials: the dz sweep sums them (and stores g); many: one summing launch
+    const int32_t gp = G.parts <= kBwFoldParts ? G.parts : 0;
+    if (gp == 0) launch_colsum(gpart, G.parts, a.T, g, st);
     hipLaunchKernelGGL((bwd_tok_kernel<RC, true>), dim3((unsigned)(D.ntb * D.splits)),
-                       dim3(64 * bw_waves<RC, true>()), 0, st, zhl, bias, g, a.pbar, a.R2t, a.T, a.M, D.WT,
-                       D.splits, dzpart);
-    launch_colsum(dzpart, D.parts, (int64_t)a.T * a.r, dzsum, st);
+                       dim3(64 * bw_waves<RC, true>()), 0, st, zhl, bias, gp ? nullptr : g, gpart, gp,
+                       gp ? g : nullptr, a.pbar, a.R2t, a.T, a.M, D.WT, D.splits, dzpart);
+    if (D.parts > kBwFoldParts) launch_colsum(dzpart, D.parts, (int64_t)a.T * a.r, dzsum, st);
     // one token split: the sweep's partials are dR2's dense part, written in place
     hipLaunchKernelGGL((bwd_exp_kernel<RC>), dim3((unsigned)((int64_t)p.eblocks * p.esplits)),
                        dim3(kBwThreads), 0, st, zhl, zb, bias, g, a.pbar, a.R2t, a.T, a.M,
@@ -1082,9 +1105,12 @@ static void launch_phase3(const BackwardPlan& p, const BackwardArgs& a, char* ws
     const uint16_t* R1 = reinterpret_cast<const uint16_t*>(ws + p.off_r1);
     float* r1part = reinterpret_cast<float*>(ws + p.off_r1part);
     // dz = the dense sum (when pbar is given) plus the dtop rows of R2, as hi/lo rows and transposed
+    const bool fold = p.balance && p.dzsweep.parts <= kBwFoldParts;
     hipLaunchKernelGGL((bwd_dz_kernel<RC>), dim3((unsigned)(p.Tp / 32)), dim3(256), 0, st,
-                       p.balance ? reinterpret_cast<const float*>(ws + p.off_dzsum) : nullptr,
-                       a.idx, a.dtop, a.k, a.R2t, a.T, a.M, p.Tp,
+                       (p.balance && !fold) ? reinterpret_cast<const float*>(ws + p.off_dzsum)
+                                            : nullptr,
+                       fold ? reinterpret_cast<const float*>(ws + p.off_dzpart) : nullptr,
+                       fold ? p.dzsweep.parts : 0, a.idx, a.dtop, a.k, a.R2t, a.T, a.M, p.Tp,
                        reinterpret_cast<uint16_t*>(ws + p.off_dzhl),
                        reinterpret_cast<uint16_t*>(ws + p.off_dzT));
     const int32_t Ct = (a.h + 31) / 32;
