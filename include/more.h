@@ -44,14 +44,19 @@
  *    (The paper's buffer leaves both the slot order and tie handling open; this total
  *    order makes every plan and every run bitwise reproducible.)
  *  - Limits: 1 <= k <= min(M, MORE_K_MAX) for the full-rank router and
- *    1 <= k <= min(M, MORE_LOWRANK_K_MAX) for the low-rank router; r in {16, 32, 64}; h a
- *    positive multiple of 16; M >= 1 (any value; the last expert tile is masked to -inf, as
+ *    1 <= k <= min(M, MORE_LOWRANK_K_MAX) for the low-rank router, with r a multiple of 16 up
+ *    to 256 (the paper's rank sweeps, Section "Routing expressivity"); the training forward
+ *    and backward passes take r in {16, 32, 64}, and the training forward k <=
+ *    MORE_LOWRANK_TRAIN_K_MAX; h a positive multiple of 16; M >= 1 (any value; the last expert tile is masked to -inf, as
  *    the paper's inference algorithm does for out-of-range experts); T <= 2^31 - 1.
  *  - Numerics: z = x R1 is accumulated in fp32.  The expert sweeps run on the matrix cores
  *    with z rounded to bfloat16 and a rigorous bound on the resulting logit error, which
  *    selects a small candidate set that provably holds the top k; the candidates' logits
  *    are then evaluated exactly in fp32 (fp32 z times the bfloat16 expert rows).  The paper's
- *    kernel instead narrows z to one bfloat16 for the whole contraction.
+ *    kernel instead narrows z to one bfloat16 for the whole contraction.  Shapes outside the
+ *    register-tiled routes (r not in {16, 32, 64}, or k > 16) take the wide route
+ *    (MORE_ROUTE_WIDE): fp32 z split exactly into three bfloat16 pieces and one fused sweep of
+ *    the matrix cores over the 3r-wide pair, i.e. the same fp32 logits up to summation order.
  */
 #ifndef MORE_H
 #define MORE_H
@@ -72,7 +77,8 @@ typedef enum more_status {
 } more_status;
 
 #define MORE_K_MAX 32
-#define MORE_LOWRANK_K_MAX 16
+#define MORE_LOWRANK_K_MAX 32
+#define MORE_LOWRANK_TRAIN_K_MAX 16
 
 /*
  * Low-rank router (Section "Preliminaries", MoRE layer; Appendix "Pseudocode", inference
@@ -107,7 +113,8 @@ more_status more_route_lowrank_workspace_size(int64_t T, int32_t h, int32_t r, i
  * inside the routing workgroup, summing the h axis in another order: its logits can differ from
  * the others' in the last bits (selections only where logits tie to rounding); so can those of
  * the single-pass route, which m_chunks = 0 picks for T >= 4096 and M >= 32768.  This entry
- * point exists for tuning and for tests of these properties.  Its workspace size comes from
+ * point exists for tuning and for tests of these properties.  The wide route ignores m_chunks
+ * (any valid value gives the same result).  Its workspace size comes from
  * more_route_lowrank_workspace_size_ex with the same m_chunks (0 bytes for the one-launch
  * route).
  */
@@ -124,7 +131,7 @@ more_status more_route_lowrank_workspace_size_ex(int64_t T, int32_t h, int32_t r
  * shape with a route that no m_chunks >= 1 selects: a fused route (expert sets with
  * r * M <= 2^18 and M <= 16384: one workgroup per 64 tokens sweeps all experts) or the
  * single-pass route (T >= 4096 and M >= 32768: one screening sweep over all experts after a
- * prescreen of an eighth of them; see more_route_lowrank_ex). */
+ * prescreen of an eighth of them; see more_route_lowrank_ex) or the wide route. */
 more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
                                     int32_t* m_chunks);
 
@@ -135,6 +142,7 @@ more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, 
 #define MORE_ROUTE_FUSED 1       /* z pass; one fused kernel per 64 tokens over all experts     */
 #define MORE_ROUTE_FUSED_LOCAL 2 /* one launch: the fused kernel also computes z                */
 #define MORE_ROUTE_SINGLE_PASS 3 /* z + prescreen, one collect sweep, finalize (+ histogram)    */
+#define MORE_ROUTE_WIDE 4        /* z per rank block; exact 3-piece split; fused 3r-wide sweep */
 more_status more_route_lowrank_route(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
                                      int32_t* route);
 
@@ -158,7 +166,9 @@ more_status more_route_lowrank_route(int64_t T, int32_t h, int32_t r, int32_t M,
  * from the matrix cores with z carried as a bfloat16 hi/lo pair (about 16 significant bits):
  * each exponent is within 2^-18 sum_i |z_i u_ei| + 2^-24 (2r + 1)(|m| + sum_i |z_i u_ei|)
  * (times log2 e) of exact, and the sums run in fp32 in a fixed order, so a shape gives the same
- * bits on every run.  Limits as for more_route_lowrank.
+ * bits on every run.  Limits: r in {16, 32, 64} and k <= MORE_LOWRANK_TRAIN_K_MAX (the
+ * register-tiled routes; other shapes return MORE_ERR_UNSUPPORTED), otherwise as for
+ * more_route_lowrank.
  */
 more_status more_route_lowrank_train(const uint16_t* x, const uint16_t* R1t, const uint16_t* R2t,
                                      int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,

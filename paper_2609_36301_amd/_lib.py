@@ -12,7 +12,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmore.so"
 
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 K_MAX = 32
-LOWRANK_K_MAX = 16
+LOWRANK_K_MAX = 32
+LOWRANK_TRAIN_K_MAX = 16
+ROUTE_WIDE = 4
 NOALLOC_SCRATCH_BYTES = 256 << 20
 
 # (name, restype, argtypes) for every symbol declared in include/more.h

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmore.so")
 SOURCES = ["lowrank.hip", "resident.hip", "fullrank.hip", "histogram.hip", "dispatch.hip", "stats.hip", "fullrank_fused.hip",
-           "backward.hip",
+           "backward.hip", "wide.hip",
            "noalloc.hip", "more_api.cpp"]
 ARCH = "gfx950"
 

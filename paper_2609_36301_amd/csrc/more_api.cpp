@@ -7,6 +7,7 @@
 #include "more.h"
 #include "lowrank.h"
 #include "backward.h"
+#include "wide.h"
 
 namespace {
 
@@ -23,12 +24,17 @@ more_status check_common(int64_t T, int32_t h, int32_t M, int32_t k) {
     return MORE_OK;
 }
 
+// Inference calls take any r that is a multiple of 16 up to 256 and k <= 32 (the shapes outside
+// the register-tiled routes go to the wide route); the training forward keeps those routes'
+// limits, r in {16, 32, 64} and k <= 16.
 more_status check_lowrank(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
-                          int32_t m_chunks) {
+                          int32_t m_chunks, bool training = false) {
     if (r <= 0) return MORE_ERR_INVALID_ARG;
     more_status s = check_common(T, h, M, k);
     if (s != MORE_OK) return s;
-    if (!rank_supported(r) || k > MORE_LOWRANK_K_MAX) return MORE_ERR_UNSUPPORTED;
+    if (r % 16 != 0 || r > more::kWideMaxRank || k > MORE_LOWRANK_K_MAX) return MORE_ERR_UNSUPPORTED;
+    if (training && (!rank_supported(r) || k > MORE_LOWRANK_TRAIN_K_MAX))
+        return MORE_ERR_UNSUPPORTED;
     if (m_chunks < 0 || (m_chunks > 1 && (m_chunks % 8 != 0 || m_chunks > 1024)))
         return MORE_ERR_INVALID_ARG;
     return MORE_OK;
@@ -62,6 +68,12 @@ more_status more_route_lowrank_workspace_size_ex(int64_t T, int32_t h, int32_t r
         *bytes = 0;
         return MORE_OK;
     }
+    if (more::wide_route_needed(r, k)) {
+        more::WidePlan w;
+        if (!more::wide_make_plan(T, h, r, M, k, &w)) return MORE_ERR_INVALID_ARG;
+        *bytes = w.workspace_bytes;
+        return MORE_OK;
+    }
     more::LowrankPlan p;
     if (!more::lowrank_make_plan(T, h, r, M, k, m_chunks, &p)) return MORE_ERR_INVALID_ARG;
     *bytes = p.workspace_bytes;
@@ -78,6 +90,10 @@ more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, 
     if (!m_chunks) return MORE_ERR_INVALID_ARG;
     more_status s = check_lowrank(T, h, r, M, k, 0);
     if (s != MORE_OK) return s;
+    if (more::wide_route_needed(r, k)) {
+        *m_chunks = 0;
+        return MORE_OK;
+    }
     more::LowrankPlan p;
     if (!more::lowrank_make_plan(T > 0 ? T : 1, h, r, M, k, 0, &p)) return MORE_ERR_INVALID_ARG;
     *m_chunks = p.fused || p.single_pass ? 0 : p.chunks;
@@ -89,6 +105,10 @@ more_status more_route_lowrank_route(int64_t T, int32_t h, int32_t r, int32_t M,
     if (!route) return MORE_ERR_INVALID_ARG;
     more_status s = check_lowrank(T, h, r, M, k, 0);
     if (s != MORE_OK) return s;
+    if (more::wide_route_needed(r, k)) {
+        *route = MORE_ROUTE_WIDE;
+        return MORE_OK;
+    }
     more::LowrankPlan p;
     if (!more::lowrank_make_plan(T > 0 ? T : 1, h, r, M, k, 0, &p)) return MORE_ERR_INVALID_ARG;
     *route = p.single_pass ? MORE_ROUTE_SINGLE_PASS
@@ -113,6 +133,16 @@ more_status more_route_lowrank_ex(const uint16_t* x, const uint16_t* R1t, const 
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (T == 0) {
         if (counts) return from_hip(more::histogram_launch(idx, 0, M, counts, st));
+        return MORE_OK;
+    }
+    if (more::wide_route_needed(r, k)) {
+        more::WidePlan w;
+        if (!more::wide_make_plan(T, h, r, M, k, &w)) return MORE_ERR_INVALID_ARG;
+        if (!workspace || workspace_bytes < w.workspace_bytes) return MORE_ERR_WORKSPACE;
+        if (more::wide_launch(w, x, R1t, R2t, T, h, r, M, k, idx, gate, topval, workspace, st) !=
+            hipSuccess)
+            return MORE_ERR_HIP;
+        if (counts) return from_hip(more::histogram_launch(idx, T * (int64_t)k, M, counts, st));
         return MORE_OK;
     }
     more::LowrankPlan p;
@@ -150,7 +180,7 @@ static bool train_plans(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
 more_status more_route_lowrank_train_workspace_size(int64_t T, int32_t h, int32_t r, int32_t M,
                                                     int32_t k, size_t* bytes) {
     if (!bytes) return MORE_ERR_INVALID_ARG;
-    more_status s = check_lowrank(T, h, r, M, k, 0);
+    more_status s = check_lowrank(T, h, r, M, k, 0, true);
     if (s != MORE_OK) return s;
     if (T == 0) {
         *bytes = 0;
@@ -173,7 +203,7 @@ more_status more_route_lowrank_train(const uint16_t* x, const uint16_t* R1t, con
         !aligned(gate, 4) || !aligned(topval, 4) || !aligned(counts, 4) || !aligned(m, 4) ||
         !aligned(Z, 4) || !aligned(psum, 4) || !aligned(workspace, 256))
         return MORE_ERR_INVALID_ARG;
-    more_status s = check_lowrank(T, h, r, M, k, 0);
+    more_status s = check_lowrank(T, h, r, M, k, 0, true);
     if (s != MORE_OK) return s;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (T == 0) {

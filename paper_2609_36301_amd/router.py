@@ -63,7 +63,7 @@ def lowrank_plan(T: int, h: int, r: int, M: int, k: int) -> int:
     return c.value
 
 
-ROUTE_NAMES = {0: "expert-resident", 1: "fused", 2: "fused-local", 3: "single-pass"}
+ROUTE_NAMES = {0: "expert-resident", 1: "fused", 2: "fused-local", 3: "single-pass", 4: "wide"}
 
 
 def lowrank_route(T: int, h: int, r: int, M: int, k: int) -> str:

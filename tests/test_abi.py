@@ -72,11 +72,15 @@ def lowrank(lib, T=64, h=64, r=16, M=64, k=4, x=FAKE, R1t=FAKE, R2t=FAKE, idx=FA
     (dict(k=0), _lib.ERR_INVALID_ARG),
     (dict(k=65, M=64), _lib.ERR_INVALID_ARG),
     (dict(k=33, M=64), _lib.ERR_UNSUPPORTED),
-    (dict(k=17, M=64), _lib.ERR_UNSUPPORTED),
-    (dict(r=128), _lib.ERR_UNSUPPORTED),
-    (dict(r=48), _lib.ERR_UNSUPPORTED),
-    (dict(r=256), _lib.ERR_UNSUPPORTED),
+    (dict(r=40), _lib.ERR_UNSUPPORTED),
+    (dict(r=272), _lib.ERR_UNSUPPORTED),
     (dict(h=72), _lib.ERR_UNSUPPORTED),
+    # the wide route's shapes pass validation and then need their workspace
+    (dict(k=17, M=64), _lib.ERR_WORKSPACE),
+    (dict(k=32, M=64), _lib.ERR_WORKSPACE),
+    (dict(r=48), _lib.ERR_WORKSPACE),
+    (dict(r=128), _lib.ERR_WORKSPACE),
+    (dict(r=256), _lib.ERR_WORKSPACE),
     (dict(T=2**31), _lib.ERR_UNSUPPORTED),
     (dict(m_chunks=3), _lib.ERR_INVALID_ARG),
     (dict(m_chunks=2048), _lib.ERR_INVALID_ARG),
@@ -160,7 +164,14 @@ def test_routes_for_the_paper_shapes(lib):
     for shape, name in want.items():
         assert router.lowrank_route(*shape) == name, shape
     c = ctypes.c_int32(0)
-    assert lib.more_route_lowrank_route(100, 64, 48, 1000, 4, ctypes.byref(c)) == _lib.ERR_UNSUPPORTED
+    assert lib.more_route_lowrank_route(100, 64, 40, 1000, 4, ctypes.byref(c)) == _lib.ERR_UNSUPPORTED
+    for r, k in ((48, 4), (128, 8), (256, 32), (16, 17), (64, 32)):
+        assert lib.more_route_lowrank_route(100, 64, r, 1000, k, ctypes.byref(c)) == _lib.OK
+        assert c.value == _lib.ROUTE_WIDE, (r, k)
+        assert router.lowrank_route(100, 64, r, 1000, k) == "wide"
+        mc = ctypes.c_int32(-1)
+        assert lib.more_route_lowrank_plan(100, 64, r, 1000, k, ctypes.byref(mc)) == _lib.OK
+        assert mc.value == 0
     assert lib.more_route_lowrank_route(100, 64, 32, 1000, 4, None) == _lib.ERR_INVALID_ARG
 
 

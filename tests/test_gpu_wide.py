@@ -1,0 +1,114 @@
+"""GPU parity of the wide low-rank route (marked `gpu`): ranks other than 16, 32 and 64 (any
+multiple of 16 up to 256, the paper's rank sweeps in Section "Routing expressivity") and
+17 <= k <= 32, against the fp64 oracle under the rules of oracle/parity.py.
+
+Shapes span every rank-block mix of the z pass (64-, 32- and 16-wide blocks), ragged token and
+expert counts, k at both ends of the list lengths and one token; a larger shape is checked on
+sampled tokens.  The route's own properties: the plain entry point and the _ex one with any
+m_chunks give identical bits, repeated calls are bitwise reproducible, the histogram matches
+the oracle's bincount, and an empty batch is a no-op.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import parity
+from gpu_util import announce, require_gpu, route_lowrank, to_dev
+from paper_2609_36301_amd import _lib, router
+from paper_2609_36301_amd.inputs import make_inputs, transposed_factors
+
+pytestmark = pytest.mark.gpu
+
+
+def _check(inp, k, idx, gate, topval, rows=None, label=""):
+    rep = parity.evaluate(inp.x, inp.R1, inp.R2, k, idx, gate, topval, rows=rows)
+    print("[parity] wide %s %s" % (label, rep), flush=True)
+    assert rep.ok(), "%s: %s mismatched rows %s band rows %s" % (
+        label, rep, rep.mismatch_rows[:10], rep.band_rows[:10])
+    return rep
+
+
+SHAPES = [
+    # T, h, r, M, k
+    (1, 32, 240, 7, 1),          # one token; blocks 64+64+64+32+16
+    (64, 64, 16, 33, 32),        # k = 32 with M = 33 at the smallest rank
+    (201, 64, 128, 301, 32),     # r = 128 with the longest list
+    (257, 96, 80, 777, 17),      # blocks 64+16, k just past the register-tiled routes
+    (513, 256, 48, 1000, 4),     # blocks 32+16
+    (300, 512, 256, 2049, 8),    # r = 256: four 64-wide blocks, ragged expert tile
+    (1000, 512, 112, 2048, 10),  # blocks 64+32+16, k = 10 (the paper's largest frontier k)
+    (130, 2048, 64, 4100, 20),   # r = 64 with k = 20, long h
+    (97, 128, 96, 64, 24),       # blocks 64+32, M = 64 (two expert tiles)
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "T%d_h%d_r%d_M%d_k%d" % s)
+def test_wide_shapes(shape):
+    T, h, r, M, k = shape
+    assert router.lowrank_route(T, h, r, M, k) == "wide"
+    inp = make_inputs(T, h, r, M, seed=7 * T + M + r)
+    idx, gate, topval, counts = route_lowrank(inp, k, histogram=True, tag="wide")
+    _check(inp, k, idx, gate, topval, label=str(shape))
+    assert np.array_equal(counts, oracle.histogram(idx, M).astype(np.int32))
+
+
+def test_wide_large_sampled():
+    # 8192 tokens, r = 128, 16384 experts, k = 8: the oracle on 600 sampled tokens
+    T, h, r, M, k = 8192, 1024, 128, 16384, 8
+    inp = make_inputs(T, h, r, M, seed=77)
+    idx, gate, topval, counts = route_lowrank(inp, k, histogram=True, tag="wide large")
+    rng = np.random.default_rng(5)
+    rows = np.unique(np.concatenate([rng.choice(T, 600, replace=False), [0, T - 1]]))
+    _check(inp, k, idx, gate, topval, rows=rows, label="large sampled")
+    assert np.array_equal(counts, np.bincount(idx.ravel(), minlength=M).astype(np.int32))
+
+
+def test_wide_plain_entry_point_matches_ex_and_is_reproducible():
+    torch = require_gpu()
+    T, h, r, M, k = 700, 256, 128, 3000, 16
+    inp = make_inputs(T, h, r, M, seed=31)
+    R1t, R2t = transposed_factors(inp)
+    x_d, r1_d, r2_d = to_dev(inp.x), to_dev(R1t), to_dev(R2t)
+    lib = _lib.load()
+    ws_n = ctypes.c_size_t(0)
+    assert lib.more_route_lowrank_workspace_size(T, h, r, M, k, ctypes.byref(ws_n)) == _lib.OK
+    ws = torch.empty(ws_n.value, dtype=torch.uint8, device="cuda")
+
+    def plain():
+        idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
+        gate = torch.empty((T, k), dtype=torch.float32, device="cuda")
+        tv = torch.empty((T, k), dtype=torch.float32, device="cuda")
+        cnt = torch.empty((M,), dtype=torch.int32, device="cuda")
+        announce("wide more_route_lowrank T=%d h=%d r=%d M=%d k=%d" % (T, h, r, M, k))
+        st = lib.more_route_lowrank(x_d.data_ptr(), r1_d.data_ptr(), r2_d.data_ptr(), T, h, r, M,
+                                    k, idx.data_ptr(), gate.data_ptr(), tv.data_ptr(),
+                                    cnt.data_ptr(), ws.data_ptr(), ws_n.value,
+                                    torch.cuda.current_stream().cuda_stream)
+        assert st == _lib.OK, lib.more_status_string(st)
+        torch.cuda.synchronize()
+        return [a.cpu().numpy() for a in (idx, gate, tv, cnt)]
+
+    a = plain()
+    b = plain()
+    for u, v in zip(a, b):
+        assert np.array_equal(u, v)
+    ex = route_lowrank(inp, k, m_chunks=8, histogram=True, tag="wide _ex m_chunks=8")
+    for u, v in zip(a, ex):
+        assert np.array_equal(u, v)
+    _check(inp, k, a[0], a[1], a[2], label="plain entry point")
+    assert np.array_equal(a[3], oracle.histogram(a[0], M).astype(np.int32))
+
+
+def test_wide_empty_batch():
+    torch = require_gpu()
+    h, r, M, k = 64, 128, 100, 20
+    x = torch.empty((0, h), dtype=torch.bfloat16, device="cuda")
+    R1t = torch.zeros((r, h), dtype=torch.bfloat16, device="cuda")
+    R2t = torch.zeros((M, r), dtype=torch.bfloat16, device="cuda")
+    announce("wide route_lowrank empty batch r=%d k=%d" % (r, k))
+    out = router.route_lowrank(x, R1t, R2t, k, topval=True, histogram=True)
+    torch.cuda.synchronize()
+    assert out.idx.shape == (0, k)
+    assert int(out.counts.abs().sum().item()) == 0
