@@ -53,8 +53,11 @@ SCOPE_LOCAL = ("one routing call: one launch of the local fused kernel (z pass, 
                "bounds, screen, threshold, collect and finalize) (+ histogram)")
 SCOPE_SINGLE = ("one routing call: the z + prescreen, collect and finalize kernels and the "
                 "histogram kernel, timed together as one step")
+SCOPE_WIDE = ("one routing call: the z pass per rank block, the three-piece split of z, the "
+              "stacked expert rows and the fused 3r-wide sweep (+ histogram), timed together as "
+              "one step")
 SCOPES = {"expert-resident": SCOPE_RESIDENT, "fused": SCOPE_FUSED, "fused-local": SCOPE_LOCAL,
-          "single-pass": SCOPE_SINGLE}
+          "single-pass": SCOPE_SINGLE, "wide": SCOPE_WIDE}
 
 
 KERNEL_SOURCES = ("lowrank.hip", "lowrank.h", "device_common.h", "route_device.h",
@@ -222,6 +225,31 @@ def backward_leg(w, dev, router, trr, bufs, nbuf, args):
                      "executed_flops": 16 * w.T * w.r * w.M + 6 * w.T * w.r * w.h}}
 
 
+def train_legs(w, dev, router, bufs, nbuf, args, sec, result):
+    """Training forward pass on the same batches: the routing call plus the softmax statistics
+    m, Z and psum over all experts (two expert sweeps); then the backward pass.  Algorithmic
+    flops of the statistics: the T x M logits once per sweep, 2 T r M each; the exponentials:
+    T M per sweep."""
+    import torch
+    trr = router.LowrankTrainRouter(w.T, w.h, w.r, w.M, w.k, device=dev, histogram=w.histogram)
+    tt = timed_graph(lambda i: trr(*bufs[i % nbuf]), args.steps, args.warmup)
+    stats_s = tt["mean_s"] - sec
+    sflops = 4 * w.T * w.r * w.M
+    sach = sflops / stats_s / 1e12
+    result["train"] = {
+        "op": "training forward (more_route_lowrank_train): routing + m, Z, psum over all experts",
+        "ms": round(tt["mean_s"] * 1e3, 5), "tokens_per_s": round(w.T / tt["mean_s"], 1),
+        "stats_ms": round(stats_s * 1e3, 5),
+        "stats_roofline": {"bound": "mfma", "achieved": round(sach, 2), "peak": PEAK_BF16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": round(sach / PEAK_BF16_TFLOPS, 4),
+                           "algorithmic_flops": sflops,
+                           "exp_per_s": round(2 * w.T * w.M / stats_s, 1)}}
+    if not args.no_backward:
+        result["backward"] = backward_leg(w, dev, router, trr, bufs, nbuf, args)
+    del trr
+    torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -249,9 +277,9 @@ def main():
 
     import torch
     from paper_2609_36301_amd import router
-    from paper_2609_36301_amd.inputs import WORKLOADS, make_workload_inputs, transposed_factors
+    from paper_2609_36301_amd.inputs import find_workload, make_workload_inputs, transposed_factors
 
-    w = WORKLOADS[args.workload]
+    w = find_workload(args.workload)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     inp = make_workload_inputs(w)
@@ -326,26 +354,10 @@ def main():
                                        "algorithmic_bytes": dbytes}}
     del ds, dsrc
 
-    # Training forward pass on the same batches: the routing call plus the softmax statistics
-    # m, Z and psum over all experts (two expert sweeps).  Algorithmic flops of the statistics:
-    # the T x M logits once per sweep, 2 T r M each; the exponentials: T M per sweep.
-    trr = router.LowrankTrainRouter(w.T, w.h, w.r, w.M, w.k, device=dev, histogram=w.histogram)
-    tt = timed_graph(lambda i: trr(*bufs[i % nbuf]), args.steps, args.warmup)
-    stats_s = tt["mean_s"] - sec
-    sflops = 4 * w.T * w.r * w.M
-    sach = sflops / stats_s / 1e12
-    result["train"] = {
-        "op": "training forward (more_route_lowrank_train): routing + m, Z, psum over all experts",
-        "ms": round(tt["mean_s"] * 1e3, 5), "tokens_per_s": round(w.T / tt["mean_s"], 1),
-        "stats_ms": round(stats_s * 1e3, 5),
-        "stats_roofline": {"bound": "mfma", "achieved": round(sach, 2), "peak": PEAK_BF16_TFLOPS,
-                           "unit": "TFLOP/s", "frac": round(sach / PEAK_BF16_TFLOPS, 4),
-                           "algorithmic_flops": sflops,
-                           "exp_per_s": round(2 * w.T * w.M / stats_s, 1)}}
-    if not args.no_backward:
-        result["backward"] = backward_leg(w, dev, router, trr, bufs, nbuf, args)
-    del trr
-    torch.cuda.empty_cache()
+    if route == "wide":  # the training passes take the register-tiled shapes only
+        result["train"] = result["backward"] = "not supported at r=%d, k=%d" % (w.r, w.k)
+    else:
+        train_legs(w, dev, router, bufs, nbuf, args, sec, result)
 
     if not args.no_fullrank:
         # full-rank router on the same token batches with W = R1 R2 rounded to bf16; logits

@@ -79,6 +79,22 @@ WORKLOADS: dict[str, Workload] = {
 }
 
 
+# Shapes outside the benchmark suite, for timing routes the suite does not reach: the paper's
+# rank sweeps go up to r = 256 (Section "Routing expressivity"); r = 128 takes the wide route.
+EXTRA_WORKLOADS: dict[str, Workload] = {
+    w.name: w
+    for w in (
+        Workload("rank128", 16384, 2048, 128, 16384, 8, histogram=True,
+                 description="rank-sweep shape at r = 128 (wide route); expert histogram"),
+    )
+}
+
+
+def find_workload(name: str) -> Workload:
+    """A benchmark-suite workload or one of the extra shapes, by name."""
+    return WORKLOADS[name] if name in WORKLOADS else EXTRA_WORKLOADS[name]
+
+
 @dataclasses.dataclass
 class RouterInputs:
     """bf16 bit patterns (uint16) in mathematical orientation."""
