@@ -1,8 +1,8 @@
 """GPU parity of the dispatch bookkeeping (Sort + Count) against the oracle: offsets and sorted
 positions bit for bit (marked `gpu`).
 
-Cases span one, two and three radix passes (keys below 2^8, 2^16 and 2^24), ids outside the
-expert range, one expert taking every entry, entry counts that are not a multiple of the
+Cases span one, two and three radix passes (keys below 2^8, 2^16 and 2^24), the one counting
+pass (keys below 2^13), ids outside the expert range, one expert taking every entry, entry counts that are not a multiple of the
 1024-entry block, no tokens, the bench workloads' sizes with a skewed expert choice, and the
 output of a routing call.
 """
@@ -51,6 +51,25 @@ def _skewed(T, k, M, seed):
 def test_random_ids(T, k, M):
     rng = np.random.default_rng(T + M)
     _check(rng.integers(0, M, size=(T, k)).astype(np.int32), M, "random")
+
+
+@pytest.mark.parametrize("T,k,M", [(3000, 4, 8192), (5000, 3, 16384), (1100, 8, 40000),
+                                   (2000, 4, 524287), (2100, 4, 524288)],
+                         ids=lambda v: str(v))
+def test_wide_keys_with_invalid_ids_and_a_hot_expert(T, k, M):
+    # keys of 14 to 20 bits (two and three radix passes), ids outside [0, M) and a hot expert
+    rng = np.random.default_rng(T + k + M)
+    idx = rng.integers(0, M, size=(T, k)).astype(np.int32)
+    idx[::13, 0] = -1
+    idx[::17, 1] = 2 ** 31 - 1
+    idx[::3, 2] = M - 1
+    _check(idx, M, "wide keys")
+
+
+def test_sixteen_hot_experts_take_every_entry():
+    rng = np.random.default_rng(8)
+    idx = rng.integers(65520, 65536, size=(10000, 8)).astype(np.int32)
+    _check(idx, 65536, "sixteen hot experts")
 
 
 def test_ids_outside_the_range_go_last():
