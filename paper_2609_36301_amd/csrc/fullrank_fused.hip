@@ -274,10 +274,11 @@ bool fullrank_fused_make_plan(int64_t T, int32_t h, int32_t M, int32_t k, FusedF
     FusedFullrankPlan q{};
     q.K = ff_pow2(k);
     // token tiles per workgroup: the x rows fit the LDS block and the lists (NT K pairs per lane)
-    // stay at most 32
+    // stay at most 16, or 32 with one tile (more spilled registers: 76 bytes per lane at
+    // NT = 4, K = 8, for no gain in speed)
     const int64_t xs_row = (((int64_t)h + 63) & ~(int64_t)63) + 8;  // bf16 per LDS row
     int NT = 4;
-    while (NT > 1 && (32 * NT * xs_row * 2 > kFfLdsBytes || NT * q.K > 32)) NT >>= 1;
+    while (NT > 1 && (32 * NT * xs_row * 2 > kFfLdsBytes || NT * q.K > 16)) NT >>= 1;
     if (32 * NT * xs_row * 2 > kFfLdsBytes || NT * q.K > 32) return false;
     // Expert splits give each wave at least 16 tiles (fewer leave the register lists filling up
     // for most of the sweep, where almost every logit is inserted); narrower token blocks then
@@ -323,8 +324,8 @@ hipError_t fullrank_fused_launch(const FusedFullrankPlan& p, const uint16_t* x, 
         launch_ff<NT_, K_>(p, x, Wt, T, h, M, k, idx, gate, topval, workspace, st);       \
         return hipGetLastError();                                                        \
     }
-    MORE_FF(4, 1) MORE_FF(4, 2) MORE_FF(4, 4) MORE_FF(4, 8)
-    MORE_FF(2, 1) MORE_FF(2, 2) MORE_FF(2, 4) MORE_FF(2, 8) MORE_FF(2, 16)
+    MORE_FF(4, 1) MORE_FF(4, 2) MORE_FF(4, 4)
+    MORE_FF(2, 1) MORE_FF(2, 2) MORE_FF(2, 4) MORE_FF(2, 8)
     MORE_FF(1, 1) MORE_FF(1, 2) MORE_FF(1, 4) MORE_FF(1, 8) MORE_FF(1, 16) MORE_FF(1, 32)
 #undef MORE_FF
     return hipErrorInvalidValue;

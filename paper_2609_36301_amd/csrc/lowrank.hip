@@ -1097,7 +1097,7 @@ bool lowrank_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, in
     // which needs no z pass and no workspace.
     q.local = q.fused && q.K <= 8 && (Mt + kRouteWaves - 1) / kRouteWaves <= fused_reg_tiles(q.RC) &&
               h < (1 << 24);
-    const int tokens_per_block = q.fused ? kFusedTokens : 32 * route_tpw(q.RC, q.K) * kRouteWaves;
+    const int tokens_per_block = q.fused ? kFusedTokens : 32 * kRouteTPW * kRouteWaves;
     q.ntb = (int32_t)((T + tokens_per_block - 1) / tokens_per_block);
     const int64_t emax_tiles = (int64_t)kChunkBytes / (2 * r) / 32;
     if (q.fused) {

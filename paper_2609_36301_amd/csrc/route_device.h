@@ -53,9 +53,10 @@ constexpr int kRouteWaves = 8;
 constexpr int kRouteThreads = 64 * kRouteWaves;
 constexpr int kChunkBytes = 128 * 1024;       // LDS for the resident expert rows
 
-// Token groups of 32 per wave: 4 at r = 64 and K <= 8 (the A-operand reads from LDS, which do not
-// overlap the MFMAs, then cost half as much per MFMA), else 2.
-__host__ __device__ constexpr int route_tpw(int RC, int K) { return RC == 4 && K <= 8 ? 4 : 2; }
+// Token groups of 32 per wave: 2.  (Four at r = 64 and K <= 8 halve the LDS reads per MFMA but
+// need more than 256 registers: the screen and collect kernels spilled 32-100 bytes per lane, and
+// the two-group version, spill-free, runs the mid workload in the same time.)
+constexpr int kRouteTPW = 2;
 
 template <int RC, int K>
 struct RouteCfg {
@@ -64,7 +65,7 @@ struct RouteCfg {
     static constexpr int U = K / 4 > 1 ? K / 4 : 1;       // bucket period, in tiles
     static constexpr int L = 4 * U;                       // bucket maxima per lane (>= K)
     static constexpr int EMAX = kChunkBytes / (2 * R);    // experts per chunk (multiple of 32)
-    static constexpr int TPW = route_tpw(RC, K);          // token groups per wave
+    static constexpr int TPW = kRouteTPW;                 // token groups per wave
     static constexpr int TOK = 32 * TPW * kRouteWaves;    // tokens per block
     // candidate slots per lane and token group (the collect kernel's LDS must stay <= 160 KiB)
     static constexpr int SLOTS = TPW == 4 ? 7 : 8;

@@ -149,7 +149,7 @@ def test_plans_for_the_paper_shapes(lib):
         if T >= 4096 and M >= 32768:  # single-pass route
             assert C == 0, name
             continue
-        tokens_per_block = 1024 if (k <= 8 and r == 64) else 512  # 8 waves x 32 x (4 or 2)
+        tokens_per_block = 512  # 8 waves x 32 tokens x 2 token groups
         assert C & (C - 1) == 0, name
         assert r * M * 2 // C <= 2 << 20, name          # expert slice fits one L2
         assert C * -(-T // tokens_per_block) >= 256, name  # at least one workgroup per CU
