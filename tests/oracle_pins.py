@@ -58,7 +58,8 @@ def brute_force(logits: np.ndarray, k: int):
 
 # ------------------------------------------------------------------ brute force / identity
 def check_bruteforce(lib=None, shapes=((256, 512, 16, 256, 8), (37, 48, 16, 100, 5),
-                                       (20, 64, 32, 33, 33), (9, 16, 48, 7, 1))):
+                                       (20, 64, 32, 33, 33), (9, 16, 48, 7, 1),
+                                       (11, 32, 128, 70, 32), (5, 64, 256, 40, 17))):
     for si, (T, h, r, M, k) in enumerate(shapes):
         inp = make_inputs(T, h, r, M, seed=100 + si)
         res = oracle.route_lowrank(inp.x, inp.R1, inp.R2, k, lib=lib)
