@@ -229,13 +229,15 @@ def test_proposition1_top1_and_counts_on_gpu():
 
 
 def test_graph_capture_replays_match_eager():
-    """Three routing calls captured in one HIP graph; every replay equals the eager result."""
+    """Routing calls of three routes (fused local, expert-resident with 16 chunks, wide at
+    r = 128, k = 20) captured in one HIP graph; every replay equals the eager result."""
     import torch
     from gpu_util import require_gpu, to_dev, announce
     from paper_2609_36301_amd import router
     from paper_2609_36301_amd.inputs import transposed_factors
     require_gpu()
-    shapes = [(700, 512, 32, 4096, 8, 0), (300, 256, 64, 20000, 16, 16)]
+    shapes = [(700, 512, 32, 4096, 8, 0), (300, 256, 64, 20000, 16, 16),
+              (400, 128, 128, 3000, 20, 0)]
     routers, args, eager = [], [], []
     for T, h, r, M, k, chunks in shapes:
         inp = make_inputs(T, h, r, M, seed=T)

@@ -101,6 +101,20 @@ def test_wide_plain_entry_point_matches_ex_and_is_reproducible():
     assert np.array_equal(a[3], oracle.histogram(a[0], M).astype(np.int32))
 
 
+def test_wide_zero_tokens_tie_to_the_smallest_ids():
+    # zero token rows: every logit is 0, so the top k are experts 0 .. k-1 with gates 1/k
+    T, h, r, M, k = 300, 256, 128, 2000, 24
+    inp = make_inputs(T, h, r, M, seed=4)
+    zero_rows = [0, 77, 299]
+    inp.x[zero_rows] = 0
+    idx, gate, topval, _ = route_lowrank(inp, k, tag="wide degenerate")
+    for t in zero_rows:
+        assert np.array_equal(idx[t], np.arange(k, dtype=np.int32))
+        assert np.allclose(gate[t], 1.0 / k, atol=1e-7)
+        assert np.all(topval[t] == 0.0)
+    _check(inp, k, idx, gate, topval, label="zero tokens")
+
+
 def test_wide_empty_batch():
     torch = require_gpu()
     h, r, M, k = 64, 128, 100, 20
