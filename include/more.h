@@ -131,7 +131,7 @@ more_status more_route_lowrank_workspace_size_ex(int64_t T, int32_t h, int32_t r
  * shape with a route that no m_chunks >= 1 selects: a fused route (expert sets with
  * r * M <= 2^18 and M <= 16384: one workgroup per 64 tokens sweeps all experts) or the
  * single-pass route (T >= 4096 and M >= 32768: one screening sweep over all experts after a
- * prescreen of an eighth of them; see more_route_lowrank_ex) or the wide route. */
+ * prescreen of a quarter of them; see more_route_lowrank_ex) or the wide route. */
 more_status more_route_lowrank_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k,
                                     int32_t* m_chunks);
 
