@@ -15,7 +15,7 @@
 // dsort_offsets_kernel derives offsets from the sorted keys: offsets[e] = the first slot whose
 // key is at least e.  Up to 4096 entries (decode-sized batches) one workgroup runs all passes in
 // LDS instead (dsort_small_kernel); with at most 8191 experts one counting pass replaces the
-// radix passes (dsort_whist, dsort_scan, dsort_wscatter).
+// radix passes (dsort_whist, dsort_wscan, dsort_wscatter).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -161,12 +161,13 @@ __global__ __launch_bounds__(kDsThreads) void dsort_scatter_kernel(
 
 // ------------------------------------------------------------------------------ one pass
 // Keys 0 .. M with M + 1 <= kDsWideBins (up to 8191 experts) need one counting pass instead of two
-// radix passes: per-block key counts, the scan of each key's block counts (dsort_scan_kernel
-// with one workgroup per key), and a scatter that also writes the offsets.
+// radix passes: per-block key counts, the scan of each key's block counts (dsort_wscan_kernel),
+// and a scatter that also writes the offsets.  The counts are stored block-major,
+// hist[b * (M + 1) + key], so that every kernel reads and writes whole rows of keys.
 constexpr int kDsWideBins = 8192;
 constexpr int kDsWideBits = 13;
 
-// Key counts of block b: hist[key * nblocks + b].
+// Key counts of block b: hist[b * (M + 1) + key].
 __global__ __launch_bounds__(kDsThreads) void dsort_whist_kernel(const int32_t* __restrict__ idx,
                                                                  int64_t N, int32_t M,
                                                                  int32_t* __restrict__ hist) {
@@ -181,7 +182,58 @@ __global__ __launch_bounds__(kDsThreads) void dsort_whist_kernel(const int32_t* 
         if (g < N) atomicAdd(&cnt[ds_key(idx[g], M)], 1);
     }
     __syncthreads();
-    for (int i = tid; i < D; i += kDsThreads) hist[(int64_t)i * gridDim.x + blockIdx.x] = cnt[i];
+    for (int i = tid; i < D; i += kDsThreads) hist[(int64_t)blockIdx.x * D + i] = cnt[i];
+}
+
+// Keys 64 q .. 64 q + 63 for workgroup q, one per lane; wave w takes the w-th quarter of the
+// nb blocks.  Each thread sums its key's counts over its blocks, the four sums give each wave's
+// start, and a second pass over the same counts replaces them with the exclusive prefix in
+// block order (start of the key's entries of block b among the key's entries); total[key]
+// = the key's entry count.
+__global__ __launch_bounds__(kDsThreads) void dsort_wscan_kernel(int32_t* __restrict__ hist,
+                                                                 int64_t nb, int32_t D,
+                                                                 int32_t* __restrict__ total) {
+    constexpr int NW = kDsThreads / 64;
+    __shared__ int32_t part[NW][64];
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int32_t key = 64 * (int32_t)blockIdx.x + lane;
+    const bool ok = key < D;
+    const int64_t b0 = nb * w / NW, b1 = nb * (w + 1) / NW;
+    int32_t sum = 0;
+    if (ok) {
+        int64_t b = b0;
+        for (; b + 8 <= b1; b += 8) {
+            int32_t v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = hist[(b + j) * D + key];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) sum += v[j];
+        }
+        for (; b < b1; ++b) sum += hist[b * D + key];
+    }
+    part[w][lane] = sum;
+    __syncthreads();
+    int32_t run = 0;
+    for (int ww = 0; ww < w; ++ww) run += part[ww][lane];
+    if (ok && w == NW - 1) total[key] = run + sum;
+    if (ok) {
+        int64_t b = b0;
+        for (; b + 8 <= b1; b += 8) {
+            int32_t v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = hist[(b + j) * D + key];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                hist[(b + j) * D + key] = run;
+                run += v[j];
+            }
+        }
+        for (; b < b1; ++b) {
+            const int32_t v = hist[b * D + key];
+            hist[b * D + key] = run;
+            run += v;
+        }
+    }
 }
 
 // Block b: base[key] = entries with a smaller key (the exclusive scan of the key totals, in LDS;
@@ -233,7 +285,7 @@ __global__ __launch_bounds__(kDsThreads) void dsort_wscatter_kernel(
     if (blockIdx.x == 0)
         for (int e = tid; e <= M; e += kDsThreads) offsets[e] = base[e];
     for (int key = tid; key < D; key += kDsThreads)
-        base[key] += start[(int64_t)key * gridDim.x + blockIdx.x];
+        base[key] += start[(int64_t)blockIdx.x * D + key];
     // the wave's keys, and its count of each key
     const int64_t b0 = (int64_t)blockIdx.x * kDsBlock + (int64_t)w * 64 * WG;
     const uint32_t one = 1u << (16 * (w & 1));
@@ -450,8 +502,8 @@ hipError_t dispatch_launch(const int32_t* idx, int64_t N, int32_t M, int32_t* of
                                                     al((size_t)nblocks * kDsWideBins * 4));
         hipLaunchKernelGGL(dsort_whist_kernel, dim3((unsigned)nblocks), dim3(kDsThreads), 0, st,
                            idx, N, M, hist);
-        hipLaunchKernelGGL(dsort_scan_kernel, dim3((unsigned)(M + 1)), dim3(kDsThreads), 0, st,
-                           hist, nblocks, total);
+        hipLaunchKernelGGL(dsort_wscan_kernel, dim3((unsigned)((M + 1 + 63) / 64)),
+                           dim3(kDsThreads), 0, st, hist, nblocks, (int32_t)(M + 1), total);
         hipLaunchKernelGGL(dsort_wscatter_kernel, dim3((unsigned)nblocks), dim3(kDsThreads), 0, st,
                            idx, N, M, hist, total, sorted, offsets);
         return hipGetLastError();
