@@ -26,6 +26,7 @@
 #include "device_common.h"
 #include "lowrank.h"
 #include "route_device.h"
+#include "wide.h"
 
 namespace more {
 
@@ -36,9 +37,14 @@ constexpr int kFfRing = 3;               // chunks of Wt rows in flight per wave
 
 template <int NT, int K>
 __global__ __launch_bounds__(kFfThreads, 1) void fullrank_fused_kernel(
-    const uint16_t* __restrict__ x, const uint16_t* __restrict__ Wt, int32_t T, int32_t h,
-    int32_t M, int32_t k, int32_t esplits, float* __restrict__ pv, int32_t* __restrict__ pi,
-    int32_t* __restrict__ idx, float* __restrict__ gate, float* __restrict__ topval) {
+    const uint16_t* __restrict__ x, const uint16_t* __restrict__ Wt, int32_t ldw, int32_t wmod,
+    int32_t T, int32_t h, int32_t M, int32_t k, int32_t esplits, float* __restrict__ pv,
+    int32_t* __restrict__ pi, int32_t* __restrict__ idx, float* __restrict__ gate,
+    float* __restrict__ topval) {
+    // Row e of the weights starts at Wt + e ldw and chunk c of the contraction reads its chunk
+    // c mod wmod: ldw = h and wmod = the chunk count for a plain [M][h] matrix; with ldw = h / p
+    // (a multiple of 64) and wmod = ldw / 64 the p chunk groups of x meet the same stored row
+    // (the wide route's three pieces of z against one copy of R2).
     constexpr int BT = 32 * NT;
     static_assert(kFfWaves * BT * K * 8 <= kFfLdsBytes, "merge lists fit the LDS block");
     __shared__ __attribute__((aligned(16))) uint16_t xs[kFfLdsBytes / 2];
@@ -103,13 +109,14 @@ __global__ __launch_bounds__(kFfThreads, 1) void fullrank_fused_kernel(
         q = q < Q ? q : Q - 1;
         const int32_t tile = wt0 + q / nch;
         const int c = q - (q / nch) * nch;
+        const int cw = c - (c / wmod) * wmod;  // the stored chunk
         int32_t e = tile * 32 + n;
         e = e < M ? e : M - 1;  // rows past M: copies of row M - 1, masked in the epilogue
-        const uint16_t* rowp = Wt + (int64_t)e * h;
+        const uint16_t* rowp = Wt + (int64_t)e * ldw;
 #pragma unroll
         for (int s = 0; s < 4; ++s) {
-            int off = 64 * c + 32 * half + 8 * s;
-            off = off < h ? off : 0;
+            int off = 64 * cw + 32 * half + 8 * s;
+            off = off < ldw ? off : 0;
             a[s] = *reinterpret_cast<const u32x4*>(rowp + off);
         }
     };
@@ -302,33 +309,49 @@ bool fullrank_fused_make_plan(int64_t T, int32_t h, int32_t M, int32_t k, FusedF
 
 template <int NT, int K>
 static void launch_ff(const FusedFullrankPlan& p, const uint16_t* x, const uint16_t* Wt,
-                      int64_t T, int32_t h, int32_t M, int32_t k, int32_t* idx, float* gate,
-                      float* topval, void* ws, hipStream_t st) {
+                      int32_t ldw, int32_t wmod, int64_t T, int32_t h, int32_t M, int32_t k,
+                      int32_t* idx, float* gate, float* topval, void* ws, hipStream_t st) {
     const int64_t nb = (T + 32 * NT - 1) / (32 * NT);
     float* pv = static_cast<float*>(ws);
     int32_t* pi = p.esplits > 1 ? reinterpret_cast<int32_t*>(pv + (int64_t)p.esplits * T * K)
                                 : nullptr;
     hipLaunchKernelGGL((fullrank_fused_kernel<NT, K>), dim3((unsigned)(nb * p.esplits)),
-                       dim3(kFfThreads), 0, st, x, Wt, (int32_t)T, h, M, k, p.esplits, pv, pi,
-                       idx, gate, topval);
+                       dim3(kFfThreads), 0, st, x, Wt, ldw, wmod, (int32_t)T, h, M, k,
+                       p.esplits, pv, pi, idx, gate, topval);
     if (p.esplits > 1)
         hipLaunchKernelGGL((fullrank_merge_kernel<K>), dim3((unsigned)((T + 255) / 256)),
                            dim3(256), 0, st, pv, pi, (int32_t)T, k, p.esplits, idx, gate, topval);
 }
 
-hipError_t fullrank_fused_launch(const FusedFullrankPlan& p, const uint16_t* x, const uint16_t* Wt,
-                                 int64_t T, int32_t h, int32_t M, int32_t k, int32_t* idx,
-                                 float* gate, float* topval, void* workspace, hipStream_t st) {
-#define MORE_FF(NT_, K_)                                                                 \
-    if (p.NT == NT_ && p.K == K_) {                                                      \
-        launch_ff<NT_, K_>(p, x, Wt, T, h, M, k, idx, gate, topval, workspace, st);       \
-        return hipGetLastError();                                                        \
+static hipError_t launch_ff_any(const FusedFullrankPlan& p, const uint16_t* x,
+                                const uint16_t* Wt, int32_t ldw, int32_t wmod, int64_t T,
+                                int32_t h, int32_t M, int32_t k, int32_t* idx, float* gate,
+                                float* topval, void* workspace, hipStream_t st) {
+#define MORE_FF(NT_, K_)                                                                   \
+    if (p.NT == NT_ && p.K == K_) {                                                        \
+        launch_ff<NT_, K_>(p, x, Wt, ldw, wmod, T, h, M, k, idx, gate, topval, workspace, st); \
+        return hipGetLastError();                                                          \
     }
     MORE_FF(4, 1) MORE_FF(4, 2) MORE_FF(4, 4)
     MORE_FF(2, 1) MORE_FF(2, 2) MORE_FF(2, 4) MORE_FF(2, 8)
     MORE_FF(1, 1) MORE_FF(1, 2) MORE_FF(1, 4) MORE_FF(1, 8) MORE_FF(1, 16) MORE_FF(1, 32)
 #undef MORE_FF
     return hipErrorInvalidValue;
+}
+
+hipError_t fullrank_fused_launch(const FusedFullrankPlan& p, const uint16_t* x, const uint16_t* Wt,
+                                 int64_t T, int32_t h, int32_t M, int32_t k, int32_t* idx,
+                                 float* gate, float* topval, void* workspace, hipStream_t st) {
+    return launch_ff_any(p, x, Wt, h, (h + 63) / 64, T, h, M, k, idx, gate, topval, workspace,
+                         st);
+}
+
+hipError_t fullrank_fused_launch_periodic(const FusedFullrankPlan& p, const uint16_t* x,
+                                          const uint16_t* Wt, int32_t ldw, int64_t T, int32_t h,
+                                          int32_t M, int32_t k, int32_t* idx, float* gate,
+                                          float* topval, void* workspace, hipStream_t st) {
+    if (ldw < 64 || ldw % 64 != 0 || h % ldw != 0) return hipErrorInvalidValue;
+    return launch_ff_any(p, x, Wt, ldw, ldw / 64, T, h, M, k, idx, gate, topval, workspace, st);
 }
 
 }  // namespace more

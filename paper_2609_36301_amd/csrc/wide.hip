@@ -7,8 +7,9 @@
 //      rank columns (a block's columns are independent rows of the contraction, so z is the
 //      same as from one pass over all r columns);
 //   2. z is split into three bfloat16 pieces per element whose sum is z exactly, stored as the
-//      rows [z_hi | z_mid | z_lo] of a 3r-wide operand, and the rows of R2t are stacked three
-//      times into a matching [M][3r] operand;
+//      rows [z_hi | z_mid | z_lo] of a 3r-wide operand; when r is not a multiple of 64 the rows
+//      of R2t are stacked three times into a matching [M][3r] operand, otherwise the sweep
+//      reads each 64-wide chunk of R2t for all three pieces;
 //   3. the fused standard router sweeps that pair: its fp32 logits are sums of exact bf16
 //      products, i.e. the fp32 dot products of the fp32 z with the bfloat16 expert rows up to
 //      the summation order, and it returns their exact top k (ties to the smaller id), the
@@ -119,8 +120,9 @@ bool wide_make_plan(int64_t T, int32_t h, int32_t r, int32_t M, int32_t k, WideP
     o += wide_align(zscr);
     q.off_zs = o;
     o += wide_align((size_t)T * 3 * r * sizeof(uint16_t));
+    q.stack = r % 64 != 0;
     q.off_w3 = o;
-    o += wide_align((size_t)M * 3 * r * sizeof(uint16_t));
+    if (q.stack) o += wide_align((size_t)M * 3 * r * sizeof(uint16_t));
     q.off_ff = o;
     o += wide_align(q.ff.workspace_bytes);
     q.workspace_bytes = o;
@@ -143,12 +145,15 @@ hipError_t wide_launch(const WidePlan& p, const uint16_t* x, const uint16_t* R1t
     uint16_t* w3 = reinterpret_cast<uint16_t*>(ws + p.off_w3);
     hipLaunchKernelGGL(wide_split_kernel, dim3(wide_grid(T * r)), dim3(kWideThreads), 0, st, z,
                        T, r, zs);
+    void* ffws = p.ff.workspace_bytes > 0 ? ws + p.off_ff : nullptr;
+    if (!p.stack)  // r a multiple of 64: the three pieces read the one copy of R2t
+        return fullrank_fused_launch_periodic(p.ff, zs, R2t, r, T, 3 * r, M, k, idx, gate,
+                                              topval, ffws, st);
     hipLaunchKernelGGL(wide_stack_kernel, dim3(wide_grid((int64_t)M * 3 * (r / 8))),
                        dim3(kWideThreads), 0, st, R2t, M, r, w3);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return fullrank_fused_launch(p.ff, zs, w3, T, 3 * r, M, k, idx, gate, topval,
-                                 p.ff.workspace_bytes > 0 ? ws + p.off_ff : nullptr, st);
+    return fullrank_fused_launch(p.ff, zs, w3, T, 3 * r, M, k, idx, gate, topval, ffws, st);
 }
 
 }  // namespace more
