@@ -175,6 +175,24 @@ def test_routes_for_the_paper_shapes(lib):
     assert lib.more_route_lowrank_route(100, 64, 32, 1000, 4, None) == _lib.ERR_INVALID_ARG
 
 
+def test_wide_route_workspace_sizes(lib):
+    # the wide route needs z, its three-piece split and (r not a multiple of 64) the stacked
+    # expert rows: more bytes for more tokens, for more experts when stacked, and at least z
+    n = ctypes.c_size_t(0)
+    sizes = {}
+    for T, h, r, M, k in ((1000, 256, 128, 3000, 8), (2000, 256, 128, 3000, 8),
+                          (1000, 256, 80, 3000, 8), (1000, 256, 80, 6000, 8),
+                          (1000, 256, 64, 3000, 20)):
+        assert lib.more_route_lowrank_workspace_size(T, h, r, M, k, ctypes.byref(n)) == _lib.OK
+        assert n.value >= T * r * 4 + T * 3 * r * 2
+        sizes[(T, r, M, k)] = n.value
+    assert sizes[(2000, 128, 3000, 8)] > sizes[(1000, 128, 3000, 8)]
+    assert sizes[(1000, 80, 6000, 8)] - sizes[(1000, 80, 3000, 8)] >= 3000 * 3 * 80 * 2
+    # one byte short of the size query: refused before any launch
+    assert lowrank(lib, T=1000, h=256, r=128, M=3000, k=8, ws=FAKE,
+                   wsb=sizes[(1000, 128, 3000, 8)] - 1) == _lib.ERR_WORKSPACE
+
+
 def test_fullrank_validation(lib):
     def call(**kw):
         a = dict(x=FAKE, W=FAKE, T=10, h=64, M=100, k=4, bits=32, idx=FAKE, gate=FAKE, ws=None,
