@@ -1,6 +1,7 @@
 """The no-allocation entry point through the C ABI (marked `gpu`): two calls in a row, the
-second on a smaller input (single-pass route, then resident route), each bitwise equal to more_route_lowrank with a torch-allocated
-workspace, and in oracle parity."""
+second on a smaller input (single-pass route, then resident route), then a call on the wide
+route, each bitwise equal to more_route_lowrank with a torch-allocated workspace, and in
+oracle parity."""
 import ctypes
 
 import numpy as np
@@ -64,3 +65,37 @@ def test_noalloc_matches_the_workspace_entry_point_on_two_calls():
         print("[parity] noalloc %s %s" % (shape, rep), flush=True)
         assert rep.ok(), str(rep)
         del args, ws
+
+
+def test_noalloc_wide_route_matches_the_workspace_entry_point():
+    # r = 128 with k = 20 takes the wide route; its z, split and list buffers come from the
+    # same static scratch, which still holds the previous calls' data
+    import torch
+    from gpu_util import announce, require_gpu, to_dev
+    from paper_2609_36301_amd import _lib, router
+    require_gpu()
+    lib = _lib.load()
+    shape = (600, 256, 128, 3000, 20)
+    T, h, r, M, k = shape
+    assert router.lowrank_route(T, h, r, M, k) == "wide"
+    inp = make_inputs(T, h, r, M, seed=17)
+    R1t, R2t = transposed_factors(inp)
+    args = (to_dev(inp.x), to_dev(R1t), to_dev(R2t), shape)
+    n = ctypes.c_size_t(0)
+    assert lib.more_route_lowrank_workspace_size(T, h, r, M, k, ctypes.byref(n)) == _lib.OK
+    assert 0 < n.value <= _lib.NOALLOC_SCRATCH_BYTES
+    announce("noalloc wide T=%d h=%d r=%d M=%d k=%d" % shape)
+    st, got = _run(lib, "noalloc", args, T, k, M)
+    assert st == _lib.OK, _lib.status_string(st)
+    torch.cuda.synchronize()
+    got = [t.cpu().numpy() for t in got]
+    ws = torch.empty(n.value, dtype=torch.uint8, device="cuda")
+    st, want = _run(lib, "ws", args, T, k, M, ws, n.value)
+    assert st == _lib.OK, _lib.status_string(st)
+    torch.cuda.synchronize()
+    want = [t.cpu().numpy() for t in want]
+    for a, b in zip(got, want):
+        assert np.array_equal(a, b)
+    rep = parity.evaluate(inp.x, inp.R1, inp.R2, k, got[0], got[1], got[2])
+    print("[parity] noalloc wide %s %s" % (shape, rep), flush=True)
+    assert rep.ok(), str(rep)
