@@ -886,7 +886,12 @@ __global__ __launch_bounds__(256) void bwd_dr1_kernel(const uint16_t* __restrict
     constexpr int R = 16 * RC, RB = (R + 31) / 32;
     constexpr int PIECES = kBwR1Tok * kBwR1Cols / 8;  // 1024
     constexpr int PPT = PIECES / 256;
+    // the stage's dz columns: rows 0 .. 2R - 1 of dzT (hi, then lo), kBwR1Tok tokens each,
+    // staged beside x so that the A operands come from LDS
+    constexpr int DZP = kBwR1Tok + 8;
+    constexpr int DPT = 2 * R * (kBwR1Tok / 8) / 256;  // 16-byte pieces per thread (= RC)
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][kBwR1Tok * kBwR1Pitch];
+    __shared__ __attribute__((aligned(16))) uint16_t dzs[2][2 * R * DZP];
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = tid >> 6;
@@ -898,9 +903,15 @@ __global__ __launch_bounds__(256) void bwd_dr1_kernel(const uint16_t* __restrict
     const int64_t s0 = Ts * split / splits, s1 = Ts * (split + 1) / splits;
     const int nst = (int)(s1 - s0);
     const int64_t c0 = (int64_t)cb * kBwR1Cols;
-    u32x4 rg[PPT];
+    u32x4 rg[PPT], dg[DPT];
     auto gload = [&](int st) __attribute__((always_inline)) {
         const int64_t tok0 = (s0 + st) * kBwR1Tok;
+#pragma unroll
+        for (int i = 0; i < DPT; ++i) {  // piece p: dzT row p / 8, tokens tok0 + 8 (p % 8) + 0..7
+            const int p = tid + i * 256;
+            dg[i] = *reinterpret_cast<const u32x4*>(dzT + (int64_t)(p >> 3) * Tp + tok0 +
+                                                    8 * (p & 7));
+        }
 #pragma unroll
         for (int i = 0; i < PPT; ++i) {
             const int p = tid + i * 256;
@@ -912,6 +923,11 @@ __global__ __launch_bounds__(256) void bwd_dr1_kernel(const uint16_t* __restrict
         }
     };
     auto stash = [&](int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < DPT; ++i) {
+            const int p = tid + i * 256;
+            *reinterpret_cast<u32x4*>(&dzs[buf][(p >> 3) * DZP + 8 * (p & 7)]) = dg[i];
+        }
 #pragma unroll
         for (int i = 0; i < PPT; ++i) {
             const int p = tid + i * 256;
@@ -929,7 +945,6 @@ __global__ __launch_bounds__(256) void bwd_dr1_kernel(const uint16_t* __restrict
         __syncthreads();
         for (int st = 0; st < nst; ++st) {
             const int buf = st & 1;
-            const int64_t tok0 = (s0 + st) * kBwR1Tok;
 #pragma unroll
             for (int ks = 0; ks < kBwR1Tok / 16; ++ks) {
                 bf16x8 bx;
@@ -941,9 +956,11 @@ __global__ __launch_bounds__(256) void bwd_dr1_kernel(const uint16_t* __restrict
                 for (int q = 0; q < RB; ++q) {
                     int jr = 32 * q + n;
                     jr = jr < R ? jr : R - 1;  // rows past r: never stored
-                    const int64_t off = tok0 + 16 * ks + 8 * half;
-                    const bf16x8 ahv = load_bf16x8(dzT + (int64_t)jr * Tp + off);
-                    const bf16x8 alv = load_bf16x8(dzT + ((int64_t)R + jr) * Tp + off);
+                    const int off = 16 * ks + 8 * half;
+                    const bf16x8 ahv =
+                        *reinterpret_cast<const bf16x8*>(&dzs[buf][jr * DZP + off]);
+                    const bf16x8 alv =
+                        *reinterpret_cast<const bf16x8*>(&dzs[buf][(R + jr) * DZP + off]);
                     acc[q] = mfma_32x32x16(ahv, bx, acc[q]);
                     acc[q] = mfma_32x32x16(alv, bx, acc[q]);
                 }
