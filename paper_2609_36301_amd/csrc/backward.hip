@@ -871,9 +871,9 @@ __global__ __launch_bounds__(256) void bwd_dx_kernel(const uint16_t* __restrict_
 
 // ------------------------------------------------------------------------------ dR1
 // part[s][j][c] = sum over the tokens of split s of dz[t][j] x[t][c]: a workgroup of 4 waves
-// takes 128 columns (wave w: columns 32 w ..) and stages 64-token slices of x through LDS; the
-// A operands are dz^T rows (hi and lo) read from dzT, the B operands eight x values of one
-// column read down the LDS slice.
+// takes 128 columns (wave w: columns 32 w ..) and stages 64-token slices of x and of dzT's rows
+// (hi and lo) through LDS, one slice ahead in registers; the A operands are dz^T rows read from
+// the staged slice, the B operands eight x values of one column read down the LDS slice.
 constexpr int kBwR1Tok = 64;
 constexpr int kBwR1Cols = 128;
 constexpr int kBwR1Pitch = kBwR1Cols + 8;
